@@ -1,0 +1,71 @@
+"""Byte/FLOP accounting pinned to the values printed in Tables 1-2 (Section 2.2).
+
+The golden fixture holds the printed numbers; each reproduction must agree to one
+unit in the last printed digit. Then the sparse formulas must reduce to the dense
+ones at full density, and the per-config totals used by the benchmark are checked
+against their closed forms.
+"""
+import json
+import os
+
+import pytest
+
+from paper_2310_17157_amd import accounting as A
+from synth import get_config
+
+GOLD = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "paper_tables_1_2.json")))
+D175 = 12288
+A100_FLOPS = 312e12
+A100_BW_TBS = 2.0
+NGPU = 8
+GiB = 2 ** 30
+
+
+def _close(x, printed, unit):
+    assert abs(x - printed) <= unit + 1e-12, (x, printed)
+
+
+def test_table2_attention_and_mlp_per_layer():
+    t2 = GOLD["table2"]
+    att_f = A.dense_attention_flops(D175)
+    mlp_f = A.dense_mlp_flops(D175, 4 * D175)
+    att_b = A.dense_attention_bytes(D175, 2)
+    mlp_b = A.dense_mlp_bytes(D175, 4 * D175, 2)
+    _close(att_f / 1e9, t2["attention"]["gflops"], 0.01)
+    _close(mlp_f / 1e9, t2["mlp"]["gflops"], 0.01)
+    _close(att_b / GiB, t2["attention"]["io_gb"], 0.01)
+    _close(mlp_b / GiB, t2["mlp"]["io_gb"], 0.01)
+    _close(att_f / (NGPU * A100_FLOPS) * 1e3, t2["attention"]["compute_ms"], 1e-5)
+    _close(mlp_f / (NGPU * A100_FLOPS) * 1e3, t2["mlp"]["compute_ms"], 1e-5)
+    _close(att_b / GiB / (NGPU * A100_BW_TBS * 1e3) * 1e3, t2["attention"]["io_ms"], 0.01)
+    _close(mlp_b / GiB / (NGPU * A100_BW_TBS * 1e3) * 1e3, t2["mlp"]["io_ms"], 0.01)
+    # The MLP is 2/3 of the layer's I/O (Section 2.2).
+    assert mlp_b / (mlp_b + att_b) == pytest.approx(2 / 3)
+
+
+def test_table1_prompt_vs_generation():
+    t1 = GOLD["table1"]
+    layer_b = A.dense_attention_bytes(D175, 2) + A.dense_mlp_bytes(D175, 4 * D175, 2)
+    model_b = 96 * layer_b
+    _close(model_b / GiB, t1["prompt_io_gb"], 10)                 # 2 significant figures
+    _close(128 * model_b / 2 ** 40, t1["generate_io_tb"], 1)
+    _close(t1["prompt_tflops"] * 1e12 / (NGPU * A100_FLOPS) * 1e3, t1["compute_ms"], 0.01)
+    _close(t1["prompt_io_gb"] / (NGPU * A100_BW_TBS) , t1["prompt_io_ms"], 0.1)
+    _close(t1["generate_io_tb"] * 1e3 / (NGPU * A100_BW_TBS), t1["generate_io_ms"], 100)
+
+
+def test_sparse_formulas_reduce_to_dense_at_full_density():
+    d, N, H, dh = 1024, 4096, 8, 128
+    assert A.sparse_mlp_bytes(d, N, 2) == A.dense_mlp_bytes(d, N, 2)
+    assert A.sparse_attn_weight_bytes(d, dh, H, 2) == A.dense_attention_bytes(d, 2)
+
+
+def test_opt175b_batch1_totals():
+    b = A.layer_bytes(get_config("opt175b_b1"))
+    d, dh, L = 12288, 128, 2048
+    assert b.mlp == 2457 * 2 * d * 2
+    assert b.attn_w == 32 * 4 * dh * d * 2
+    assert b.kv == 32 * 2 * L * dh * 2
+    assert b.pred == (d * 1000 + 1000 * 96 + d * 1000 + 1000 * 49152) * 2
+    assert round(b.block / 1e6, 2) == 556.97
+    assert round(b.total / 1e6, 1) == 704.6
