@@ -1,0 +1,233 @@
+/*
+ * dv.h — C ABI of the Deja Vu decode hot path for AMD Instinct MI355X (gfx950).
+ *
+ * Deja Vu (Liu et al., ICML 2023, arXiv 2310.17157) skips, for each generated
+ * token, the attention heads and MLP neurons that a cheap predictor deems
+ * irrelevant to that token ("contextual sparsity"). This library implements the
+ * decode-time hot path on one GPU:
+ *   - the low-rank sparsity predictors (two thin GEMVs, then top-k or threshold
+ *     selection): dv_predict_mlp, dv_predict_heads;
+ *   - the sparsified MLP of Eq. (1): dv_sparse_mlp;
+ *   - the sparsified multi-head attention of Eq. (2) over a KV cache:
+ *     dv_sparse_attn;
+ *   - one whole decoder layer with predictors, layer norms and residuals
+ *     (Section 4.3): dv_sparse_block.
+ *
+ * Conventions shared by every entry point
+ *   Memory.   Every array pointer is a DEVICE pointer owned by the caller, except
+ *             dv_kv.pos, which is a HOST array. The library never allocates or
+ *             frees memory on these paths and keeps no per-call state; scratch
+ *             space is the caller's workspace `ws` of at least the size returned
+ *             by the matching *_workspace_bytes query (256-byte aligned). Calls
+ *             that share a workspace must be ordered on one stream.
+ *   Layout.   Row-major. A weight row is 16-byte aligned: base pointers must be
+ *             16-byte aligned and d (and r for predictors) a multiple of 8 for
+ *             fp16 or 4 for fp32 elements.
+ *   Types.    Weights and predictor factors are fp16 or fp32 (dv_dtype); biases,
+ *             layer-norm parameters, hidden states and outputs are fp32; index
+ *             sets are int32. Arithmetic accumulates in fp32.
+ *   Streams.  `stream` is a hipStream_t (NULL = the null stream). Each call
+ *             validates its arguments on the host, synchronously, before any
+ *             device work; on success it enqueues its kernels and returns DV_OK
+ *             without waiting. Results are valid in stream order.
+ *   Errors.   A failed check returns its dv_status and enqueues nothing. A failed
+ *             launch returns DV_ERR_HIP. No C++ exception crosses the ABI.
+ *   Sets.     An index set is int32, strictly ascending, within [0, n). Selection
+ *             outputs always satisfy this. Consumers trust their input sets; an
+ *             out-of-range index is clamped into range (no fault, unspecified
+ *             result) unless DV_VALIDATE is set, in which case the set is checked
+ *             on the device first, the call waits for that check, and a bad set
+ *             returns DV_ERR_INDEX with no compute enqueued.
+ *   Outputs.  Overwritten, never accumulated. Inputs and outputs must not alias.
+ *   Numerics. All reductions run in a fixed order: two identical calls produce
+ *             bitwise identical outputs (DV_DETERMINISTIC is always honoured).
+ */
+#ifndef DV_H
+#define DV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DV_ABI_VERSION 1
+
+typedef enum dv_status {
+  DV_OK = 0,
+  DV_ERR_NULL = 1,        /* a required pointer is NULL */
+  DV_ERR_SHAPE = 2,       /* inconsistent or out-of-range sizes (k > n, pos >= cap, ...) */
+  DV_ERR_DTYPE = 3,       /* unknown dv_dtype */
+  DV_ERR_ALIGN = 4,       /* a pointer or row is not 16-byte aligned */
+  DV_ERR_WORKSPACE = 5,   /* workspace NULL, too small or not 256-byte aligned */
+  DV_ERR_INDEX = 6,       /* DV_VALIDATE only: an index set is not ascending within [0, n) */
+  DV_ERR_HIP = 7,         /* a HIP runtime call or kernel launch failed */
+  DV_ERR_UNSUPPORTED = 8, /* a valid request outside what this build implements */
+  DV_ERR_ARG = 9          /* an invalid mode or flag value */
+} dv_status;
+
+typedef enum dv_dtype { DV_F32 = 0, DV_F16 = 1 } dv_dtype;
+
+/* Selection rule (Section 4.1; Algorithm 1 labels s >= t as positive). */
+enum { DV_SELECT_TOPK = 0, DV_SELECT_THRESHOLD = 1 };
+/* Which hidden state feeds the neuron predictor in dv_sparse_block (Section 4.3):
+ * LOOKAHEAD = LN1(y), the attention block's input, so the prediction can run ahead
+ * of the attention; SEQUENTIAL = LN2(y~), the MLP block's own input. */
+enum { DV_LOOKAHEAD = 0, DV_SEQUENTIAL = 1 };
+/* Batch > 1 (Section 5.2, Appendix C.1): UNION runs every sequence on the union of
+ * the batch's neuron sets (one skinny GEMM over the union's rows); MASKED gives each
+ * sequence only its own neurons. */
+enum { DV_MLP_UNION = 0, DV_MLP_MASKED = 1 };
+/* Flags. */
+enum { DV_DETERMINISTIC = 1u << 0, DV_VALIDATE = 1u << 1 };
+
+/* Two-layer low-rank sparsity predictor (Section 4.1 "Design", Section 4.2
+ * "Approach"): scores s = (x A) B, A = AT^T (d x r), B = BT^T (r x n_out); no hidden
+ * activation and no bias. n_out is the neuron count N (MLP) or the head count H. */
+typedef struct dv_predictor {
+  int32_t d;          /* input width */
+  int32_t r;          /* rank (hidden width of the predictor) */
+  int32_t n_out;      /* number of scored items */
+  int32_t wtype;      /* dv_dtype of AT and BT */
+  const void *AT;     /* [r][d]; row m = column m of A */
+  const void *BT;     /* [n_out][r]; row i = column i of B */
+} dv_predictor;
+
+/* ReLU MLP of Eq. (1) with its weights stored transposed (Section 4.4 "Memory
+ * coalescing"): neuron i's input weights W^1_i and output weights W^2_i are each one
+ * contiguous row. */
+typedef struct dv_mlp {
+  int32_t d;          /* model width */
+  int32_t n;          /* neurons N */
+  int32_t wtype;      /* dv_dtype of W1T and W2T */
+  int32_t reserved;   /* must be 0 */
+  const void *W1T;    /* [n][d]; row i = W^1_i */
+  const float *b1;    /* [n] or NULL */
+  const void *W2T;    /* [n][d]; row i = W^2_i */
+  const float *b2;    /* [d] or NULL; added once */
+} dv_mlp;
+
+/* Multi-head attention of Eq. (2): per head i, W^Q_i, W^K_i, W^V_i (d x dh) stored as
+ * the row block [i*dh, (i+1)*dh) of Wq/Wk/Wv (the nn.Linear layout), and W^O_i
+ * (dh x d) as the same row block of WoT. */
+typedef struct dv_attn {
+  int32_t d;          /* model width */
+  int32_t H;          /* heads */
+  int32_t dh;         /* head width */
+  int32_t wtype;      /* dv_dtype of Wq, Wk, Wv, WoT */
+  const void *Wq, *Wk, *Wv;        /* [H*dh][d] */
+  const float *bq, *bk, *bv;       /* [H*dh] or NULL */
+  const void *WoT;                 /* [H*dh][d] */
+  const float *bo;                 /* [d] or NULL; added once */
+} dv_attn;
+
+/* KV cache: the keys X W^K_i and values X W^V_i of the attended tokens, per head. */
+typedef struct dv_kv {
+  int32_t B;          /* sequences */
+  int32_t H;          /* heads (= dv_attn.H) */
+  int32_t dh;         /* head width (= dv_attn.dh) */
+  int32_t cap;        /* rows per (sequence, head) */
+  int32_t ktype;      /* dv_dtype of K and V */
+  int32_t reserved;   /* must be 0 */
+  void *K, *V;        /* [B][H][cap][dh], device */
+  const int32_t *pos; /* HOST [B]: row of the current token; attention covers rows 0..pos */
+} dv_kv;
+
+/* Pre-layer-norm parameters (biased variance). g1 == NULL means no normalisation
+ * before the attention block; g2 == NULL none before the MLP. be* may be NULL (0). */
+typedef struct dv_ln {
+  const float *g1, *be1, *g2, *be2;   /* [d] each */
+  float eps;
+} dv_ln;
+
+const char *dv_status_string(int32_t status);
+int32_t dv_abi_version(void);
+
+/* Per-launch timing (tracing aid). While armed on the calling thread, every entry point
+ * called on that thread records, on its stream, events[2*i] just before and
+ * events[2*i+1] just after its i-th timed kernel launch (for i < n_pairs), where events
+ * are hipEvent_t handles created by the caller. A launch is timed if `only` is NULL or
+ * equals its label. The number of launches of the latest call is stored in
+ * *n_launched; dv_launch_label(i) names its i-th launch. Pass events == NULL to
+ * disarm. Returns DV_ERR_SHAPE if n_pairs < 0. */
+dv_status dv_set_launch_events(void **events, int32_t n_pairs, int32_t *n_launched, const char *only);
+const char *dv_launch_label(int32_t i);
+
+/* ---------------------------------------------------------------- predictors
+ * dv_predict_mlp / dv_predict_heads: S = select(s), s = (x A) B (Sections 4.1-4.2).
+ *   x      [B][d] fp32 device: the predictor input (already normalised, if any).
+ *   mode   DV_SELECT_TOPK: the k highest scores, ties to the lower index;
+ *          DV_SELECT_THRESHOLD: every i with s_i >= thresh (k ignored).
+ *   idx    [B][cap_idx] int32 device, out: each sequence's set, ascending. Top-k
+ *          needs cap_idx >= k. Threshold mode writes the first cap_idx members.
+ *   count  [B] int32 device, out (may be NULL for top-k): |S| (threshold mode: the
+ *          full count, which may exceed cap_idx).
+ *   scores [B][n_out] fp32 device, out, or NULL: the raw scores s.
+ * Limits: n_out <= 65536 for selection. Both functions compute the same thing;
+ * they differ only in launch tuning for a large (neurons) or small (heads) n_out.
+ */
+size_t dv_predict_workspace_bytes(const dv_predictor *p, int32_t B);
+dv_status dv_predict_mlp(const dv_predictor *p, const float *x, int32_t B, int32_t mode,
+                         int32_t k, float thresh, int32_t *idx, int32_t cap_idx, int32_t *count,
+                         float *scores, void *ws, size_t ws_bytes, uint32_t flags, void *stream);
+dv_status dv_predict_heads(const dv_predictor *p, const float *x, int32_t B, int32_t mode,
+                           int32_t k, float thresh, int32_t *idx, int32_t cap_idx, int32_t *count,
+                           float *scores, void *ws, size_t ws_bytes, uint32_t flags, void *stream);
+
+/* --------------------------------------------------------------- sparse MLP
+ * dv_sparse_mlp: out[b] = MLP_S(x[b]) = b2 + sum_{i in S} ReLU(x[b] . W^1_i + b1_i) W^2_i
+ * (Eq. (1)), without any residual.
+ *   idx          device int32: idx_per_seq == 0: one set idx[n_idx] shared by all B
+ *                sequences; idx_per_seq == 1: idx[B][n_idx], one set per sequence.
+ *   batch_mode   with per-sequence sets and B > 1: DV_MLP_UNION or DV_MLP_MASKED.
+ * Each selected row of W1T and W2T is read from HBM once per call, whatever B is.
+ */
+size_t dv_sparse_mlp_workspace_bytes(const dv_mlp *m, int32_t B, int32_t n_idx, int32_t idx_per_seq);
+dv_status dv_sparse_mlp(const dv_mlp *m, const float *x, int32_t B, const int32_t *idx,
+                        int32_t n_idx, int32_t idx_per_seq, int32_t batch_mode, float *out,
+                        void *ws, size_t ws_bytes, uint32_t flags, void *stream);
+
+/* ---------------------------------------------------------- sparse attention
+ * dv_sparse_attn: out[b] = bo + sum_{i in S_A^b} H_i(x[b]) W^O_i (Eq. (2) with a
+ * `scale` on the logits; scale = 1 is Eq. (2) literally, 1/sqrt(dh) is the usual
+ * convention), without any residual.
+ *   heads   [B][n_heads] int32 device: each sequence's head set S_A^b.
+ *   kv      the cache; for every b and every i in S_A^b the fresh key and value of
+ *           x[b] are written at row pos[b] (Section 4.2: keys and values only for
+ *           the selected heads; other heads' rows are left untouched), then head i
+ *           attends over rows 0..pos[b].
+ */
+size_t dv_sparse_attn_workspace_bytes(const dv_attn *a, const dv_kv *kv, int32_t B, int32_t n_heads);
+dv_status dv_sparse_attn(const dv_attn *a, const float *x, int32_t B, const dv_kv *kv,
+                         const int32_t *heads, int32_t n_heads, float scale, float *out,
+                         void *ws, size_t ws_bytes, uint32_t flags, void *stream);
+
+/* ------------------------------------------------------------- decoder layer
+ * dv_sparse_block: one decoder layer for one token per sequence (Section 4.3):
+ *   S_A  = top-k_heads(SP_A(LN1(y)))
+ *   y~   = y + MHA_{S_A}(LN1(y))
+ *   S_M  = top-k_mlp(SP_M(LN1(y)))   (mode DV_LOOKAHEAD)
+ *        = top-k_mlp(SP_M(LN2(y~)))  (mode DV_SEQUENTIAL)
+ *   y^   = y~ + MLP_{S_M}(LN2(y~))   -> x_out
+ *   pa, pm      head and neuron predictors (pa->n_out = H, pm->n_out = N).
+ *   heads_out   [B][k_heads] or NULL: S_A per sequence, ascending.
+ *   idx_out     [B][k_mlp] or NULL: S_M per sequence, ascending.
+ *   batch_mode  B > 1: DV_MLP_UNION or DV_MLP_MASKED (see above).
+ * The KV cache is updated as in dv_sparse_attn.
+ */
+size_t dv_sparse_block_workspace_bytes(const dv_attn *a, const dv_mlp *m, const dv_predictor *pa,
+                                       const dv_predictor *pm, const dv_kv *kv, int32_t B,
+                                       int32_t k_heads, int32_t k_mlp);
+dv_status dv_sparse_block(const dv_attn *a, const dv_mlp *m, const dv_predictor *pa,
+                          const dv_predictor *pm, const dv_ln *ln, const dv_kv *kv,
+                          const float *x_in, float *x_out, int32_t B, int32_t k_heads,
+                          int32_t k_mlp, int32_t mode, int32_t batch_mode, float scale,
+                          int32_t *heads_out, int32_t *idx_out, void *ws, size_t ws_bytes,
+                          uint32_t flags, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DV_H */

@@ -1,0 +1,373 @@
+"""ctypes binding of libdejavu_hip.so (the C ABI declared in include/dv.h).
+
+Argument marshalling only: torch tensors supply device memory and the current
+stream; every step of the computation runs in the library's HIP kernels. The
+library is loaded from this package directory and nothing else is tried: if it is
+missing, loading raises (there is no CPU fallback).
+
+Entry points keep the C names: dv_predict_mlp, dv_predict_heads, dv_sparse_mlp,
+dv_sparse_attn, dv_sparse_block. Each takes the tensors, allocates outputs and the
+workspace with torch when they are not given, calls the C function on the current
+stream and raises DvError on a non-zero status.
+"""
+import ctypes
+import os
+from ctypes import POINTER, c_char_p, c_float, c_int32, c_size_t, c_uint32, c_void_p
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdejavu_hip.so")
+
+DV_F32, DV_F16 = 0, 1
+DV_SELECT_TOPK, DV_SELECT_THRESHOLD = 0, 1
+DV_LOOKAHEAD, DV_SEQUENTIAL = 0, 1
+DV_MLP_UNION, DV_MLP_MASKED = 0, 1
+DV_DETERMINISTIC, DV_VALIDATE = 1, 2
+
+STATUS = {0: "DV_OK", 1: "DV_ERR_NULL", 2: "DV_ERR_SHAPE", 3: "DV_ERR_DTYPE", 4: "DV_ERR_ALIGN",
+          5: "DV_ERR_WORKSPACE", 6: "DV_ERR_INDEX", 7: "DV_ERR_HIP", 8: "DV_ERR_UNSUPPORTED",
+          9: "DV_ERR_ARG"}
+
+
+class DvError(RuntimeError):
+    def __init__(self, fn, status, msg):
+        super().__init__(f"{fn}: {STATUS.get(status, status)} ({msg})")
+        self.status = status
+
+
+class CPredictor(ctypes.Structure):
+    _fields_ = [("d", c_int32), ("r", c_int32), ("n_out", c_int32), ("wtype", c_int32),
+                ("AT", c_void_p), ("BT", c_void_p)]
+
+
+class CMlp(ctypes.Structure):
+    _fields_ = [("d", c_int32), ("n", c_int32), ("wtype", c_int32), ("reserved", c_int32),
+                ("W1T", c_void_p), ("b1", c_void_p), ("W2T", c_void_p), ("b2", c_void_p)]
+
+
+class CAttn(ctypes.Structure):
+    _fields_ = [("d", c_int32), ("H", c_int32), ("dh", c_int32), ("wtype", c_int32),
+                ("Wq", c_void_p), ("Wk", c_void_p), ("Wv", c_void_p),
+                ("bq", c_void_p), ("bk", c_void_p), ("bv", c_void_p),
+                ("WoT", c_void_p), ("bo", c_void_p)]
+
+
+class CKV(ctypes.Structure):
+    _fields_ = [("B", c_int32), ("H", c_int32), ("dh", c_int32), ("cap", c_int32),
+                ("ktype", c_int32), ("reserved", c_int32), ("K", c_void_p), ("V", c_void_p),
+                ("pos", POINTER(c_int32))]
+
+
+class CLN(ctypes.Structure):
+    _fields_ = [("g1", c_void_p), ("be1", c_void_p), ("g2", c_void_p), ("be2", c_void_p),
+                ("eps", c_float)]
+
+
+_PRED_ARGS = [POINTER(CPredictor), c_void_p, c_int32, c_int32, c_int32, c_float, c_void_p, c_int32,
+              c_void_p, c_void_p, c_void_p, c_size_t, c_uint32, c_void_p]
+_SIGS = {
+    "dv_status_string": (c_char_p, [c_int32]),
+    "dv_set_launch_events": (c_int32, [POINTER(c_void_p), c_int32, POINTER(c_int32), c_char_p]),
+    "dv_launch_label": (c_char_p, [c_int32]),
+    "dv_abi_version": (c_int32, []),
+    "dv_predict_workspace_bytes": (c_size_t, [POINTER(CPredictor), c_int32]),
+    "dv_predict_mlp": (c_int32, _PRED_ARGS),
+    "dv_predict_heads": (c_int32, _PRED_ARGS),
+    "dv_sparse_mlp_workspace_bytes": (c_size_t, [POINTER(CMlp), c_int32, c_int32, c_int32]),
+    "dv_sparse_mlp": (c_int32, [POINTER(CMlp), c_void_p, c_int32, c_void_p, c_int32, c_int32, c_int32,
+                                c_void_p, c_void_p, c_size_t, c_uint32, c_void_p]),
+    "dv_sparse_attn_workspace_bytes": (c_size_t, [POINTER(CAttn), POINTER(CKV), c_int32, c_int32]),
+    "dv_sparse_attn": (c_int32, [POINTER(CAttn), c_void_p, c_int32, POINTER(CKV), c_void_p, c_int32,
+                                 c_float, c_void_p, c_void_p, c_size_t, c_uint32, c_void_p]),
+    "dv_sparse_block_workspace_bytes": (c_size_t, [POINTER(CAttn), POINTER(CMlp), POINTER(CPredictor),
+                                                   POINTER(CPredictor), POINTER(CKV), c_int32, c_int32,
+                                                   c_int32]),
+    "dv_sparse_block": (c_int32, [POINTER(CAttn), POINTER(CMlp), POINTER(CPredictor), POINTER(CPredictor),
+                                  POINTER(CLN), POINTER(CKV), c_void_p, c_void_p, c_int32, c_int32, c_int32,
+                                  c_int32, c_int32, c_float, c_void_p, c_void_p, c_void_p, c_size_t,
+                                  c_uint32, c_void_p]),
+}
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load the HIP library (raises OSError if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(path):
+            raise OSError(f"{path} not found: build it with `python -m paper_2310_17157_amd.build`")
+        lib = ctypes.CDLL(path)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(lib, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = lib
+    return _lib
+
+
+def lib_path() -> str:
+    return LIB_PATH
+
+
+# ------------------------------------------------------------------ helpers
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _wtype(t: torch.Tensor) -> int:
+    if t.dtype == torch.float16:
+        return DV_F16
+    if t.dtype == torch.float32:
+        return DV_F32
+    raise TypeError(f"unsupported storage dtype {t.dtype}")
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _check(fn: str, st: int):
+    if st != 0:
+        raise DvError(fn, st, load().dv_status_string(st).decode())
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor:
+    # 256-byte alignment: torch's caching allocator returns 512-byte aligned blocks.
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+@dataclass
+class Predictor:
+    """Two-layer low-rank predictor: AT [r][d], BT [n_out][r] (same storage dtype)."""
+    AT: torch.Tensor
+    BT: torch.Tensor
+
+    def c(self) -> CPredictor:
+        r, d = self.AT.shape
+        return CPredictor(d, r, self.BT.shape[0], _wtype(self.AT), _ptr(self.AT), _ptr(self.BT))
+
+
+@dataclass
+class MLP:
+    W1T: torch.Tensor
+    W2T: torch.Tensor
+    b1: Optional[torch.Tensor] = None
+    b2: Optional[torch.Tensor] = None
+
+    def c(self) -> CMlp:
+        n, d = self.W1T.shape
+        return CMlp(d, n, _wtype(self.W1T), 0, _ptr(self.W1T), _ptr(self.b1), _ptr(self.W2T), _ptr(self.b2))
+
+
+@dataclass
+class Attn:
+    Wq: torch.Tensor
+    Wk: torch.Tensor
+    Wv: torch.Tensor
+    WoT: torch.Tensor
+    H: int
+    bq: Optional[torch.Tensor] = None
+    bk: Optional[torch.Tensor] = None
+    bv: Optional[torch.Tensor] = None
+    bo: Optional[torch.Tensor] = None
+
+    def c(self) -> CAttn:
+        hd, d = self.Wq.shape
+        return CAttn(d, self.H, hd // self.H, _wtype(self.Wq), _ptr(self.Wq), _ptr(self.Wk), _ptr(self.Wv),
+                     _ptr(self.bq), _ptr(self.bk), _ptr(self.bv), _ptr(self.WoT), _ptr(self.bo))
+
+
+class KVCache:
+    """K, V [B][H][cap][dh] device tensors and the host positions pos[B]."""
+
+    def __init__(self, K: torch.Tensor, V: torch.Tensor, pos):
+        self.K, self.V = K, V
+        self._pos = (c_int32 * K.shape[0])(*[int(p) for p in pos])
+
+    def c(self) -> CKV:
+        B, H, cap, dh = self.K.shape
+        return CKV(B, H, dh, cap, _wtype(self.K), 0, _ptr(self.K), _ptr(self.V),
+                   ctypes.cast(self._pos, POINTER(c_int32)))
+
+
+@dataclass
+class LN:
+    g1: Optional[torch.Tensor] = None
+    be1: Optional[torch.Tensor] = None
+    g2: Optional[torch.Tensor] = None
+    be2: Optional[torch.Tensor] = None
+    eps: float = 1e-5
+
+    def c(self) -> CLN:
+        return CLN(_ptr(self.g1), _ptr(self.be1), _ptr(self.g2), _ptr(self.be2), self.eps)
+
+
+# ------------------------------------------------------------- entry points
+def _predict(fn, pred: Predictor, x, k=0, mode=DV_SELECT_TOPK, thresh=0.0, idx=None, count=None,
+             scores=None, cap_idx=None, ws=None, flags=0, stream=None):
+    lib = load()
+    cp = pred.c()
+    B = x.shape[0]
+    if cap_idx is None:
+        cap_idx = k if mode == DV_SELECT_TOPK else cp.n_out
+    if idx is None:
+        idx = torch.empty((B, max(cap_idx, 1)), dtype=torch.int32, device=x.device)
+    if count is None:
+        count = torch.empty(B, dtype=torch.int32, device=x.device)
+    if ws is None:
+        ws = _workspace(lib.dv_predict_workspace_bytes(ctypes.byref(cp), B), x.device)
+    st = getattr(lib, fn)(ctypes.byref(cp), _ptr(x), B, mode, k, thresh, _ptr(idx), cap_idx, _ptr(count),
+                          _ptr(scores), _ptr(ws), ws.numel(), flags, _stream(stream))
+    _check(fn, st)
+    return idx, count
+
+
+def dv_predict_mlp(pred: Predictor, x, k=0, **kw):
+    """S_M per sequence from s = (x A) B: top-k (default) or threshold. Returns (idx, count)."""
+    return _predict("dv_predict_mlp", pred, x, k, **kw)
+
+
+def dv_predict_heads(pred: Predictor, x, k=0, **kw):
+    """S_A per sequence from the head predictor. Returns (idx, count)."""
+    return _predict("dv_predict_heads", pred, x, k, **kw)
+
+
+def dv_sparse_mlp(mlp: MLP, x, idx, idx_per_seq=0, batch_mode=DV_MLP_UNION, out=None, ws=None,
+                  flags=0, stream=None):
+    """out[b] = MLP_S(x[b]) (Eq. (1)), without residual."""
+    lib = load()
+    cm = mlp.c()
+    B = x.shape[0]
+    n_idx = idx.shape[-1]
+    if out is None:
+        out = torch.empty((B, cm.d), dtype=torch.float32, device=x.device)
+    if ws is None:
+        ws = _workspace(lib.dv_sparse_mlp_workspace_bytes(ctypes.byref(cm), B, n_idx, idx_per_seq), x.device)
+    st = lib.dv_sparse_mlp(ctypes.byref(cm), _ptr(x), B, _ptr(idx), n_idx, idx_per_seq, batch_mode,
+                           _ptr(out), _ptr(ws), ws.numel(), flags, _stream(stream))
+    _check("dv_sparse_mlp", st)
+    return out
+
+
+def dv_sparse_attn(attn: Attn, x, kv: KVCache, heads, scale, out=None, ws=None, flags=0, stream=None):
+    """out[b] = bo + sum_{i in S_A^b} H_i(x[b]) W^O_i (Eq. (2)); updates the cache rows at pos."""
+    lib = load()
+    ca, ck = attn.c(), kv.c()
+    B = x.shape[0]
+    n_heads = heads.shape[-1]
+    if out is None:
+        out = torch.empty((B, ca.d), dtype=torch.float32, device=x.device)
+    if ws is None:
+        ws = _workspace(lib.dv_sparse_attn_workspace_bytes(ctypes.byref(ca), ctypes.byref(ck), B, n_heads),
+                        x.device)
+    st = lib.dv_sparse_attn(ctypes.byref(ca), _ptr(x), B, ctypes.byref(ck), _ptr(heads), n_heads, scale,
+                            _ptr(out), _ptr(ws), ws.numel(), flags, _stream(stream))
+    _check("dv_sparse_attn", st)
+    return out
+
+
+def dv_sparse_block(attn: Attn, mlp: MLP, pred_h: Predictor, pred_m: Predictor, ln: Optional[LN],
+                    kv: KVCache, x, k_heads, k_mlp, scale, mode=DV_LOOKAHEAD, batch_mode=DV_MLP_UNION,
+                    out=None, heads_out=None, idx_out=None, ws=None, flags=0, stream=None):
+    """One decoder layer with contextual sparsity (Section 4.3). Returns (out, heads, idx)."""
+    lib = load()
+    ca, cm, cph, cpm, ck = attn.c(), mlp.c(), pred_h.c(), pred_m.c(), kv.c()
+    cl = ln.c() if ln is not None else None
+    B = x.shape[0]
+    if out is None:
+        out = torch.empty_like(x)
+    if heads_out is None:
+        heads_out = torch.empty((B, k_heads), dtype=torch.int32, device=x.device)
+    if idx_out is None:
+        idx_out = torch.empty((B, k_mlp), dtype=torch.int32, device=x.device)
+    if ws is None:
+        ws = _workspace(block_workspace_bytes(attn, mlp, pred_h, pred_m, kv, B, k_heads, k_mlp), x.device)
+    st = lib.dv_sparse_block(ctypes.byref(ca), ctypes.byref(cm), ctypes.byref(cph), ctypes.byref(cpm),
+                             ctypes.byref(cl) if cl is not None else None, ctypes.byref(ck), _ptr(x),
+                             _ptr(out), B, k_heads, k_mlp, mode, batch_mode, scale, _ptr(heads_out),
+                             _ptr(idx_out), _ptr(ws), ws.numel(), flags, _stream(stream))
+    _check("dv_sparse_block", st)
+    return out, heads_out, idx_out
+
+
+def block_workspace_bytes(attn, mlp, pred_h, pred_m, kv, B, k_heads, k_mlp) -> int:
+    lib = load()
+    ca, cm, cph, cpm, ck = attn.c(), mlp.c(), pred_h.c(), pred_m.c(), kv.c()
+    return lib.dv_sparse_block_workspace_bytes(ctypes.byref(ca), ctypes.byref(cm), ctypes.byref(cph),
+                                               ctypes.byref(cpm), ctypes.byref(ck), B, k_heads, k_mlp)
+
+
+def mlp_workspace_bytes(mlp, B, n_idx, idx_per_seq=0) -> int:
+    cm = mlp.c()
+    return load().dv_sparse_mlp_workspace_bytes(ctypes.byref(cm), B, n_idx, idx_per_seq)
+
+
+def attn_workspace_bytes(attn, kv, B, n_heads) -> int:
+    ca, ck = attn.c(), kv.c()
+    return load().dv_sparse_attn_workspace_bytes(ctypes.byref(ca), ctypes.byref(ck), B, n_heads)
+
+
+def predict_workspace_bytes(pred, B) -> int:
+    cp = pred.c()
+    return load().dv_predict_workspace_bytes(ctypes.byref(cp), B)
+
+
+# --------------------------------------------------------- per-launch timing
+class LaunchTimer:
+    """HIP events around each kernel launch of the library's entry points.
+
+    Arms dv_set_launch_events with `n_pairs` event pairs created through the HIP
+    runtime; after a call (and a synchronisation) `times_ms()` returns
+    [(label, milliseconds)] for each launch of that call. Events are recorded on
+    the stream the library launched on.
+    """
+
+    def __init__(self, n_pairs: int = 16, only: Optional[str] = None):
+        self._hip = ctypes.CDLL("libamdhip64.so")
+        self._hip.hipEventCreate.argtypes = [POINTER(c_void_p)]
+        self._hip.hipEventElapsedTime.argtypes = [POINTER(c_float), c_void_p, c_void_p]
+        self._hip.hipEventSynchronize.argtypes = [c_void_p]
+        self._hip.hipEventDestroy.argtypes = [c_void_p]
+        self.n = n_pairs
+        self.events = (c_void_p * (2 * n_pairs))()
+        for i in range(2 * n_pairs):
+            ev = c_void_p()
+            if self._hip.hipEventCreate(ctypes.byref(ev)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+            self.events[i] = ev
+        self.n_launched = c_int32(0)
+        self.only = only.encode() if only else None
+        self.labels = []
+
+    def arm(self):
+        _check("dv_set_launch_events",
+               load().dv_set_launch_events(self.events, self.n, ctypes.byref(self.n_launched), self.only))
+
+    def disarm(self):
+        lib = load()
+        labels = [lib.dv_launch_label(i).decode() for i in range(self.n_launched.value)]
+        if self.only is not None:
+            labels = [l for l in labels if l == self.only.decode()]
+        self.labels = labels[: self.n]
+        lib.dv_set_launch_events(None, 0, None, None)
+
+    def times_ms(self):
+        out = []
+        for i in range(len(self.labels)):
+            a, b = self.events[2 * i], self.events[2 * i + 1]
+            self._hip.hipEventSynchronize(b)
+            ms = c_float(0.0)
+            if self._hip.hipEventElapsedTime(ctypes.byref(ms), a, b) != 0:
+                raise RuntimeError("hipEventElapsedTime failed")
+            out.append((self.labels[i], ms.value))
+        return out
+
+    def close(self):
+        load().dv_set_launch_events(None, 0, None, None)
+        for i in range(2 * self.n):
+            self._hip.hipEventDestroy(self.events[i])

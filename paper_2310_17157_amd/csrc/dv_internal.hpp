@@ -1,0 +1,396 @@
+// Internal definitions shared by the HIP translation units of the Deja Vu decode
+// library: device helpers (16-byte weight chunks, wavefront and workgroup
+// reductions, layer-norm staging into LDS, order-preserving float keys), kernel
+// argument structures and the host-side launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "dv.h"
+
+namespace dv {
+
+constexpr int kWave = 64;
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+
+// Elements per 16-byte chunk for a storage type.
+template <typename T> struct Chunk;
+template <> struct Chunk<float> { static constexpr int E = 4; };
+template <> struct Chunk<_Float16> { static constexpr int E = 8; };
+
+// ---------------------------------------------------------------- loads
+// Weights are streamed once per call: non-temporal 16-byte loads.
+__device__ __forceinline__ u32x4 ld_stream(const void* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
+__device__ __forceinline__ u32x4 ld_plain(const void* p) {
+  return *reinterpret_cast<const u32x4*>(p);
+}
+
+// Unpack a 16-byte chunk into E floats.
+template <typename T>
+__device__ __forceinline__ void unpack(u32x4 w, float* v);
+template <>
+__device__ __forceinline__ void unpack<float>(u32x4 w, float* v) {
+  f32x4 f = __builtin_bit_cast(f32x4, w);
+  v[0] = f[0]; v[1] = f[1]; v[2] = f[2]; v[3] = f[3];
+}
+template <>
+__device__ __forceinline__ void unpack<_Float16>(u32x4 w, float* v) {
+  f16x8 h = __builtin_bit_cast(f16x8, w);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = (float)h[i];
+}
+
+// Store E floats as one chunk of storage type T (round to nearest even for fp16).
+template <typename T>
+__device__ __forceinline__ void store_elem(T* p, float v) { *p = (T)v; }
+
+// ---------------------------------------------------- x-hat in LDS
+// The input vector of a row-dot is staged in LDS as fp32. For fp16 rows a 16-byte
+// chunk c holds elements 8c..8c+7; its fp32 operands live in two planes (elements
+// 8c..8c+3 at plane 0, 8c+4..8c+7 at plane 1) so that lanes reading consecutive
+// chunks read consecutive 16-byte words of each plane. For fp32 rows chunk c is
+// elements 4c..4c+3 of a single plane.
+template <typename T>
+__device__ __forceinline__ int xs_index(int e, int d);
+template <>
+__device__ __forceinline__ int xs_index<float>(int e, int) { return e; }
+template <>
+__device__ __forceinline__ int xs_index<_Float16>(int e, int d) {
+  return ((e >> 2) & 1) * (d >> 1) + ((e >> 3) << 2) + (e & 3);
+}
+
+template <typename T>
+__device__ __forceinline__ float dot_chunk(u32x4 w, const float* xs, int d, int c, float acc);
+template <>
+__device__ __forceinline__ float dot_chunk<float>(u32x4 w, const float* xs, int, int c, float acc) {
+  f32x4 wf = __builtin_bit_cast(f32x4, w);
+  f32x4 x = *reinterpret_cast<const f32x4*>(xs + 4 * c);
+  acc = fmaf(wf[0], x[0], acc);
+  acc = fmaf(wf[1], x[1], acc);
+  acc = fmaf(wf[2], x[2], acc);
+  acc = fmaf(wf[3], x[3], acc);
+  return acc;
+}
+template <>
+__device__ __forceinline__ float dot_chunk<_Float16>(u32x4 w, const float* xs, int d, int c, float acc) {
+  f16x8 h = __builtin_bit_cast(f16x8, w);
+  f32x4 xa = *reinterpret_cast<const f32x4*>(xs + 4 * c);
+  f32x4 xb = *reinterpret_cast<const f32x4*>(xs + (d >> 1) + 4 * c);
+  acc = fmaf((float)h[0], xa[0], acc);
+  acc = fmaf((float)h[1], xa[1], acc);
+  acc = fmaf((float)h[2], xa[2], acc);
+  acc = fmaf((float)h[3], xa[3], acc);
+  acc = fmaf((float)h[4], xb[0], acc);
+  acc = fmaf((float)h[5], xb[1], acc);
+  acc = fmaf((float)h[6], xb[2], acc);
+  acc = fmaf((float)h[7], xb[3], acc);
+  return acc;
+}
+
+// ------------------------------------------------------------ reductions
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+  return v;
+}
+
+// Sum over the workgroup in a fixed order; every thread gets the result.
+// `red` holds at least NT/64 floats of LDS.
+template <int NT>
+__device__ __forceinline__ float block_sum(float v, float* red) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  float t = 0.f;
+#pragma unroll
+  for (int i = 0; i < NT / kWave; ++i) t += red[i];
+  return t;
+}
+
+// Exclusive prefix sum of one int per thread over the workgroup (thread order).
+// `red` holds at least NT/64 + 1 ints of LDS. Returns the exclusive prefix; the
+// total goes to *total.
+template <int NT>
+__device__ __forceinline__ int block_excl_scan(int v, int* red, int* total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int inc = v;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    int n = __shfl_up(inc, o, kWave);
+    if (lane >= o) inc += n;
+  }
+  __syncthreads();
+  if (lane == 63) red[w] = inc;
+  __syncthreads();
+  int base = 0, tot = 0;
+#pragma unroll
+  for (int i = 0; i < NT / kWave; ++i) {
+    if (i < w) base += red[i];
+    tot += red[i];
+  }
+  *total = tot;
+  return base + inc - v;
+}
+
+// Stage x[0..d) (fp32, 16-byte aligned, d % 4 == 0) into LDS in the layout of
+// xs_index<T>, optionally applying layer norm with gamma g (NULL: no LN) and beta b
+// (NULL: 0). Biased variance, two passes over LDS. Ends with a barrier.
+template <typename T, int NT>
+__device__ void stage_x(const float* __restrict__ x, int d, const float* __restrict__ g,
+                        const float* __restrict__ b, float eps, float* xs, float* red) {
+  const int n4 = d >> 2;
+  float s = 0.f;
+  for (int i = threadIdx.x; i < n4; i += NT) {
+    f32x4 v = *reinterpret_cast<const f32x4*>(x + 4 * i);
+    *reinterpret_cast<f32x4*>(xs + xs_index<T>(4 * i, d)) = v;
+    s += (v[0] + v[1]) + (v[2] + v[3]);
+  }
+  if (g == nullptr) {
+    __syncthreads();
+    return;
+  }
+  const float mean = block_sum<NT>(s, red) / (float)d;
+  float q = 0.f;
+  for (int i = threadIdx.x; i < n4; i += NT) {
+    f32x4 v = *reinterpret_cast<const f32x4*>(xs + xs_index<T>(4 * i, d));
+    float a0 = v[0] - mean, a1 = v[1] - mean, a2 = v[2] - mean, a3 = v[3] - mean;
+    q += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
+  }
+  const float var = block_sum<NT>(q, red) / (float)d;
+  const float rstd = 1.0f / sqrtf(var + eps);
+  for (int i = threadIdx.x; i < n4; i += NT) {
+    float* p = xs + xs_index<T>(4 * i, d);
+    f32x4 v = *reinterpret_cast<const f32x4*>(p);
+    f32x4 gg = *reinterpret_cast<const f32x4*>(g + 4 * i);
+    f32x4 bb = {0.f, 0.f, 0.f, 0.f};
+    if (b != nullptr) bb = *reinterpret_cast<const f32x4*>(b + 4 * i);
+    f32x4 o;
+    o[0] = (v[0] - mean) * rstd * gg[0] + bb[0];
+    o[1] = (v[1] - mean) * rstd * gg[1] + bb[1];
+    o[2] = (v[2] - mean) * rstd * gg[2] + bb[2];
+    o[3] = (v[3] - mean) * rstd * gg[3] + bb[3];
+    *reinterpret_cast<f32x4*>(p) = o;
+  }
+  __syncthreads();
+}
+
+// Dot product of one row (d elements of T, 16-byte aligned) with the staged x-hat,
+// computed by one wavefront over the chunks c = lane + 64*(seg + S*j). Returns the
+// wavefront total (in every lane) of this segment. U chunks per lane are in flight.
+template <typename T, int U, int S>
+__device__ __forceinline__ float wave_rowdot(const T* __restrict__ row, const float* xs, int d,
+                                             int lane, int seg) {
+  constexpr int E = Chunk<T>::E;
+  const int nch = d / E;
+  const char* base = reinterpret_cast<const char*>(row);
+  float acc0 = 0.f, acc1 = 0.f;
+  int c = lane + 64 * seg;
+  constexpr int step = 64 * S;
+  for (; c + step * (U - 1) < nch; c += step * U) {
+    u32x4 w[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) w[u] = ld_stream(base + (size_t)(c + step * u) * 16);
+#pragma unroll
+    for (int u = 0; u < U; u += 2) {
+      acc0 = dot_chunk<T>(w[u], xs, d, c + step * u, acc0);
+      if (u + 1 < U) acc1 = dot_chunk<T>(w[u + 1], xs, d, c + step * (u + 1), acc1);
+    }
+  }
+  for (; c < nch; c += step) {
+    u32x4 w = ld_stream(base + (size_t)c * 16);
+    acc0 = dot_chunk<T>(w, xs, d, c, acc0);
+  }
+  return wave_sum(acc0 + acc1);
+}
+
+// The first U chunks a wavefront will need for a row (same chunk order as
+// wave_rowdot), loaded early so that HBM latency overlaps a workgroup prologue.
+template <typename T, int U, int S>
+__device__ __forceinline__ void row_prefetch(const T* __restrict__ row, int d, int lane, int seg,
+                                             u32x4 (&w)[U]) {
+  constexpr int E = Chunk<T>::E;
+  const int nch = d / E;
+  const char* base = reinterpret_cast<const char*>(row);
+  const int c0 = lane + 64 * seg;
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int c = c0 + 64 * S * u;
+    w[u] = c < nch ? ld_stream(base + (size_t)c * 16) : u32x4{0u, 0u, 0u, 0u};
+  }
+}
+
+// wave_rowdot whose first U chunks were loaded by row_prefetch.
+template <typename T, int U, int S>
+__device__ __forceinline__ float wave_rowdot_pf(const T* __restrict__ row, const float* xs, int d, int lane,
+                                                int seg, const u32x4 (&w0)[U]) {
+  constexpr int E = Chunk<T>::E;
+  constexpr int step = 64 * S;
+  const int nch = d / E;
+  const char* base = reinterpret_cast<const char*>(row);
+  const int c0 = lane + 64 * seg;
+  float acc0 = 0.f, acc1 = 0.f;
+#pragma unroll
+  for (int u = 0; u < U; u += 2) {
+    if (c0 + step * u < nch) acc0 = dot_chunk<T>(w0[u], xs, d, c0 + step * u, acc0);
+    if (u + 1 < U && c0 + step * (u + 1) < nch) acc1 = dot_chunk<T>(w0[u + 1], xs, d, c0 + step * (u + 1), acc1);
+  }
+  int c = c0 + step * U;
+  for (; c + step * (U - 1) < nch; c += step * U) {
+    u32x4 w[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) w[u] = ld_stream(base + (size_t)(c + step * u) * 16);
+#pragma unroll
+    for (int u = 0; u < U; u += 2) {
+      acc0 = dot_chunk<T>(w[u], xs, d, c + step * u, acc0);
+      if (u + 1 < U) acc1 = dot_chunk<T>(w[u + 1], xs, d, c + step * (u + 1), acc1);
+    }
+  }
+  for (; c < nch; c += step) {
+    u32x4 w = ld_stream(base + (size_t)c * 16);
+    acc0 = dot_chunk<T>(w, xs, d, c, acc0);
+  }
+  return wave_sum(acc0 + acc1);
+}
+
+// Order-preserving key of a float: a > b  <=>  key(a) > key(b); -0 maps to +0.
+__device__ __forceinline__ uint32_t fkey(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u << 1) == 0u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// ------------------------------------------------------------------ host
+struct Workspace {
+  size_t off = 0;
+  char* base = nullptr;
+  explicit Workspace(void* b) : base(static_cast<char*>(b)) {}
+  template <typename P>
+  P* take(size_t bytes) {
+    P* p = reinterpret_cast<P*>(base ? base + off : nullptr);
+    off += (bytes + 255) & ~size_t(255);
+    return p;
+  }
+};
+
+inline int elem_bytes(int dtype) { return dtype == DV_F16 ? 2 : 4; }
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int device_cu_count();   // cached per device
+
+// Optional per-launch event recording (dv_set_launch_events), per calling thread.
+void trace_reset();
+void trace_begin(const char* label, hipStream_t st);
+void trace_end(hipStream_t st);
+
+#define DV_LAUNCH(label, stream, expr)              \
+  do {                                              \
+    ::dv::trace_begin(label, stream);               \
+    const hipError_t dv_e_ = (expr);                \
+    ::dv::trace_end(stream);                        \
+    if (dv_e_ != hipSuccess) return DV_ERR_HIP;     \
+  } while (0)
+
+// ---------------------------------------------------------- launchers
+// Each returns hipSuccess or the launch error. All work goes on `st`.
+
+// Select per row of scores [B][n]: top-k or threshold, ascending output.
+hipError_t launch_select(const float* scores, int B, int n, int mode, int k, float thresh,
+                         int32_t* idx, int cap, int32_t* count, int32_t* idx2, hipStream_t st);
+
+// Device-side check that each of B sets set[b][0..n) is strictly ascending within
+// [0, range); writes 0 (valid) or 1 to *bad.
+hipError_t launch_validate_sets(const int32_t* set, int B, int n, int range, int32_t* bad, hipStream_t st);
+
+// Predictor hidden layer: hid[b][j] = x-hat[b] . AT[j], for up to two predictors
+// sharing one input (rows of P0 first, then rows of P1). LN applied if g != NULL.
+struct PredHidArgs {
+  int d, B;
+  const float* x;           // [B][d]
+  const float* g; const float* be; float eps;
+  const void* AT0; int r0; float* hid0;   // [B][r0]
+  const void* AT1; int r1; float* hid1;   // [B][r1] (r1 = 0: none)
+};
+hipError_t launch_pred_hidden(int wtype, const PredHidArgs& a, hipStream_t st);
+
+// Predictor scores: s[b][i] = hid[b] . BT[i] for up to two predictors.
+struct PredScoreArgs {
+  int r0, n0; const void* BT0; const float* hid0; float* s0;   // hid0 [B][r0], s0 [B][n0]
+  int r1, n1; const void* BT1; const float* hid1; float* s1;   // n1 = 0: none
+  int B;
+};
+hipError_t launch_pred_scores(int wtype, const PredScoreArgs& a, hipStream_t st);
+
+// Gathered row-dot for Q/K/V of the selected heads (B = 1) plus optional fused work.
+struct QkvArgs {
+  int d, H, dh, cap, pos, n_heads;
+  const float* x; const float* g; const float* be; float eps;    // LN1 (g NULL: none)
+  const void* Wq; const void* Wk; const void* Wv;
+  const float* bq; const float* bk; const float* bv;
+  void* K; void* V;                 // [H][cap][dh] of this sequence
+  float* q;                         // [n_heads][dh] out
+  const int32_t* heads_in;          // given head set, or NULL when selecting from scores
+  const float* head_scores;         // [H] (when heads_in == NULL)
+  int32_t* heads_ws;                // [n_heads] out: the set used (written by workgroup 0)
+  int32_t* heads_out;               // optional caller copy
+};
+hipError_t launch_qkv(int wtype, int kvtype, const QkvArgs& a, hipStream_t st);
+
+// Split-KV decode attention for the selected heads (B = 1).
+struct AttnArgs {
+  int H, dh, cap, pos, n_heads, n_split, chunk;
+  const float* q; const int32_t* heads; const void* K; const void* V; float scale;
+  float* part;                      // [n_heads][n_split][dh + 2]
+};
+hipError_t launch_attn(int kvtype, const AttnArgs& a, hipStream_t st);
+
+// Gathered row-axpy: out = resid + bias + sum_rows coef[row] * M[rowidx(row)], tiled by
+// columns with a split over rows. With one row range the kernel writes out directly;
+// otherwise it writes partial[split][d] and launch_reduce finishes the sum.
+struct AxpyArgs {
+  int d, nrows;
+  const void* M; int m_rows;        // M is [m_rows][d]
+  // Row source: neuron rows (rows = set) or head rows (rows = set[row / dh] * dh + row % dh).
+  const int32_t* set; int dh;       // dh = 0: neuron rows
+  // Coefficients: coef[row] (neurons), or from attention partials (heads).
+  const float* coef;
+  const float* part; int n_split;   // attention partials when coef == NULL
+  const float* resid; const float* bias;   // optional, [d]
+  float* out;                        // [d]
+  float* out2;                       // optional second copy of out
+  float* partial;                    // [n_rsplit][d] scratch
+  int n_rsplit, rows_per_split;
+};
+hipError_t launch_axpy(int wtype, const AxpyArgs& a, hipStream_t st);
+// out = resid + bias + sum over nsplit rows of partial[nsplit][d] (fixed order); d % 4 == 0.
+hipError_t launch_reduce(const float* partial, int nsplit, int d, const float* resid, const float* bias,
+                         float* out, float* out2, hipStream_t st);
+
+// fc1 + ReLU over the selected neurons (B = 1): h[s] = max(x-hat . W1T[set[s]] + b1, 0).
+struct Fc1Args {
+  int d, k, n;                      // width, selected neurons, neurons in W1T
+  const float* x; const float* g; const float* be; float eps;    // LN (g NULL: none)
+  const void* W1T; const float* b1; const int32_t* set;
+  float* h;
+};
+hipError_t launch_fc1(int wtype, const Fc1Args& a, hipStream_t st);
+
+// Tiling helpers shared by the host code.
+int axpy_tiles(int d, int wtype);
+int axpy_rsplit(int nrows, int d, int wtype, int* rows_per_split);
+int attn_chunk(int n_heads, int attended, int dh, int kvtype);
+
+}  // namespace dv

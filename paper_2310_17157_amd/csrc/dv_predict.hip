@@ -1,0 +1,298 @@
+// Sparsity predictors (Sections 4.1-4.2): s = (x A) B, then top-k or threshold
+// selection. A = AT^T is d x r and B = BT^T is r x n; both factors are stored with
+// their output index as the row so every GEMV streams whole contiguous rows.
+#include "dv_internal.hpp"
+#include "dv_select.hpp"
+
+namespace dv {
+
+// Combine S partial dots of one row computed by S consecutive wavefronts.
+template <int NW, int S>
+__device__ __forceinline__ float combine_segments(float v, float* lds) {
+  if constexpr (S == 1) {
+    return v;
+  } else {
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) lds[wave] = v;
+    __syncthreads();
+    float t = 0.f;
+    if (wave % S == 0) {
+#pragma unroll
+      for (int j = 0; j < S; ++j) t += lds[wave + j];
+    }
+    __syncthreads();
+    return t;
+  }
+}
+
+// ----------------------------------------------------------- hidden layer
+// One wavefront (or S of them) per predictor row; x-hat staged once per workgroup.
+template <typename T, int NW, int S, int U>
+__global__ void __launch_bounds__(NW * 64) k_pred_hidden(PredHidArgs a) {
+  extern __shared__ float smem[];
+  float* xs = smem;
+  float* red = smem + a.d;          // NW floats (block sums)
+  float* seg = red + NW;            // NW floats (segment combine)
+  constexpr int NT = NW * 64;
+  const int b = blockIdx.y;
+  const int nrows = a.r0 + a.r1;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  constexpr int RPI = NW / S;
+  auto row_ptr = [&](int row) {
+    return row < a.r0 ? static_cast<const T*>(a.AT0) + (size_t)row * a.d
+                      : static_cast<const T*>(a.AT1) + (size_t)(row - a.r0) * a.d;
+  };
+  u32x4 pf[U];
+  {
+    const int row0 = blockIdx.x * RPI + wave / S;
+    if (row0 < nrows) row_prefetch<T, U, S>(row_ptr(row0), a.d, lane, wave % S, pf);
+  }
+  stage_x<T, NT>(a.x + (size_t)b * a.d, a.d, a.g, a.be, a.eps, xs, red);
+  bool first = true;
+  for (int base = blockIdx.x * RPI; base < nrows; base += gridDim.x * RPI) {
+    const int row = base + wave / S;
+    float v = 0.f;
+    if (row < nrows) {
+      v = first ? wave_rowdot_pf<T, U, S>(row_ptr(row), xs, a.d, lane, wave % S, pf)
+                : wave_rowdot<T, U, S>(row_ptr(row), xs, a.d, lane, wave % S);
+    }
+    first = false;
+    v = combine_segments<NW, S>(v, seg);
+    if (wave % S == 0 && lane == 0 && row < nrows) {
+      if (row < a.r0)
+        a.hid0[(size_t)b * a.r0 + row] = v;
+      else
+        a.hid1[(size_t)b * a.r1 + row - a.r0] = v;
+    }
+  }
+}
+
+hipError_t launch_pred_hidden(int wtype, const PredHidArgs& a, hipStream_t st) {
+  constexpr int NW = 8, S = 2, U = 6;
+  const int nrows = a.r0 + a.r1;
+  const int rpi = NW / S;
+  int blocks = (nrows + rpi - 1) / rpi;
+  const size_t lds = (size_t)(a.d + 2 * NW) * sizeof(float);
+  dim3 grid(blocks, a.B);
+  if (wtype == DV_F16)
+    hipLaunchKernelGGL((k_pred_hidden<_Float16, NW, S, U>), grid, dim3(NW * 64), lds, st, a);
+  else
+    hipLaunchKernelGGL((k_pred_hidden<float, NW, S, U>), grid, dim3(NW * 64), lds, st, a);
+  return hipGetLastError();
+}
+
+// ----------------------------------------------------------------- scores
+// G lanes per row (a row is r elements, short); RU rows per lane group in flight.
+template <typename T, int NW, int G, int RU>
+__global__ void __launch_bounds__(NW * 64) k_pred_scores(PredScoreArgs a) {
+  extern __shared__ float smem[];
+  constexpr int NT = NW * 64;
+  constexpr int E = Chunk<T>::E;
+  const int b = blockIdx.y;
+  const int r0a = (a.r0 + 3) & ~3;
+  float* xs0 = smem;
+  float* xs1 = smem + r0a;
+  stage_x<T, NT>(a.hid0 + (size_t)b * a.r0, a.r0, nullptr, nullptr, 0.f, xs0, nullptr);
+  if (a.n1 > 0) stage_x<T, NT>(a.hid1 + (size_t)b * a.r1, a.r1, nullptr, nullptr, 0.f, xs1, nullptr);
+  const int nrows = a.n0 + a.n1;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int grp = lane / G, gl = lane % G;
+  constexpr int GPW = 64 / G;          // row groups per wavefront
+  constexpr int RPW = GPW * RU;        // rows per wavefront iteration
+  for (int base = (blockIdx.x * NW + wave) * RPW; base < nrows; base += gridDim.x * NW * RPW) {
+    const char* rp[RU];
+    const float* xsu[RU];
+    int ru[RU], nch[RU];
+    float acc[RU];
+    int cmax = 0;
+#pragma unroll
+    for (int u = 0; u < RU; ++u) {
+      const int row = base + u * GPW + grp;
+      acc[u] = 0.f;
+      if (row < a.n0) {
+        rp[u] = reinterpret_cast<const char*>(static_cast<const T*>(a.BT0) + (size_t)row * a.r0);
+        xsu[u] = xs0; ru[u] = a.r0; nch[u] = a.r0 / E;
+      } else if (row < nrows) {
+        rp[u] = reinterpret_cast<const char*>(static_cast<const T*>(a.BT1) + (size_t)(row - a.n0) * a.r1);
+        xsu[u] = xs1; ru[u] = a.r1; nch[u] = a.r1 / E;
+      } else {
+        rp[u] = nullptr; xsu[u] = xs0; ru[u] = a.r0; nch[u] = 0;
+      }
+      cmax = max(cmax, nch[u]);
+    }
+    for (int c = gl; c < cmax; c += G) {
+      u32x4 w[RU];
+#pragma unroll
+      for (int u = 0; u < RU; ++u) w[u] = c < nch[u] ? ld_stream(rp[u] + (size_t)c * 16) : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int u = 0; u < RU; ++u)
+        if (c < nch[u]) acc[u] = dot_chunk<T>(w[u], xsu[u], ru[u], c, acc[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < RU; ++u) {
+      float v = acc[u];
+#pragma unroll
+      for (int o = G / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+      const int row = base + u * GPW + grp;
+      if (gl == 0 && row < nrows) {
+        if (row < a.n0)
+          a.s0[(size_t)b * a.n0 + row] = v;
+        else
+          a.s1[(size_t)b * a.n1 + row - a.n0] = v;
+      }
+    }
+  }
+}
+
+template <typename T>
+static hipError_t launch_scores_t(const PredScoreArgs& a, hipStream_t st) {
+  constexpr int NW = 8;
+  constexpr int E = Chunk<T>::E;
+  const int nch = max(a.r0, a.r1) / E;
+  const int nrows = a.n0 + a.n1;
+  const size_t lds = (size_t)(((a.r0 + 3) & ~3) + a.r1 + 4) * sizeof(float);
+  if (nch > 32) {
+    constexpr int G = 64, RU = 8, RPB = NW * (64 / G) * RU;
+    dim3 grid(min((nrows + RPB - 1) / RPB, 4096), a.B);
+    hipLaunchKernelGGL((k_pred_scores<T, NW, G, RU>), grid, dim3(NW * 64), lds, st, a);
+  } else if (nch > 16) {
+    constexpr int G = 32, RU = 4, RPB = NW * (64 / G) * RU;
+    dim3 grid(min((nrows + RPB - 1) / RPB, 4096), a.B);
+    hipLaunchKernelGGL((k_pred_scores<T, NW, G, RU>), grid, dim3(NW * 64), lds, st, a);
+  } else {
+    constexpr int G = 16, RU = 4, RPB = NW * (64 / G) * RU;
+    dim3 grid(min((nrows + RPB - 1) / RPB, 4096), a.B);
+    hipLaunchKernelGGL((k_pred_scores<T, NW, G, RU>), grid, dim3(NW * 64), lds, st, a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_pred_scores(int wtype, const PredScoreArgs& a, hipStream_t st) {
+  return wtype == DV_F16 ? launch_scores_t<_Float16>(a, st) : launch_scores_t<float>(a, st);
+}
+
+// ---------------------------------------------------------------- select
+__global__ void __launch_bounds__(1024) k_select(const float* s, int n, int mode, int k, float thresh,
+                                                 int32_t* idx, int cap, int32_t* count, int32_t* idx2) {
+  __shared__ uint32_t hist[kSelBins];
+  __shared__ int sm[kSelSm(1024)];
+  const int b = blockIdx.x;
+  if (n <= 1024 * 48)
+    wg_select_reg<1024, 48>(s + (size_t)b * n, n, mode, k, thresh, idx + (size_t)b * cap, cap,
+                            count ? count + b : nullptr, idx2 ? idx2 + (size_t)b * cap : nullptr, hist, sm);
+  else
+    wg_select<1024>(s + (size_t)b * n, n, mode, k, thresh, idx + (size_t)b * cap, cap,
+                    count ? count + b : nullptr, idx2 ? idx2 + (size_t)b * cap : nullptr, hist, sm);
+}
+
+hipError_t launch_select(const float* scores, int B, int n, int mode, int k, float thresh,
+                         int32_t* idx, int cap, int32_t* count, int32_t* idx2, hipStream_t st) {
+  hipLaunchKernelGGL(k_select, dim3(B), dim3(1024), 0, st, scores, n, mode, k, thresh, idx, cap, count, idx2);
+  return hipGetLastError();
+}
+
+// One workgroup checks every set: strictly ascending and within [0, range).
+// A debugging aid (DV_VALIDATE), not on the timed path.
+__global__ void __launch_bounds__(1024) k_validate_sets(const int32_t* set, int B, int n, int range,
+                                                        int32_t* bad) {
+  __shared__ int any_bad;
+  if (threadIdx.x == 0) any_bad = 0;
+  __syncthreads();
+  int ok = 1;
+  const long total = (long)B * n;
+  for (long g = threadIdx.x; g < total; g += 1024) {
+    const int i = (int)(g % n);
+    const int v = set[g];
+    ok &= (v >= 0) & (v < range);
+    if (i > 0) ok &= set[g - 1] < v;
+  }
+  if (!ok) atomicOr(&any_bad, 1);
+  __syncthreads();
+  if (threadIdx.x == 0) *bad = any_bad;
+}
+
+hipError_t launch_validate_sets(const int32_t* set, int B, int n, int range, int32_t* bad, hipStream_t st) {
+  hipLaunchKernelGGL(k_validate_sets, dim3(1), dim3(1024), 0, st, set, B, n, range, bad);
+  return hipGetLastError();
+}
+
+}  // namespace dv
+
+// ------------------------------------------------------------------ C ABI
+using namespace dv;
+
+static dv_status check_predictor(const dv_predictor* p) {
+  if (p == nullptr || p->AT == nullptr || p->BT == nullptr) return DV_ERR_NULL;
+  if (p->wtype != DV_F16 && p->wtype != DV_F32) return DV_ERR_DTYPE;
+  if (p->d <= 0 || p->r <= 0 || p->n_out <= 0) return DV_ERR_SHAPE;
+  const int E = 16 / elem_bytes(p->wtype);
+  if (p->d % E != 0 || p->r % E != 0) return DV_ERR_ALIGN;
+  if (!aligned16(p->AT) || !aligned16(p->BT)) return DV_ERR_ALIGN;
+  if (p->d > 16000 || p->r > 16000) return DV_ERR_UNSUPPORTED;   // LDS staging budget
+  if (p->n_out > (1 << 26)) return DV_ERR_UNSUPPORTED;
+  return DV_OK;
+}
+
+static size_t predict_ws(const dv_predictor* p, int32_t B, float* scores_given, Workspace& w,
+                         float** hid, float** scores) {
+  *hid = w.take<float>((size_t)B * p->r * sizeof(float));
+  float* s = w.take<float>(scores_given ? 0 : (size_t)B * p->n_out * sizeof(float));
+  *scores = scores_given ? scores_given : s;
+  return w.off;
+}
+
+extern "C" size_t dv_predict_workspace_bytes(const dv_predictor* p, int32_t B) {
+  if (p == nullptr || B <= 0 || p->r <= 0 || p->n_out <= 0) return 0;
+  Workspace w(nullptr);
+  float *h, *s;
+  return predict_ws(p, B, nullptr, w, &h, &s);
+}
+
+static dv_status predict_impl(const dv_predictor* p, const float* x, int32_t B, int32_t mode, int32_t k,
+                              float thresh, int32_t* idx, int32_t cap_idx, int32_t* count, float* scores,
+                              void* ws, size_t ws_bytes, uint32_t flags, void* stream) {
+  trace_reset();
+  dv_status st = check_predictor(p);
+  if (st != DV_OK) return st;
+  if (x == nullptr || idx == nullptr) return DV_ERR_NULL;
+  if (B <= 0 || B > 65535) return DV_ERR_SHAPE;
+  if (!aligned16(x)) return DV_ERR_ALIGN;
+  if (flags & ~(uint32_t)(DV_DETERMINISTIC | DV_VALIDATE)) return DV_ERR_ARG;
+  if (mode == DV_SELECT_TOPK) {
+    if (k < 0 || k > p->n_out || cap_idx < k) return DV_ERR_SHAPE;
+  } else if (mode == DV_SELECT_THRESHOLD) {
+    if (cap_idx < 0) return DV_ERR_SHAPE;
+  } else {
+    return DV_ERR_ARG;
+  }
+  if (ws == nullptr || (reinterpret_cast<uintptr_t>(ws) & 255u) != 0) return DV_ERR_WORKSPACE;
+  Workspace w(ws);
+  float *hid, *s;
+  if (predict_ws(p, B, scores, w, &hid, &s) > ws_bytes) return DV_ERR_WORKSPACE;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+
+  PredHidArgs ha{};
+  ha.d = p->d; ha.B = B; ha.x = x; ha.g = nullptr; ha.be = nullptr; ha.eps = 0.f;
+  ha.AT0 = p->AT; ha.r0 = p->r; ha.hid0 = hid; ha.AT1 = nullptr; ha.r1 = 0; ha.hid1 = nullptr;
+  DV_LAUNCH("pred_hidden", hs, launch_pred_hidden(p->wtype, ha, hs));
+  PredScoreArgs sa{};
+  sa.r0 = p->r; sa.n0 = p->n_out; sa.BT0 = p->BT; sa.hid0 = hid; sa.s0 = s;
+  sa.r1 = 0; sa.n1 = 0; sa.B = B;
+  DV_LAUNCH("pred_scores", hs, launch_pred_scores(p->wtype, sa, hs));
+  DV_LAUNCH("select", hs, launch_select(s, B, p->n_out, mode, k, thresh, idx, cap_idx, count, nullptr, hs));
+  return DV_OK;
+}
+
+extern "C" dv_status dv_predict_mlp(const dv_predictor* p, const float* x, int32_t B, int32_t mode,
+                                    int32_t k, float thresh, int32_t* idx, int32_t cap_idx,
+                                    int32_t* count, float* scores, void* ws, size_t ws_bytes,
+                                    uint32_t flags, void* stream) {
+  return predict_impl(p, x, B, mode, k, thresh, idx, cap_idx, count, scores, ws, ws_bytes, flags, stream);
+}
+
+extern "C" dv_status dv_predict_heads(const dv_predictor* p, const float* x, int32_t B, int32_t mode,
+                                      int32_t k, float thresh, int32_t* idx, int32_t cap_idx,
+                                      int32_t* count, float* scores, void* ws, size_t ws_bytes,
+                                      uint32_t flags, void* stream) {
+  return predict_impl(p, x, B, mode, k, thresh, idx, cap_idx, count, scores, ws, ws_bytes, flags, stream);
+}

@@ -1,0 +1,334 @@
+// Workgroup-level set selection over one row of predictor scores.
+//
+// Top-k: the k largest scores, ties broken toward the lower index; threshold:
+// every score >= t (the labelling rule of Algorithm 1). Output is ascending.
+//
+// Method: scores are mapped to order-preserving 32-bit keys. An MSB-first radix
+// select finds the key digit by digit (13, 13, then 6 bits) with LDS histograms of
+// the candidates that still match the prefix found so far; it stops as soon as the
+// digit's bin holds exactly the number of elements still needed. An ordered
+// compaction (two workgroup-wide exclusive scans over contiguous per-thread ranges)
+// then writes the selected indices in ascending order, taking equal keys at the
+// boundary lowest index first. Everything is integer work on keys, so the result is
+// exact and deterministic. Score loads are coalesced and several are kept in flight,
+// since the scores come from L2 and every pass is latency-bound.
+#pragma once
+
+#include <limits.h>
+
+#include "dv_internal.hpp"
+
+namespace dv {
+
+constexpr int kSelBins = 8192;   // LDS histogram bins (13-bit digits)
+// Scratch ints needed by the selection routines for an NT-thread workgroup.
+constexpr int kSelSm(int NT) { return 2 * (NT / 64) + 8; }
+
+__device__ __forceinline__ uint32_t shr32(uint32_t v, int s) { return s >= 32 ? 0u : (v >> s); }
+
+// Find the digit holding the krem-th largest candidate: bins above it hold `above`
+// (< krem) candidates, and above + hist[digit] >= krem. sm: >= NT/64 + 2 ints.
+template <int NT>
+__device__ __forceinline__ void find_digit(const uint32_t* hist, int nb, int krem, int* sm,
+                                           int* digit, int* above) {
+  const int R = (nb + NT - 1) / NT;
+  const int b0 = threadIdx.x * R;
+  int local = 0;
+  for (int j = 0; j < R; ++j)
+    if (b0 + j < nb) local += (int)hist[b0 + j];
+  int tot;
+  const int pre = block_excl_scan<NT>(local, sm, &tot);
+  const int suffix = tot - pre - local;   // candidates in bins owned by higher threads
+  if (suffix < krem && krem <= suffix + local) {
+    int run = suffix;
+    for (int j = R - 1; j >= 0; --j) {
+      const int b = b0 + j;
+      if (b >= nb) continue;
+      const int c = (int)hist[b];
+      if (run + c >= krem) {
+        sm[NT / kWave] = b;
+        sm[NT / kWave + 1] = run;
+        break;
+      }
+      run += c;
+    }
+  }
+  __syncthreads();
+  *digit = sm[NT / kWave];
+  *above = sm[NT / kWave + 1];
+}
+
+// Select over s[0..n). Writes the set to out[0..min(count, cap)) (and out2 if not
+// NULL) and the set size to *count_out (if not NULL). hist: kSelBins u32 of LDS;
+// sm: kSelSm(NT) ints of LDS. Called by the whole workgroup.
+template <int NT>
+__device__ void wg_select(const float* __restrict__ s, int n, int mode, int k, float thresh,
+                          int32_t* __restrict__ out, int cap, int32_t* __restrict__ count_out,
+                          int32_t* __restrict__ out2, uint32_t* hist, int* sm) {
+  const int tid = threadIdx.x;
+  uint32_t prefix = 0u;
+  int pbits = 0;
+  int eq_take = INT_MAX;
+  bool all = false;
+  if (mode == DV_SELECT_THRESHOLD) {
+    prefix = fkey(thresh);
+    pbits = 32;
+  } else if (k >= n) {
+    all = true;
+  } else if (k <= 0) {
+    if (tid == 0 && count_out) *count_out = 0;
+    return;
+  } else {
+    int krem = k;
+    for (int p = 0; p < 3; ++p) {
+      const int D = p < 2 ? 13 : 6, nb = 1 << D;   // 13 + 13 + 6 = 32 key bits
+      for (int i = tid; i < nb; i += NT) hist[i] = 0u;
+      __syncthreads();
+      const int lo = 32 - pbits - D;
+      const int hi = 32 - pbits;
+      for (int b = 0; b < n; b += NT * 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int i = b + u * NT + tid;
+          v[u] = i < n ? s[i] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const uint32_t key = fkey(v[u]);
+          if (b + u * NT + tid < n && (pbits == 0 || shr32(key, hi) == prefix))
+            atomicAdd(&hist[(key >> lo) & (uint32_t)(nb - 1)], 1u);
+        }
+      }
+      __syncthreads();
+      int dig, above;
+      find_digit<NT>(hist, nb, krem, sm, &dig, &above);
+      const int cnt = (int)hist[dig];
+      krem -= above;
+      prefix = (prefix << D) | (uint32_t)dig;
+      pbits += D;
+      __syncthreads();
+      if (cnt == krem) {          // the whole bin is selected: a strict key prefix test suffices
+        eq_take = INT_MAX;
+        break;
+      }
+      eq_take = krem;             // ties at the full key: lowest indices first
+    }
+  }
+
+  // Ordered compaction. Wavefront w owns the contiguous segment [w*seg, (w+1)*seg)
+  // and walks it 64 scores at a time (coalesced loads, kUnroll in flight); ranks
+  // within a group come from ballots, across groups from running counts, across
+  // wavefronts from one exclusive scan of the per-wavefront totals.
+  constexpr int NW = NT / kWave;
+  constexpr int kUnroll = 8;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int seg = ((n + NW - 1) / NW + 63) & ~63;
+  const int w0 = min(n, wave * seg), w1 = min(n, w0 + seg);
+  const int sh = 32 - pbits;
+  int cgt = 0, ceq = 0;
+  for (int b = w0; b < w1; b += 64 * kUnroll) {
+    float v[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int i = b + u * 64 + lane;
+      v[u] = i < w1 ? s[i] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int i = b + u * 64 + lane;
+      const uint32_t key = shr32(fkey(v[u]), sh);
+      const bool in = i < w1;
+      cgt += __popcll(__ballot(in && (all || key > prefix)));
+      ceq += __popcll(__ballot(in && !all && key == prefix));
+    }
+  }
+  if (lane == 0) {
+    sm[2 * wave] = cgt;
+    sm[2 * wave + 1] = ceq;
+  }
+  __syncthreads();
+  int rg = 0, re = 0, tgt = 0, teq = 0;
+  for (int w = 0; w < NW; ++w) {
+    if (w < wave) {
+      rg += sm[2 * w];
+      re += sm[2 * w + 1];
+    }
+    tgt += sm[2 * w];
+    teq += sm[2 * w + 1];
+  }
+  const int total = tgt + min(teq, eq_take);
+  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int b = w0; b < w1; b += 64 * kUnroll) {
+    float v[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int i = b + u * 64 + lane;
+      v[u] = i < w1 ? s[i] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int i = b + u * 64 + lane;
+      const uint32_t key = shr32(fkey(v[u]), sh);
+      const bool in = i < w1;
+      const bool gt = in && (all || key > prefix);
+      const bool eq = in && !all && key == prefix;
+      const uint64_t bg = __ballot(gt), be = __ballot(eq);
+      const int pg = rg + __popcll(bg & below);
+      const int pe = re + __popcll(be & below);
+      if (gt || (eq && pe < eq_take)) {
+        const int p = pg + min(pe, eq_take);
+        if (p < cap) {
+          out[p] = i;
+          if (out2) out2[p] = i;
+        }
+      }
+      rg += __popcll(bg);
+      re += __popcll(be);
+    }
+  }
+  if (tid == 0 && count_out) *count_out = total;
+  __syncthreads();
+}
+
+// The same selection with every key held in registers: thread t holds the keys of
+// the contiguous indices [t*IPT, (t+1)*IPT) (IPT % 4 == 0), loaded once with 16-byte
+// loads; all radix passes and the ordered compaction (per-thread counts, two
+// workgroup-wide exclusive scans, then an in-order walk) run on-chip with no further
+// memory round trips. Requires n <= NT * IPT (16-byte loads when s is aligned).
+//
+// Slots past n hold key 0, which no real score produces (every finite or infinite
+// float maps above 2^22), so they fall in the lowest histogram bin, never match a
+// selected prefix, and need no separate validity test. The selection boundary is
+// re-read from LDS before the write walk so the compiler recomputes the per-key
+// predicates instead of keeping IPT of them live across the scans.
+template <int NT, int IPT>
+__device__ void wg_select_reg(const float* __restrict__ s, int n, int mode, int k, float thresh,
+                              int32_t* __restrict__ out, int cap, int32_t* __restrict__ count_out,
+                              int32_t* __restrict__ out2, uint32_t* hist, int* sm) {
+  static_assert(IPT % 4 == 0, "IPT must be a multiple of 4");
+  const int tid = threadIdx.x;
+  const int i0 = tid * IPT;
+  const bool vec = (reinterpret_cast<uintptr_t>(s) & 15u) == 0;
+  uint32_t key[IPT];
+#pragma unroll
+  for (int j = 0; j < IPT; j += 4) {
+    if (vec && i0 + j + 3 < n) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(s + i0 + j);
+      key[j] = fkey(v[0]);
+      key[j + 1] = fkey(v[1]);
+      key[j + 2] = fkey(v[2]);
+      key[j + 3] = fkey(v[3]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) key[j + e] = i0 + j + e < n ? fkey(s[i0 + j + e]) : 0u;
+    }
+  }
+  uint32_t prefix = 0u;
+  int pbits = 0;
+  int eq_take = INT_MAX;
+  if (mode == DV_SELECT_THRESHOLD) {
+    prefix = fkey(thresh);
+    pbits = 32;
+  } else if (k >= n) {
+    prefix = 0u;          // every real key is > 0
+    pbits = 32;
+  } else if (k <= 0) {
+    if (tid == 0 && count_out) *count_out = 0;
+    __syncthreads();
+    return;
+  } else {
+    int krem = k;
+    for (int p = 0; p < 3; ++p) {
+      const int D = p < 2 ? 13 : 6, nb = 1 << D;   // 13 + 13 + 6 = 32 key bits
+      for (int i = tid; i < nb; i += NT) hist[i] = 0u;
+      __syncthreads();
+      const int lo = 32 - pbits - D;
+      const int hi = 32 - pbits;
+#pragma unroll
+      for (int j = 0; j < IPT; ++j) {
+        if (shr32(key[j], hi) == prefix) atomicAdd(&hist[(key[j] >> lo) & (uint32_t)(nb - 1)], 1u);
+      }
+      __syncthreads();
+      int dig, above;
+      find_digit<NT>(hist, nb, krem, sm, &dig, &above);
+      const int cnt = (int)hist[dig];
+      krem -= above;
+      prefix = (prefix << D) | (uint32_t)dig;
+      pbits += D;
+      __syncthreads();
+      if (cnt == krem) {
+        eq_take = INT_MAX;
+        break;
+      }
+      eq_take = krem;
+    }
+  }
+  volatile int* bound = sm + 2 * (NT / kWave) + 4;   // prefix, shift
+  if (tid == 0) {
+    bound[0] = (int)prefix;
+    bound[1] = 32 - pbits;
+  }
+  int sh = 32 - pbits;
+  int ngt = 0, neq = 0;
+#pragma unroll
+  for (int j = 0; j < IPT; ++j) {
+    const uint32_t u = shr32(key[j], sh);
+    ngt += u > prefix;
+    neq += u == prefix;
+  }
+  int tgt, teq;
+  int rg = block_excl_scan<NT>(ngt, sm, &tgt);
+  int re = block_excl_scan<NT>(neq, sm, &teq);
+  const int total = tgt + min(teq, eq_take);
+  prefix = (uint32_t)bound[0];
+  sh = bound[1];
+#pragma unroll
+  for (int j = 0; j < IPT; ++j) {
+    const uint32_t u = shr32(key[j], sh);
+    const bool gt = u > prefix;
+    const bool eq = u == prefix;
+    if (gt || (eq && re < eq_take)) {
+      const int p = rg + min(re, eq_take);
+      if (p < cap) {
+        out[p] = i0 + j;
+        if (out2) out2[p] = i0 + j;
+      }
+    }
+    rg += gt;
+    re += eq;
+  }
+  if (tid == 0 && count_out) *count_out = total;
+  __syncthreads();
+}
+
+// Top-k of a short score vector (n <= NT) by rank counting; writes the ascending set
+// to lds_set[0..k). The keys are staged in LDS first (one coalesced load each), then
+// every thread ranks its key against all of them: O(n^2) LDS compares, used for the
+// head selection inside other kernels. keys: n u32 of LDS; sel: n ints of LDS.
+// Ends with a barrier.
+template <int NT>
+__device__ void wg_topk_small(const float* __restrict__ s, int n, int k, uint32_t* keys, int* sel,
+                              int32_t* lds_set) {
+  const int i = threadIdx.x;
+  if (i < n) keys[i] = fkey(s[i]);
+  __syncthreads();
+  if (i < n) {
+    const uint32_t ki = keys[i];
+    int rank = 0;
+    for (int j = 0; j < n; ++j) {
+      const uint32_t kj = keys[j];
+      rank += (kj > ki) || (kj == ki && j < i);
+    }
+    sel[i] = rank < k;
+  }
+  __syncthreads();
+  if (i < n && sel[i]) {
+    int p = 0;
+    for (int j = 0; j < i; ++j) p += sel[j];
+    lds_set[p] = i;
+  }
+  __syncthreads();
+}
+
+}  // namespace dv

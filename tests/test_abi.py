@@ -1,0 +1,130 @@
+"""The C ABI without a GPU: the library loads, exports every function include/dv.h
+declares, and rejects bad arguments on the host before any device call.
+
+Pointers here are fake (aligned, non-NULL integers). Every call below fails host
+validation, so no HIP API is reached.
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2310_17157_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dv.h")
+FAKE = 0x10000000          # 256-byte aligned fake device address
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(dv_[a-z_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return B.load()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = _declared()
+    assert {"dv_predict_mlp", "dv_predict_heads", "dv_sparse_mlp", "dv_sparse_attn",
+            "dv_sparse_block"} <= set(names)
+    out = subprocess.run(["nm", "-D", "--defined-only", B.lib_path()], capture_output=True, text=True).stdout
+    exported = set(re.findall(r"\bT (dv_\w+)", out))
+    missing = [n for n in names if n not in exported]
+    assert not missing, missing
+    for n in names:
+        assert hasattr(lib, n)
+
+
+def test_status_strings_and_version(lib):
+    assert lib.dv_abi_version() == 1
+    for s in range(10):
+        assert lib.dv_status_string(s)
+    assert lib.dv_status_string(99) == b"unknown status"
+
+
+def _mlp(d=64, n=128, wtype=B.DV_F16):
+    return B.CMlp(d, n, wtype, 0, FAKE, None, FAKE, None)
+
+
+def _call_mlp(lib, m, x=FAKE, Bn=1, idx=FAKE, n_idx=8, per_seq=0, mode=0, out=FAKE, ws=FAKE,
+              ws_bytes=1 << 30, flags=0):
+    return lib.dv_sparse_mlp(ctypes.byref(m) if m is not None else None, x, Bn, idx, n_idx, per_seq, mode,
+                             out, ws, ws_bytes, flags, None)
+
+
+def test_sparse_mlp_validation(lib):
+    assert _call_mlp(lib, None) == 1                                   # NULL
+    assert _call_mlp(lib, _mlp(), x=None) == 1
+    assert _call_mlp(lib, _mlp(wtype=7)) == 3                         # dtype
+    assert _call_mlp(lib, _mlp(d=60)) == 4                            # fp16 row not 16-byte multiple
+    assert _call_mlp(lib, _mlp(), x=FAKE + 4) == 4                    # misaligned x
+    assert _call_mlp(lib, _mlp(), n_idx=129) == 2                     # k > n
+    assert _call_mlp(lib, _mlp(), Bn=0) == 2
+    assert _call_mlp(lib, _mlp(), per_seq=2) == 9
+    assert _call_mlp(lib, _mlp(), mode=5) == 9
+    assert _call_mlp(lib, _mlp(), flags=1 << 7) == 9
+    assert _call_mlp(lib, _mlp(), ws=None) == 5
+    assert _call_mlp(lib, _mlp(), ws=FAKE + 16) == 5
+    assert _call_mlp(lib, _mlp(), ws_bytes=16) == 5
+    m = _mlp()
+    need = lib.dv_sparse_mlp_workspace_bytes(ctypes.byref(m), 1, 8, 0)
+    assert need > 0 and need % 256 == 0
+    assert _call_mlp(lib, _mlp(), ws_bytes=need - 1) == 5
+
+
+def _attn(d=64, H=4, dh=16):
+    return B.CAttn(d, H, dh, B.DV_F16, FAKE, FAKE, FAKE, None, None, None, FAKE, None)
+
+
+def _kv(Bn=1, H=4, dh=16, cap=10, pos=(3,)):
+    arr = (ctypes.c_int32 * len(pos))(*pos)
+    kv = B.CKV(Bn, H, dh, cap, B.DV_F16, 0, FAKE, FAKE, ctypes.cast(arr, ctypes.POINTER(ctypes.c_int32)))
+    kv._keep = arr
+    return kv
+
+
+def test_sparse_attn_validation(lib):
+    a, kv = _attn(), _kv()
+    call = lambda a=a, kv=kv, n_heads=2, scale=0.25, ws_bytes=1 << 30, x=FAKE: lib.dv_sparse_attn(
+        ctypes.byref(a), x, 1, ctypes.byref(kv), FAKE, n_heads, scale, FAKE, FAKE, ws_bytes, 0, None)
+    assert call(x=None) == 1
+    assert call(n_heads=5) == 2                                       # more heads than H
+    assert call(kv=_kv(pos=(10,))) == 2                               # pos >= cap
+    assert call(kv=_kv(pos=(-1,))) == 2
+    assert call(kv=_kv(H=3)) == 2                                     # cache/head mismatch
+    assert call(kv=_kv(dh=4)) == 2
+    assert call(scale=float("nan")) == 9
+    assert call(ws_bytes=0) == 5
+    need = lib.dv_sparse_attn_workspace_bytes(ctypes.byref(a), ctypes.byref(kv), 1, 2)
+    assert need > 0 and call(ws_bytes=need - 256) == 5
+
+
+def test_predict_and_block_validation(lib):
+    p = B.CPredictor(64, 16, 128, B.DV_F16, FAKE, FAKE)
+    call = lambda p=p, k=8, mode=0, cap=8, x=FAKE: lib.dv_predict_mlp(
+        ctypes.byref(p), x, 1, mode, k, 0.0, FAKE, cap, FAKE, None, FAKE, 1 << 30, 0, None)
+    assert call(x=None) == 1
+    assert call(k=129) == 2
+    assert call(cap=4) == 2                                           # cap_idx < k
+    assert call(mode=3) == 9
+    assert call(p=B.CPredictor(64, 12, 128, B.DV_F16, FAKE, FAKE)) == 4   # r % 8 != 0
+    assert lib.dv_predict_workspace_bytes(ctypes.byref(p), 1) > 0
+
+    a, m, kv = _attn(), _mlp(), _kv()
+    ph = B.CPredictor(64, 16, 4, B.DV_F16, FAKE, FAKE)
+    pm = B.CPredictor(64, 16, 128, B.DV_F16, FAKE, FAKE)
+    blk = lambda ph=ph, pm=pm, kh=2, km=8, mode=0, ws_bytes=1 << 30: lib.dv_sparse_block(
+        ctypes.byref(a), ctypes.byref(m), ctypes.byref(ph), ctypes.byref(pm), None, ctypes.byref(kv),
+        FAKE, FAKE + 4096, 1, kh, km, mode, 0, 0.25, None, None, FAKE, ws_bytes, 0, None)
+    assert blk(ph=B.CPredictor(64, 16, 5, B.DV_F16, FAKE, FAKE)) == 2   # head predictor n_out != H
+    assert blk(kh=0) == 2
+    assert blk(km=129) == 2
+    assert blk(mode=4) == 9
+    assert blk(pm=B.CPredictor(64, 16, 128, B.DV_F32, FAKE, FAKE)) == 3  # predictor dtypes differ
+    assert blk(ws_bytes=1) == 5
