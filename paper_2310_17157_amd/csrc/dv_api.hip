@@ -85,7 +85,6 @@ extern "C" const char* dv_launch_label(int32_t i) {
 static bool dtype_ok(int t) { return t == DV_F16 || t == DV_F32; }
 static int chunk_elems(int t) { return 16 / elem_bytes(t); }
 static bool ws_ok(void* ws) { return ws != nullptr && (reinterpret_cast<uintptr_t>(ws) & 255u) == 0; }
-static constexpr int kMaxSplit = 64;   // row splits of the gathered axpy
 static constexpr int kMaxWidth = 16000;
 
 static dv_status check_mlp(const dv_mlp* m) {
@@ -140,24 +139,18 @@ static dv_status validate_sets(const int32_t* set, int B, int n, int range, int3
   return bad ? DV_ERR_INDEX : DV_OK;
 }
 
-// Gathered row-axpy, then (with more than one row range) the fixed-order reduction.
 static dv_status enqueue_axpy(const char* label, int wtype, const AxpyArgs& ax, hipStream_t hs) {
   DV_LAUNCH(label, hs, launch_axpy(wtype, ax, hs));
-  if (ax.n_rsplit > 1) {
-    const char* rl = label[0] == 'f' ? "fc2_reduce" : "oproj_reduce";
-    DV_LAUNCH(rl, hs, launch_reduce(ax.partial, ax.n_rsplit, ax.d, ax.resid, ax.bias, ax.out, ax.out2, hs));
-  }
   return DV_OK;
 }
 
 // ---------------------------------------------------------------- sparse MLP
 struct MlpWs {
-  float* h; float* partial; int32_t* flag;
+  float* h; int32_t* flag;
 };
 
 static size_t mlp_ws_layout(const dv_mlp* m, int B, int n_idx, Workspace& w, MlpWs* o) {
   o->h = w.take<float>((size_t)B * n_idx * sizeof(float));
-  o->partial = w.take<float>((size_t)kMaxSplit * B * m->d * sizeof(float));
   o->flag = w.take<int32_t>(sizeof(int32_t));
   return w.off;
 }
@@ -200,25 +193,22 @@ extern "C" dv_status dv_sparse_mlp(const dv_mlp* m, const float* x, int32_t B, c
   AxpyArgs ax{};
   ax.d = m->d; ax.nrows = n_idx; ax.M = m->W2T; ax.m_rows = m->n; ax.set = idx; ax.dh = 0;
   ax.coef = o.h; ax.resid = nullptr; ax.bias = m->b2; ax.out = out; ax.out2 = nullptr;
-  ax.partial = o.partial;
-  ax.n_rsplit = axpy_rsplit(n_idx, m->d, m->wtype, &ax.rows_per_split);
   if ((st = enqueue_axpy("fc2", m->wtype, ax, hs)) != DV_OK) return st;
   return DV_OK;
 }
 
 // ---------------------------------------------------------- sparse attention
 struct AttnWs {
-  int32_t* heads; float* q; float* part; float* partial; int32_t* flag;
+  int32_t* heads; float* q; float* part; int32_t* flag;
 };
 
-// Upper bound of split-KV chunks: attn_chunk never returns fewer than 16 positions.
-static int max_split(int cap) { return (cap + 15) / 16; }
+// Upper bound of split-KV chunks per head.
+static int max_split(int) { return kAttnMaxSplit; }
 
 static size_t attn_ws_layout(const dv_attn* a, int cap, int B, int n_heads, Workspace& w, AttnWs* o) {
   o->heads = w.take<int32_t>((size_t)B * n_heads * sizeof(int32_t));
   o->q = w.take<float>((size_t)B * n_heads * a->dh * sizeof(float));
   o->part = w.take<float>((size_t)B * n_heads * max_split(cap) * (a->dh + 2) * sizeof(float));
-  o->partial = w.take<float>((size_t)kMaxSplit * B * a->d * sizeof(float));
   o->flag = w.take<int32_t>(sizeof(int32_t));
   return w.off;
 }
@@ -278,8 +268,7 @@ extern "C" dv_status dv_sparse_attn(const dv_attn* a, const float* x, int32_t B,
     // MHA over the empty set is bo (or zero): one axpy over no rows writes it.
     AxpyArgs ax{};
     ax.d = a->d; ax.nrows = 0; ax.M = a->WoT; ax.m_rows = a->H * a->dh; ax.set = o.heads; ax.dh = 0;
-    ax.coef = o.q; ax.bias = a->bo; ax.out = out; ax.partial = o.partial;
-    ax.n_rsplit = 1; ax.rows_per_split = 1;
+    ax.coef = o.q; ax.bias = a->bo; ax.out = out;
     DV_LAUNCH("oproj", hs, launch_axpy(a->wtype, ax, hs));
     return DV_OK;
   }
@@ -296,15 +285,13 @@ extern "C" dv_status dv_sparse_attn(const dv_attn* a, const float* x, int32_t B,
   ax.d = a->d; ax.nrows = n_heads * a->dh; ax.M = a->WoT; ax.m_rows = a->H * a->dh; ax.set = o.heads;
   ax.dh = a->dh; ax.coef = nullptr; ax.part = o.part; ax.n_split = attn_nsplit(a, kv, n_heads);
   ax.resid = nullptr; ax.bias = a->bo; ax.out = out; ax.out2 = nullptr;
-  ax.partial = o.partial;
-  ax.n_rsplit = axpy_rsplit(ax.nrows, a->d, a->wtype, &ax.rows_per_split);
   return enqueue_axpy("oproj", a->wtype, ax, hs);
 }
 
 // ------------------------------------------------------------- decoder layer
 struct BlockWs {
   float* hid_h; float* hid_m; float* s_h; float* s_m; int32_t* heads; int32_t* idx;
-  float* q; float* part; float* ytilde; float* h; float* partial; int32_t* flag;
+  float* q; float* part; float* ytilde; float* xhat; float* h; int32_t* flag;
 };
 
 static size_t block_ws_layout(const dv_attn* a, const dv_mlp* m, const dv_predictor* pa,
@@ -319,8 +306,8 @@ static size_t block_ws_layout(const dv_attn* a, const dv_mlp* m, const dv_predic
   o->q = w.take<float>((size_t)B * kh * a->dh * sizeof(float));
   o->part = w.take<float>((size_t)B * kh * max_split(cap) * (a->dh + 2) * sizeof(float));
   o->ytilde = w.take<float>((size_t)B * a->d * sizeof(float));
+  o->xhat = w.take<float>((size_t)B * a->d * sizeof(float));
   o->h = w.take<float>((size_t)B * km * sizeof(float));
-  o->partial = w.take<float>((size_t)kMaxSplit * B * a->d * sizeof(float));
   o->flag = w.take<int32_t>(sizeof(int32_t));
   return w.off;
 }
@@ -392,6 +379,7 @@ extern "C" dv_status dv_sparse_block(const dv_attn* a, const dv_mlp* m, const dv
   ha.d = a->d; ha.B = 1; ha.x = x_in; ha.g = g1; ha.be = be1; ha.eps = eps;
   ha.AT0 = pa->AT; ha.r0 = pa->r; ha.hid0 = o.hid_h;
   ha.AT1 = ahead ? pm->AT : nullptr; ha.r1 = ahead ? pm->r : 0; ha.hid1 = o.hid_m;
+  ha.xhat_out = o.xhat;   // LN1(y), reused by the QKV launch
   DV_LAUNCH("pred_hidden", hs, launch_pred_hidden(pa->wtype, ha, hs));
   // 2. Predictor scores.
   PredScoreArgs sa{};
@@ -399,14 +387,10 @@ extern "C" dv_status dv_sparse_block(const dv_attn* a, const dv_mlp* m, const dv
   sa.r1 = ahead ? pm->r : 0; sa.n1 = ahead ? m->n : 0; sa.BT1 = pm->BT; sa.hid1 = o.hid_m; sa.s1 = o.s_m;
   sa.B = 1;
   DV_LAUNCH("pred_scores", hs, launch_pred_scores(pa->wtype, sa, hs));
-  // 3. Neuron selection (look-ahead: from the LN1(y) scores), then head selection +
-  //    gathered QKV + cache append.
-  if (ahead)
-    DV_LAUNCH("select_mlp", hs,
-              launch_select(o.s_m, 1, m->n, DV_SELECT_TOPK, k_mlp, 0.f, o.idx, k_mlp, nullptr, idx_out, hs));
+  // 3. Head selection + gathered QKV + cache append.
   QkvArgs q{};
   q.d = a->d; q.H = a->H; q.dh = a->dh; q.cap = kv->cap; q.pos = kv->pos[0]; q.n_heads = k_heads;
-  q.x = x_in; q.g = g1; q.be = be1; q.eps = eps;
+  q.x = o.xhat; q.g = nullptr; q.be = nullptr; q.eps = 0.f;
   q.Wq = a->Wq; q.Wk = a->Wk; q.Wv = a->Wv; q.bq = a->bq; q.bk = a->bk; q.bv = a->bv;
   q.K = kv->K; q.V = kv->V; q.q = o.q; q.heads_in = nullptr; q.head_scores = o.s_h;
   q.heads_ws = o.heads; q.heads_out = heads_out;
@@ -415,13 +399,16 @@ extern "C" dv_status dv_sparse_block(const dv_attn* a, const dv_mlp* m, const dv
   AttnWs ao{};
   ao.heads = o.heads; ao.q = o.q; ao.part = o.part;
   if ((st = enqueue_attention(a, kv, ao, k_heads, scale, hs)) != DV_OK) return st;
-  // 5. Out-projection + residual: y~ = y + MHA(LN1(y)).
+  // 5. Out-projection + residual: y~ = y + MHA(LN1(y)). Look-ahead: the neuron
+  //    selection (from the LN1(y) scores) runs in one extra workgroup of this launch,
+  //    beside the out-projection's weight stream, off the critical path (Section 4.3).
   AxpyArgs ax{};
   ax.d = a->d; ax.nrows = k_heads * a->dh; ax.M = a->WoT; ax.m_rows = a->H * a->dh; ax.set = o.heads;
   ax.dh = a->dh; ax.coef = nullptr; ax.part = o.part; ax.n_split = attn_nsplit(a, kv, k_heads);
   ax.resid = x_in; ax.bias = a->bo; ax.out = o.ytilde; ax.out2 = nullptr;
-  ax.partial = o.partial;
-  ax.n_rsplit = axpy_rsplit(ax.nrows, a->d, a->wtype, &ax.rows_per_split);
+  if (ahead) {
+    ax.sel_n = m->n; ax.sel_scores = o.s_m; ax.sel_k = k_mlp; ax.sel_idx = o.idx; ax.sel_idx_out = idx_out;
+  }
   if ((st = enqueue_axpy("oproj", a->wtype, ax, hs)) != DV_OK) return st;
   // 5b. Sequential mode: the neuron predictor reads LN2(y~).
   if (!ahead) {
@@ -444,8 +431,6 @@ extern "C" dv_status dv_sparse_block(const dv_attn* a, const dv_mlp* m, const dv
   AxpyArgs ay{};
   ay.d = m->d; ay.nrows = k_mlp; ay.M = m->W2T; ay.m_rows = m->n; ay.set = o.idx; ay.dh = 0;
   ay.coef = o.h; ay.resid = o.ytilde; ay.bias = m->b2; ay.out = x_out; ay.out2 = nullptr;
-  ay.partial = o.partial;
-  ay.n_rsplit = axpy_rsplit(k_mlp, m->d, m->wtype, &ay.rows_per_split);
   if ((st = enqueue_axpy("fc2", m->wtype, ay, hs)) != DV_OK) return st;
   return DV_OK;
 }

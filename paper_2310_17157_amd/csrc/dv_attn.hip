@@ -12,6 +12,7 @@
 #include <math.h>
 
 #include "dv_internal.hpp"
+#include "dv_rowdot.hpp"
 #include "dv_select.hpp"   // wg_topk_small
 
 namespace dv {
@@ -20,6 +21,7 @@ template <typename T, typename KT, int NW, int U>
 __global__ void __launch_bounds__(NW * 64) k_qkv(QkvArgs a) {
   extern __shared__ float smem[];
   constexpr int NT = NW * 64;
+  const int wg = blockIdx.x, nwg = gridDim.x;
   float* xs = smem;
   float* red = smem + a.d;
   int32_t* hset = reinterpret_cast<int32_t*>(red + NW);
@@ -31,64 +33,44 @@ __global__ void __launch_bounds__(NW * 64) k_qkv(QkvArgs a) {
   } else {
     wg_topk_small<NT>(a.head_scores, a.H, a.n_heads, hkeys, tmp, hset);
   }
-  if (blockIdx.x == 0) {
+  if (wg == 0) {
     for (int i = threadIdx.x; i < a.n_heads; i += NT) {
       a.heads_ws[i] = hset[i];
       if (a.heads_out) a.heads_out[i] = hset[i];
     }
   }
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int per_mat = a.n_heads * a.dh;
-  const int nrows = 3 * per_mat;
-  const int nblk = gridDim.x;
-  struct RowRef { const T* p; int m, rem, head, t; };
-  auto row_ref = [&](int row) {
-    RowRef r;
-    r.m = row / per_mat;
-    r.rem = row - r.m * per_mat;
-    const int j = r.rem / a.dh;
-    r.t = r.rem - j * a.dh;
-    r.head = hset[j];
-    const void* W = r.m == 0 ? a.Wq : (r.m == 1 ? a.Wk : a.Wv);
-    r.p = static_cast<const T*>(W) + ((size_t)r.head * a.dh + r.t) * a.d;
-    return r;
+  auto row_ptr = [&](int row) {
+    const int m = row / per_mat;
+    const int rem = row - m * per_mat;
+    const int j = rem / a.dh, t = rem - j * a.dh;
+    const void* W = m == 0 ? a.Wq : (m == 1 ? a.Wk : a.Wv);
+    return static_cast<const T*>(W) + ((size_t)hset[j] * a.dh + t) * a.d;
   };
-  // Issue the first row's loads before the layer-norm prologue.
-  u32x4 pf[U];
-  {
-    const int row0 = blockIdx.x * NW + wave;
-    if (row0 < nrows) row_prefetch<T, U, 1>(row_ref(row0).p, a.d, lane, 0, pf);
-  }
-  stage_x<T, NT>(a.x, a.d, a.g, a.be, a.eps, xs, red);
-
-  bool first = true;
-  for (int row = blockIdx.x * NW + wave; row < nrows; row += nblk * NW) {
-    const RowRef r = row_ref(row);
-    const int m = r.m, rem = r.rem, head = r.head, t = r.t;
+  auto epi = [&](int row, float v) {
+    const int m = row / per_mat;
+    const int rem = row - m * per_mat;
+    const int j = rem / a.dh, t = rem - j * a.dh;
+    const int head = hset[j];
     const size_t wrow = (size_t)head * a.dh + t;
-    float v = first ? wave_rowdot_pf<T, U, 1>(r.p, xs, a.d, lane, 0, pf) : wave_rowdot<T, U, 1>(r.p, xs, a.d, lane, 0);
-    first = false;
-    if (lane == 0) {
-      const float* bias = m == 0 ? a.bq : (m == 1 ? a.bk : a.bv);
-      if (bias) v += bias[wrow];
-      if (m == 0) {
-        a.q[rem] = v;
-      } else {
-        KT* C = static_cast<KT*>(m == 1 ? a.K : a.V);
-        C[((size_t)head * a.cap + a.pos) * a.dh + t] = (KT)v;
-      }
+    const float* bias = m == 0 ? a.bq : (m == 1 ? a.bk : a.bv);
+    if (bias) v += bias[wrow];
+    if (m == 0) {
+      a.q[rem] = v;
+    } else {
+      KT* C = static_cast<KT*>(m == 1 ? a.K : a.V);
+      C[((size_t)head * a.cap + a.pos) * a.dh + t] = (KT)v;
     }
-  }
+  };
+  rowdot_wave_loop<T, NW, U>(row_ptr, epi, 3 * per_mat, a.d, a.x, a.g, a.be, a.eps, xs, red, nullptr, wg, nwg);
 }
 
 template <typename T, typename KT>
 static hipError_t launch_qkv_t(const QkvArgs& a, hipStream_t st) {
-  constexpr int NW = 8, U = 8;
+  constexpr int NW = 16, U = 8;
   const int nrows = 3 * a.n_heads * a.dh;
-  const int cus = device_cu_count();
-  // Every row is one wavefront task; cap the grid at a few resident workgroups per CU.
-  int blocks = min((nrows + NW - 1) / NW, 2 * cus);
-  blocks = max(blocks, 1);
+  // One workgroup per CU; rows dealt round-robin (one wavefront per row).
+  const int blocks = max(1, min(nrows, device_cu_count()));
   size_t lds = (size_t)(a.d + NW) * sizeof(float) + (size_t)(a.n_heads + 2 * a.H + 4) * sizeof(int32_t);
   hipLaunchKernelGGL((k_qkv<T, KT, NW, U>), dim3(blocks), dim3(NW * 64), lds, st, a);
   return hipGetLastError();
@@ -102,12 +84,16 @@ hipError_t launch_qkv(int wtype, int kvtype, const QkvArgs& a, hipStream_t st) {
 
 // ------------------------------------------------------------ attention
 // LPP lanes hold one cache row (dh elements, 16 bytes per lane); a wavefront covers
-// 64 / LPP positions per step and NSTEP steps; NW wavefronts per workgroup.
+// 64 / LPP positions per step and NSTEP steps per sub-chunk; NW wavefronts per
+// workgroup. A workgroup walks its chunk of positions sub-chunk by sub-chunk with a
+// running max, sum of exponentials and value sum per wavefront (online softmax), so a
+// chunk may be any multiple of the sub-chunk length.
 template <typename KT, int LPP, int NSTEP>
 __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   constexpr int NW = 4;
   constexpr int E = Chunk<KT>::E;
   constexpr int PPW = 64 / LPP;
+  constexpr int SUB = NSTEP * NW * PPW;
   __shared__ float sm_m[NW], sm_l[NW];
   __shared__ float sm_o[NW][256];
   const int j = blockIdx.y, c = blockIdx.x;
@@ -125,49 +111,58 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   const char* Kb = static_cast<const char*>(a.K) + (size_t)head * a.cap * rowb + (size_t)gl * 16;
   const char* Vb = static_cast<const char*>(a.V) + (size_t)head * a.cap * rowb + (size_t)gl * 16;
 
-  u32x4 kw[NSTEP];
-#pragma unroll
-  for (int s = 0; s < NSTEP; ++s) {
-    const int t = t0 + (s * NW + wave) * PPW + grp;
-    kw[s] = (t < tend && lane_on) ? ld_plain(Kb + (size_t)t * rowb) : u32x4{0u, 0u, 0u, 0u};
-  }
-  float sc[NSTEP];
-  float m = -INFINITY;
-#pragma unroll
-  for (int s = 0; s < NSTEP; ++s) {
-    float kv[E];
-    unpack<KT>(kw[s], kv);
-    float p = 0.f;
-#pragma unroll
-    for (int e = 0; e < E; ++e) p = fmaf(qv[e], kv[e], p);
-#pragma unroll
-    for (int o = LPP / 2; o > 0; o >>= 1) p += __shfl_xor(p, o, kWave);
-    const int t = t0 + (s * NW + wave) * PPW + grp;
-    sc[s] = t < tend ? p * a.scale : -INFINITY;
-    m = fmaxf(m, sc[s]);
-  }
-#pragma unroll
-  for (int o = LPP; o < 64; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
-
-  u32x4 vw[NSTEP];
-#pragma unroll
-  for (int s = 0; s < NSTEP; ++s) {
-    const int t = t0 + (s * NW + wave) * PPW + grp;
-    vw[s] = (t < tend && lane_on) ? ld_plain(Vb + (size_t)t * rowb) : u32x4{0u, 0u, 0u, 0u};
-  }
-  float l = 0.f;
+  float m = -INFINITY, l = 0.f;
   float o[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) o[e] = 0.f;
+  for (int sb = t0; sb < tend; sb += SUB) {
+    u32x4 kw[NSTEP], vw[NSTEP];
 #pragma unroll
-  for (int s = 0; s < NSTEP; ++s) {
-    const float p = sc[s] == -INFINITY ? 0.f : __expf(sc[s] - m);
-    l += p;
-    float vv[E];
-    unpack<KT>(vw[s], vv);
+    for (int s = 0; s < NSTEP; ++s) {
+      const int t = sb + (s * NW + wave) * PPW + grp;
+      kw[s] = (t < tend && lane_on) ? ld_plain(Kb + (size_t)t * rowb) : u32x4{0u, 0u, 0u, 0u};
+    }
 #pragma unroll
-    for (int e = 0; e < E; ++e) o[e] = fmaf(p, vv[e], o[e]);
+    for (int s = 0; s < NSTEP; ++s) {
+      const int t = sb + (s * NW + wave) * PPW + grp;
+      vw[s] = (t < tend && lane_on) ? ld_plain(Vb + (size_t)t * rowb) : u32x4{0u, 0u, 0u, 0u};
+    }
+    float sc[NSTEP];
+    float mb = -INFINITY;
+#pragma unroll
+    for (int s = 0; s < NSTEP; ++s) {
+      float kv[E];
+      unpack<KT>(kw[s], kv);
+      float p = 0.f;
+#pragma unroll
+      for (int e = 0; e < E; ++e) p = fmaf(qv[e], kv[e], p);
+#pragma unroll
+      for (int off = LPP / 2; off > 0; off >>= 1) p += __shfl_xor(p, off, kWave);
+      const int t = sb + (s * NW + wave) * PPW + grp;
+      sc[s] = t < tend ? p * a.scale : -INFINITY;
+      mb = fmaxf(mb, sc[s]);
+    }
+#pragma unroll
+    for (int off = LPP; off < 64; off <<= 1) mb = fmaxf(mb, __shfl_xor(mb, off, kWave));
+    const float mn = fmaxf(m, mb);
+    if (mn != -INFINITY) {
+      const float r = m == -INFINITY ? 0.f : __expf(m - mn);
+      l *= r;
+#pragma unroll
+      for (int e = 0; e < E; ++e) o[e] *= r;
+#pragma unroll
+      for (int s = 0; s < NSTEP; ++s) {
+        const float p = sc[s] == -INFINITY ? 0.f : __expf(sc[s] - mn);
+        l += p;
+        float vv[E];
+        unpack<KT>(vw[s], vv);
+#pragma unroll
+        for (int e = 0; e < E; ++e) o[e] = fmaf(p, vv[e], o[e]);
+      }
+      m = mn;
+    }
   }
+  // Each lane's l and o cover its own position group; sum over the groups.
 #pragma unroll
   for (int off = LPP; off < 64; off <<= 1) {
     l += __shfl_xor(l, off, kWave);
@@ -210,40 +205,40 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   }
 }
 
-int attn_chunk(int n_heads, int attended, int dh, int kvtype) {
-  // Positions per workgroup: a multiple of the 4 wavefronts x positions per step, at
-  // most 16 steps per wavefront; prefer long chunks (fewer partials) while keeping
-  // about 2 workgroups per CU busy.
+constexpr int kAttnNStep = 8;
+
+static int attn_lpp(int dh, int kvtype) {
   const int nchr = dh * elem_bytes(kvtype) / 16;
-  const int lpp = nchr <= 16 ? 16 : (nchr <= 32 ? 32 : 64);
-  const int ppw = 64 / lpp;
-  const int cmax = 16 * 4 * ppw, cmin = 4 * 4 * ppw;
-  const int target = 2 * device_cu_count();
-  for (int ch = cmax; ch > cmin; ch >>= 1)
-    if ((long)n_heads * ((attended + ch - 1) / ch) >= target) return ch;
-  return cmin;
+  return nchr <= 16 ? 16 : (nchr <= 32 ? 32 : 64);
+}
+
+int attn_chunk(int n_heads, int attended, int dh, int kvtype) {
+  // Positions per workgroup: a multiple of the sub-chunk (8 steps x 4 wavefronts x
+  // positions per step). At most kAttnMaxSplit chunks per head (they are combined in
+  // the out-projection's prologue); otherwise aim at about one workgroup per CU.
+  const int sub = kAttnNStep * 4 * (64 / attn_lpp(dh, kvtype));
+  const int nsub = (attended + sub - 1) / sub;
+  const int cus = device_cu_count();
+  int per = 1;                                               // sub-chunks per workgroup
+  while ((long)n_heads * ((nsub + per - 1) / per) > cus && per < nsub) per *= 2;
+  while ((nsub + per - 1) / per > kAttnMaxSplit) ++per;
+  return per * sub;
 }
 
 template <typename KT, int LPP>
 static hipError_t launch_attn_l(const AttnArgs& a, hipStream_t st) {
-  constexpr int PPW = 64 / LPP;
-  const int nstep = a.chunk / (4 * PPW);
   dim3 grid(a.n_split, a.n_heads);
-  switch (nstep) {
-    case 4: hipLaunchKernelGGL((k_attn<KT, LPP, 4>), grid, dim3(256), 0, st, a); break;
-    case 8: hipLaunchKernelGGL((k_attn<KT, LPP, 8>), grid, dim3(256), 0, st, a); break;
-    case 16: hipLaunchKernelGGL((k_attn<KT, LPP, 16>), grid, dim3(256), 0, st, a); break;
-    default: return hipErrorInvalidValue;
-  }
+  hipLaunchKernelGGL((k_attn<KT, LPP, kAttnNStep>), grid, dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
 template <typename KT>
 static hipError_t launch_attn_t(const AttnArgs& a, hipStream_t st) {
-  const int nchr = a.dh * (int)sizeof(KT) / 16;
-  if (nchr <= 16) return launch_attn_l<KT, 16>(a, st);
-  if (nchr <= 32) return launch_attn_l<KT, 32>(a, st);
-  return launch_attn_l<KT, 64>(a, st);
+  switch (attn_lpp(a.dh, sizeof(KT) == 2 ? DV_F16 : DV_F32)) {
+    case 16: return launch_attn_l<KT, 16>(a, st);
+    case 32: return launch_attn_l<KT, 32>(a, st);
+    default: return launch_attn_l<KT, 64>(a, st);
+  }
 }
 
 hipError_t launch_attn(int kvtype, const AttnArgs& a, hipStream_t st) {

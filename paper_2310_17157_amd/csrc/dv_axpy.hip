@@ -6,204 +6,229 @@
 // Both weights are stored transposed so that a selected neuron or head is a set of
 // whole contiguous rows (Section 4.4 "Memory coalescing").
 //
-// Tiling: a workgroup owns one column tile (64 lanes x one 16-byte chunk = 1 KB of
-// fp16) and a contiguous range of selected rows; each wavefront streams every NW-th
-// row of that range with U rows in flight and accumulates in registers. Wavefront
-// partials are summed in LDS in a fixed order and written per row range; a small
-// second kernel (k_reduce) adds the ranges in order plus residual and bias. No
-// floating-point atomics and no device-scope fences (on a multi-XCD part a
-// device-scope release writes back the XCD's L2, which costs far more than a second
-// launch): the result is bitwise reproducible.
+// Tiling: a workgroup owns a 128-byte column tile (8 lanes x one 16-byte chunk) of
+// every selected row, so each wavefront load instruction covers 8 rows and each
+// wavefront keeps U such instructions in flight. The workgroup sums all selected rows
+// of its tile, so no cross-workgroup reduction, atomics or device-scope fences are
+// needed (on a multi-XCD part a device-scope release writes back the whole L2 of the
+// XCD). Lane partials are combined across row groups with shuffles and across
+// wavefronts in LDS, in a fixed order: the result is bitwise reproducible.
 //
-// For the attention, the coefficients H_i(y)[t] are first combined from the split-KV
-// partials (max logit, sum of exponentials, unnormalised value sums per chunk).
+// For the attention the coefficients H_i(y)[t] are combined first, in the prologue,
+// from the split-KV partials (max logit, sum of exponentials and unnormalised value
+// sums per position chunk) of every selected head.
 #include <math.h>
 
 #include "dv_internal.hpp"
+#include "dv_select.hpp"
 
 namespace dv {
 
-constexpr int kAxpyNW = 8;
-constexpr int kAxpyU = 8;
+constexpr int kAxNW = 16;   // wavefronts per workgroup
+constexpr int kAxTL = 8;    // lanes (16-byte chunks) per row segment: 128-byte tiles
+constexpr int kAxU = 8;     // row instructions per batch (two batches in flight)
 
-template <typename T, int NW, int U>
-__global__ void __launch_bounds__(NW * 64) k_axpy(AxpyArgs a) {
-  constexpr int E = Chunk<T>::E;
-  extern __shared__ float smem[];
-  const int tile = blockIdx.x, split = blockIdx.y;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int nch = a.d / E;
-  const int c = tile * 64 + lane;
-  const int r0 = split * a.rows_per_split;
-  const int nloc = max(0, min(a.nrows, r0 + a.rows_per_split) - r0);
-  float* cf = smem;                                        // rows_per_split
-  int* ri = reinterpret_cast<int*>(cf + a.rows_per_split); // rows_per_split
-  float* red = reinterpret_cast<float*>(ri + a.rows_per_split);   // NW * 64 * E
+constexpr int kAxMaxSplit = kAttnMaxSplit;   // split-KV chunks, combined with all loads in flight
 
-  for (int i = threadIdx.x; i < nloc; i += NW * 64) {
-    const int row = r0 + i;
-    if (a.dh == 0) {
-      cf[i] = a.coef[row];
-      ri[i] = min(max(a.set[row], 0), a.m_rows - 1);
-    } else {
-      const int j = row / a.dh, t = row - j * a.dh;
-      if (a.coef != nullptr) {
-        cf[i] = a.coef[row];
-      } else {
-        const float* P = a.part + (size_t)j * a.n_split * (a.dh + 2);
-        float M = -INFINITY;
-        for (int s = 0; s < a.n_split; ++s) M = fmaxf(M, P[(size_t)s * (a.dh + 2)]);
-        float L = 0.f, O = 0.f;
-        for (int s = 0; s < a.n_split; ++s) {
-          const float ms = P[(size_t)s * (a.dh + 2)];
-          const float f = ms == -INFINITY ? 0.f : __expf(ms - M);
-          L += P[(size_t)s * (a.dh + 2) + 1] * f;
-          O += P[(size_t)s * (a.dh + 2) + 2 + t] * f;
-        }
-        cf[i] = O / L;
-      }
-      ri[i] = min(max(a.set[j], 0), a.m_rows / a.dh - 1) * a.dh + t;
-    }
+template <typename T, int TL, int U>
+__device__ __forceinline__ void ax_load(u32x4 (&w)[U], const char* Mb, size_t rowb, const int* ri, int r,
+                                        int step, int nb) {
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int row = r + step * u;
+    w[u] = row < nb ? ld_stream(Mb + (size_t)ri[row] * rowb) : u32x4{0u, 0u, 0u, 0u};
   }
-  __syncthreads();
+}
+
+template <typename T, int E, int U>
+__device__ __forceinline__ void ax_consume(const u32x4 (&w)[U], const float* cf, int r, int step, int nb,
+                                           float (&acc)[E]) {
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int row = r + step * u;
+    float v[E];
+    unpack<T>(w[u], v);
+    const float f = row < nb ? cf[row] : 0.f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] = fmaf(f, v[e], acc[e]);
+  }
+}
+
+// Top-k selection hosted by one extra workgroup of an axpy launch. The axpy grid (one
+// workgroup per 128-byte column tile: 192 at d = 12288 in fp16) leaves CUs free, so
+// the selection (about 20-30 us on one CU) runs beside the weight stream instead of
+// on the critical path; it is kept out of line so that its register allocation does
+// not constrain the axpy path. Up to kSelIPT * NT scores are selected from registers,
+// larger score vectors stream from memory.
+constexpr int kSelIPT = 48;
+
+template <int NT>
+__device__ __noinline__ void axpy_hosted_select(const float* scores, int n, int k, int32_t* idx,
+                                                int32_t* idx_out, float* smem) {
+  uint32_t* hist = reinterpret_cast<uint32_t*>(smem);
+  int* sm = reinterpret_cast<int*>(smem + kSelBins);
+  if (n <= NT * kSelIPT)
+    wg_select_reg<NT, kSelIPT>(scores, n, DV_SELECT_TOPK, k, 0.f, idx, k, nullptr, idx_out, hist, sm);
+  else
+    wg_select<NT>(scores, n, DV_SELECT_TOPK, k, 0.f, idx, k, nullptr, idx_out, hist, sm);
+}
+
+template <typename T, int NW, int TL, int U>
+__global__ void __launch_bounds__(NW * 64) k_axpy(AxpyArgs a) {
+  constexpr int NT = NW * 64;
+  extern __shared__ float smem[];
+  if (a.sel_n > 0 && blockIdx.x == gridDim.x - 1) {
+    axpy_hosted_select<NT>(a.sel_scores, a.sel_n, a.sel_k, a.sel_idx, a.sel_idx_out, smem);
+    return;
+  }
+  constexpr int E = Chunk<T>::E;
+  constexpr int RPI = 64 / TL;                  // rows per load instruction
+  constexpr int step = NW * RPI;                // rows per wavefront-group step
+  float* cf = smem;                                              // [rows_per_batch] coefficients
+  int* ri = reinterpret_cast<int*>(cf + a.rows_per_batch);       // [rows_per_batch] row indices
+  float* red = reinterpret_cast<float*>(ri + a.rows_per_batch);  // [NW][TL*E] wavefront sums
+  float* fac = red + NW * TL * E;                                // [heads of a batch][n_split]
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int nch = a.d / E;
+  const int c = blockIdx.x * TL + (lane % TL);
+  const int grp = lane / TL;
+  const bool on = c < nch;
 
   float acc[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) acc[e] = 0.f;
-  if (c < nch) {
-    const char* Mb = static_cast<const char*>(a.M) + (size_t)c * 16;
-    const size_t rowb = (size_t)a.d * sizeof(T);
-    int i = wave;
-    for (; i + NW * (U - 1) < nloc; i += NW * U) {
-      u32x4 w[U];
-#pragma unroll
-      for (int u = 0; u < U; ++u) w[u] = ld_stream(Mb + (size_t)ri[i + NW * u] * rowb);
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        float v[E];
-        unpack<T>(w[u], v);
-        const float f = cf[i + NW * u];
-#pragma unroll
-        for (int e = 0; e < E; ++e) acc[e] = fmaf(f, v[e], acc[e]);
+  const char* Mb = static_cast<const char*>(a.M) + (size_t)(on ? c : 0) * 16;
+  const size_t rowb = (size_t)a.d * sizeof(T);
+  const int ns = a.n_split;
+  const int stride = a.dh + 2;
+
+  // Rows are processed in batches of at most rows_per_batch so that their
+  // coefficients and row indices fit in LDS.
+  for (int rb = 0; rb < a.nrows; rb += a.rows_per_batch) {
+    const int nb = min(a.rows_per_batch, a.nrows - rb);
+    const int h0 = a.dh > 0 ? rb / a.dh : 0;
+    // ---- row indices (they need only the set), then this wavefront's first loads
+    for (int i = tid; i < nb; i += NT) {
+      const int row = rb + i;
+      if (a.dh == 0) {
+        ri[i] = min(max(a.set[row], 0), a.m_rows - 1);
+      } else {
+        const int h = row / a.dh;
+        ri[i] = min(max(a.set[h], 0), a.m_rows / a.dh - 1) * a.dh + (row - h * a.dh);
       }
     }
-    for (; i < nloc; i += NW) {
-      u32x4 w = ld_stream(Mb + (size_t)ri[i] * rowb);
-      float v[E];
-      unpack<T>(w, v);
-      const float f = cf[i];
-#pragma unroll
-      for (int e = 0; e < E; ++e) acc[e] = fmaf(f, v[e], acc[e]);
-    }
-  }
-  // Wavefront partials -> LDS -> fixed-order sum by wavefront 0.
-#pragma unroll
-  for (int e = 0; e < E; ++e) red[(wave * E + e) * 64 + lane] = acc[e];
-  __syncthreads();
-  const bool single = gridDim.y == 1;
-  if (wave == 0 && c < nch) {
-    float s[E];
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-      float t = 0.f;
-#pragma unroll
-      for (int w = 0; w < NW; ++w) t += red[(w * E + e) * 64 + lane];
-      s[e] = t;
-    }
-    if (single) {
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const int col = c * E + e;
-        float v = s[e];
-        if (a.resid) v += a.resid[col];
-        if (a.bias) v += a.bias[col];
-        a.out[col] = v;
-        if (a.out2) a.out2[col] = v;
-      }
+    __syncthreads();
+    const int rfirst = wave * RPI + grp;
+    u32x4 wa[U];
+    if (on) ax_load<T, TL, U>(wa, Mb, rowb, ri, rfirst, step, nb);
+    // ---- coefficients, while those loads are in flight
+    if (a.dh == 0) {
+      for (int i = tid; i < nb; i += NT) cf[i] = a.coef[rb + i];
     } else {
-      float* P = a.partial + (size_t)split * a.d + (size_t)c * E;
+      // fac[h][s] = exp(m_s - M_h) / L_h for the heads of this batch (ns <= kAxMaxSplit)
+      const int h1 = (rb + nb - 1) / a.dh;
+      for (int hh = tid; hh <= h1 - h0; hh += NT) {
+        const float* P = a.part + (size_t)(h0 + hh) * ns * stride;
+        float m[kAxMaxSplit], l[kAxMaxSplit];
+        float M = -INFINITY;
 #pragma unroll
-      for (int e = 0; e < E; ++e) P[e] = s[e];
+        for (int sp = 0; sp < kAxMaxSplit; ++sp) {
+          m[sp] = sp < ns ? P[(size_t)sp * stride] : -INFINITY;
+          l[sp] = sp < ns ? P[(size_t)sp * stride + 1] : 0.f;
+          M = fmaxf(M, m[sp]);
+        }
+        float L = 0.f;
+#pragma unroll
+        for (int sp = 0; sp < kAxMaxSplit; ++sp) {
+          m[sp] = m[sp] == -INFINITY ? 0.f : __expf(m[sp] - M);
+          L += l[sp] * m[sp];
+        }
+        const float inv = 1.f / L;
+#pragma unroll
+        for (int sp = 0; sp < kAxMaxSplit; ++sp)
+          if (sp < ns) fac[hh * ns + sp] = m[sp] * inv;
+      }
+      __syncthreads();
+      for (int i = tid; i < nb; i += NT) {
+        const int row = rb + i;
+        const int h = row / a.dh, t = row - h * a.dh;
+        const float* P = a.part + (size_t)h * ns * stride + 2 + t;
+        const float* F = fac + (h - h0) * ns;
+        float o[kAxMaxSplit];
+#pragma unroll
+        for (int sp = 0; sp < kAxMaxSplit; ++sp) o[sp] = sp < ns ? P[(size_t)sp * stride] : 0.f;
+        float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+        for (int sp = 0; sp < kAxMaxSplit; sp += 2) {
+          if (sp < ns) s0 = fmaf(o[sp], F[sp], s0);
+          if (sp + 1 < ns) s1 = fmaf(o[sp + 1], F[sp + 1], s1);
+        }
+        cf[i] = s0 + s1;
+      }
     }
-  }
-}
+    __syncthreads();
 
-// out[c] = resid[c] + bias[c] + sum_{s < nsplit} partial[s][c]. A workgroup covers 64
-// float4 columns with 4 thread groups; group g sums the splits s = g (mod 4) in
-// increasing order, then the 4 group sums are added in order g = 0..3: a fixed
-// association, so the result is bitwise reproducible.
-__global__ void __launch_bounds__(256) k_reduce(const float* __restrict__ partial, int nsplit, int d,
-                                                const float* __restrict__ resid, const float* __restrict__ bias,
-                                                float* __restrict__ out, float* __restrict__ out2) {
-  __shared__ f32x4 part[4][64];
-  const int col = threadIdx.x & 63, g = threadIdx.x >> 6;
-  const int c4 = blockIdx.x * 64 + col;
-  const bool on = c4 * 4 < d;
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  if (on) {
-    int sp = g;
-    for (; sp + 12 < nsplit; sp += 16) {
-      f32x4 v[4];
+    // ---- stream: wavefront w, row group g takes rows w*RPI + g + k*step, U load
+    // instructions per batch, the next batch issued before the current is consumed.
+    if (on) {
+      for (int r = rfirst; r - grp < nb; r += step * U) {
+        u32x4 wb[U];
+        const bool more = r - grp + step * U < nb;
+        if (more) ax_load<T, TL, U>(wb, Mb, rowb, ri, r + step * U, step, nb);
+        ax_consume<T, E, U>(wa, cf, r, step, nb, acc);
+        if (more) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const f32x4*>(partial + (size_t)(sp + 4 * u) * d + 4 * c4);
-#pragma unroll
-      for (int u = 0; u < 4; ++u) acc += v[u];
+          for (int u = 0; u < U; ++u) wa[u] = wb[u];
+        }
+      }
     }
-    for (; sp < nsplit; sp += 4) acc += *reinterpret_cast<const f32x4*>(partial + (size_t)sp * d + 4 * c4);
+    __syncthreads();
   }
-  part[g][col] = acc;
+  // ---- combine row groups (lanes with equal lane % TL), then wavefronts, in order
+#pragma unroll
+  for (int o = TL; o < 64; o <<= 1)
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] += __shfl_xor(acc[e], o, kWave);
+  if (grp == 0) {
+#pragma unroll
+    for (int e = 0; e < E; ++e) red[wave * TL * E + lane * E + e] = acc[e];
+  }
   __syncthreads();
-  if (g == 0 && on) {
-    f32x4 t = part[0][col];
-    t += part[1][col];
-    t += part[2][col];
-    t += part[3][col];
-    if (resid) t += *reinterpret_cast<const f32x4*>(resid + 4 * c4);
-    if (bias) t += *reinterpret_cast<const f32x4*>(bias + 4 * c4);
-    *reinterpret_cast<f32x4*>(out + 4 * c4) = t;
-    if (out2) *reinterpret_cast<f32x4*>(out2 + 4 * c4) = t;
+  if (tid < TL * E) {
+    const int col = blockIdx.x * TL * E + tid;
+    if (col < a.d) {
+      float s = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) s += red[w * TL * E + tid];
+      if (a.resid) s += a.resid[col];
+      if (a.bias) s += a.bias[col];
+      a.out[col] = s;
+      if (a.out2) a.out2[col] = s;
+    }
   }
-}
-
-hipError_t launch_reduce(const float* partial, int nsplit, int d, const float* resid, const float* bias,
-                         float* out, float* out2, hipStream_t st) {
-  const int n4 = d / 4;
-  hipLaunchKernelGGL(k_reduce, dim3((n4 + 63) / 64), dim3(256), 0, st, partial, nsplit, d, resid, bias, out,
-                     out2);
-  return hipGetLastError();
-}
-
-int axpy_tiles(int d, int wtype) {
-  const int nch = d / (16 / elem_bytes(wtype));
-  return (nch + 63) / 64;
-}
-
-int axpy_rsplit(int nrows, int d, int wtype, int* rows_per_split) {
-  // Aim for about 4 workgroups per CU in total, with at least 4 rows per wavefront
-  // where possible and at most 64 row ranges.
-  if (nrows <= 0) {
-    *rows_per_split = 1;
-    return 1;
-  }
-  const int tiles = axpy_tiles(d, wtype);
-  const int target = 4 * device_cu_count();
-  int splits = (target + tiles - 1) / tiles;
-  const int min_rows = kAxpyNW * 4;
-  splits = max(1, min(splits, (nrows + min_rows - 1) / min_rows));
-  splits = min(splits, 64);
-  int rps = (nrows + splits - 1) / splits;
-  splits = (nrows + rps - 1) / rps;
-  *rows_per_split = max(rps, 1);
-  return max(splits, 1);
 }
 
 template <typename T>
-static hipError_t launch_axpy_t(const AxpyArgs& a, hipStream_t st) {
-  constexpr int NW = kAxpyNW, U = kAxpyU;
+static hipError_t launch_axpy_t(AxpyArgs a, hipStream_t st) {
   constexpr int E = Chunk<T>::E;
-  const int tiles = axpy_tiles(a.d, sizeof(T) == 2 ? DV_F16 : DV_F32);
-  const size_t lds = (size_t)a.rows_per_split * 8 + (size_t)NW * 64 * E * sizeof(float);
-  hipLaunchKernelGGL((k_axpy<T, NW, U>), dim3(tiles, a.n_rsplit), dim3(NW * 64), lds, st, a);
+  const int nch = a.d / E;
+  const int tiles = (nch + kAxTL - 1) / kAxTL;
+  // LDS budget: 40 KB of (coefficient, row index) pairs plus the combine factors of
+  // the heads a batch touches.
+  int rpb = 5120;
+  size_t fac = 0;
+  if (a.dh > 0) {
+    for (;;) {
+      fac = (size_t)(rpb / a.dh + 2) * a.n_split * 4;
+      if (fac <= 16384 || rpb <= 256) break;
+      rpb /= 2;
+    }
+  }
+  a.rows_per_batch = max(1, min(rpb, max(a.nrows, 1)));
+  size_t lds = (size_t)a.rows_per_batch * 8 + (size_t)kAxNW * kAxTL * E * 4 + fac + 16;
+  if (a.sel_n > 0) lds = max(lds, (size_t)kSelBins * 4 + kSelSm(kAxNW * 64) * sizeof(int));
+  const int blocks = tiles + (a.sel_n > 0 ? 1 : 0);
+  hipLaunchKernelGGL((k_axpy<T, kAxNW, kAxTL, kAxU>), dim3(blocks), dim3(kAxNW * 64), lds, st, a);
   return hipGetLastError();
 }
 

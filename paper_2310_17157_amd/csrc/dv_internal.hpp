@@ -266,6 +266,37 @@ __device__ __forceinline__ float wave_rowdot_pf(const T* __restrict__ row, const
   return wave_sum(acc0 + acc1);
 }
 
+// A whole workgroup streams one row: wavefront w of NW takes the chunks
+// c = lane + 64*(w + NW*j), j < JMAX (every chunk of a row of up to 64*NW*JMAX
+// chunks). load() issues the loads; dot() consumes them against the staged x-hat and
+// returns this wavefront's partial sum (in every lane).
+template <typename T, int NW, int JMAX>
+struct WgRow {
+  u32x4 w[JMAX];
+  __device__ __forceinline__ void load(const T* __restrict__ row, int nch, int lane, int wave) {
+    const char* base = reinterpret_cast<const char*>(row);
+#pragma unroll
+    for (int j = 0; j < JMAX; ++j) {
+      const int c = lane + 64 * (wave + NW * j);
+      w[j] = c < nch ? ld_stream(base + (size_t)c * 16) : u32x4{0u, 0u, 0u, 0u};
+    }
+  }
+  __device__ __forceinline__ float dot(const float* xs, int d, int nch, int lane, int wave) const {
+    float acc0 = 0.f, acc1 = 0.f;
+#pragma unroll
+    for (int j = 0; j < JMAX; ++j) {
+      const int c = lane + 64 * (wave + NW * j);
+      if (c < nch) {
+        if (j & 1)
+          acc1 = dot_chunk<T>(w[j], xs, d, c, acc1);
+        else
+          acc0 = dot_chunk<T>(w[j], xs, d, c, acc0);
+      }
+    }
+    return wave_sum(acc0 + acc1);
+  }
+};
+
 // Order-preserving key of a float: a > b  <=>  key(a) > key(b); -0 maps to +0.
 __device__ __forceinline__ uint32_t fkey(float f) {
   uint32_t u = __float_as_uint(f);
@@ -323,6 +354,7 @@ struct PredHidArgs {
   const float* g; const float* be; float eps;
   const void* AT0; int r0; float* hid0;   // [B][r0]
   const void* AT1; int r1; float* hid1;   // [B][r1] (r1 = 0: none)
+  float* xhat_out;                        // optional [B][d]: the normalised input, written once
 };
 hipError_t launch_pred_hidden(int wtype, const PredHidArgs& a, hipStream_t st);
 
@@ -344,7 +376,7 @@ struct QkvArgs {
   float* q;                         // [n_heads][dh] out
   const int32_t* heads_in;          // given head set, or NULL when selecting from scores
   const float* head_scores;         // [H] (when heads_in == NULL)
-  int32_t* heads_ws;                // [n_heads] out: the set used (written by workgroup 0)
+  int32_t* heads_ws;                // [n_heads] out: the set used (written by one workgroup)
   int32_t* heads_out;               // optional caller copy
 };
 hipError_t launch_qkv(int wtype, int kvtype, const QkvArgs& a, hipStream_t st);
@@ -358,10 +390,9 @@ struct AttnArgs {
 hipError_t launch_attn(int kvtype, const AttnArgs& a, hipStream_t st);
 
 // Gathered row-axpy: out = resid + bias + sum_rows coef[row] * M[rowidx(row)], tiled by
-// columns with a split over rows. With one row range the kernel writes out directly;
-// otherwise it writes partial[split][d] and launch_reduce finishes the sum.
+// 128-byte column tiles; every workgroup sums all selected rows of its tile.
 struct AxpyArgs {
-  int d, nrows;
+  int d, nrows;                     // row length, selected rows
   const void* M; int m_rows;        // M is [m_rows][d]
   // Row source: neuron rows (rows = set) or head rows (rows = set[row / dh] * dh + row % dh).
   const int32_t* set; int dh;       // dh = 0: neuron rows
@@ -371,13 +402,11 @@ struct AxpyArgs {
   const float* resid; const float* bias;   // optional, [d]
   float* out;                        // [d]
   float* out2;                       // optional second copy of out
-  float* partial;                    // [n_rsplit][d] scratch
-  int n_rsplit, rows_per_split;
+  int rows_per_batch;                // set by the launcher
+  // Top-k selection run by one extra workgroup of the launch (sel_n == 0: none).
+  const float* sel_scores; int sel_n; int sel_k; int32_t* sel_idx; int32_t* sel_idx_out;
 };
 hipError_t launch_axpy(int wtype, const AxpyArgs& a, hipStream_t st);
-// out = resid + bias + sum over nsplit rows of partial[nsplit][d] (fixed order); d % 4 == 0.
-hipError_t launch_reduce(const float* partial, int nsplit, int d, const float* resid, const float* bias,
-                         float* out, float* out2, hipStream_t st);
 
 // fc1 + ReLU over the selected neurons (B = 1): h[s] = max(x-hat . W1T[set[s]] + b1, 0).
 struct Fc1Args {
@@ -388,9 +417,9 @@ struct Fc1Args {
 };
 hipError_t launch_fc1(int wtype, const Fc1Args& a, hipStream_t st);
 
-// Tiling helpers shared by the host code.
-int axpy_tiles(int d, int wtype);
-int axpy_rsplit(int nrows, int d, int wtype, int* rows_per_split);
+// Split-KV chunk length (positions per attention workgroup); at most kAttnMaxSplit
+// chunks per head.
+constexpr int kAttnMaxSplit = 16;
 int attn_chunk(int n_heads, int attended, int dh, int kvtype);
 
 }  // namespace dv

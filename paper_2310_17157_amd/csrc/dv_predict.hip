@@ -2,82 +2,43 @@
 // selection. A = AT^T is d x r and B = BT^T is r x n; both factors are stored with
 // their output index as the row so every GEMV streams whole contiguous rows.
 #include "dv_internal.hpp"
+#include "dv_rowdot.hpp"
 #include "dv_select.hpp"
 
 namespace dv {
 
-// Combine S partial dots of one row computed by S consecutive wavefronts.
-template <int NW, int S>
-__device__ __forceinline__ float combine_segments(float v, float* lds) {
-  if constexpr (S == 1) {
-    return v;
-  } else {
-    const int wave = threadIdx.x >> 6;
-    if ((threadIdx.x & 63) == 0) lds[wave] = v;
-    __syncthreads();
-    float t = 0.f;
-    if (wave % S == 0) {
-#pragma unroll
-      for (int j = 0; j < S; ++j) t += lds[wave + j];
-    }
-    __syncthreads();
-    return t;
-  }
-}
-
 // ----------------------------------------------------------- hidden layer
-// One wavefront (or S of them) per predictor row; x-hat staged once per workgroup.
-template <typename T, int NW, int S, int U>
+// h[b][j] = x-hat[b] . AT[j] for the rows of up to two predictors; one wavefront per
+// row, rows dealt round-robin over one workgroup per CU.
+template <typename T, int NW, int U>
 __global__ void __launch_bounds__(NW * 64) k_pred_hidden(PredHidArgs a) {
   extern __shared__ float smem[];
   float* xs = smem;
-  float* red = smem + a.d;          // NW floats (block sums)
-  float* seg = red + NW;            // NW floats (segment combine)
-  constexpr int NT = NW * 64;
+  float* red = smem + a.d;
   const int b = blockIdx.y;
-  const int nrows = a.r0 + a.r1;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  constexpr int RPI = NW / S;
   auto row_ptr = [&](int row) {
     return row < a.r0 ? static_cast<const T*>(a.AT0) + (size_t)row * a.d
                       : static_cast<const T*>(a.AT1) + (size_t)(row - a.r0) * a.d;
   };
-  u32x4 pf[U];
-  {
-    const int row0 = blockIdx.x * RPI + wave / S;
-    if (row0 < nrows) row_prefetch<T, U, S>(row_ptr(row0), a.d, lane, wave % S, pf);
-  }
-  stage_x<T, NT>(a.x + (size_t)b * a.d, a.d, a.g, a.be, a.eps, xs, red);
-  bool first = true;
-  for (int base = blockIdx.x * RPI; base < nrows; base += gridDim.x * RPI) {
-    const int row = base + wave / S;
-    float v = 0.f;
-    if (row < nrows) {
-      v = first ? wave_rowdot_pf<T, U, S>(row_ptr(row), xs, a.d, lane, wave % S, pf)
-                : wave_rowdot<T, U, S>(row_ptr(row), xs, a.d, lane, wave % S);
-    }
-    first = false;
-    v = combine_segments<NW, S>(v, seg);
-    if (wave % S == 0 && lane == 0 && row < nrows) {
-      if (row < a.r0)
-        a.hid0[(size_t)b * a.r0 + row] = v;
-      else
-        a.hid1[(size_t)b * a.r1 + row - a.r0] = v;
-    }
-  }
+  auto epi = [&](int row, float v) {
+    if (row < a.r0)
+      a.hid0[(size_t)b * a.r0 + row] = v;
+    else
+      a.hid1[(size_t)b * a.r1 + row - a.r0] = v;
+  };
+  rowdot_wave_loop<T, NW, U>(row_ptr, epi, a.r0 + a.r1, a.d, a.x + (size_t)b * a.d, a.g, a.be, a.eps, xs, red,
+                             a.xhat_out ? a.xhat_out + (size_t)b * a.d : nullptr, blockIdx.x, gridDim.x);
 }
 
 hipError_t launch_pred_hidden(int wtype, const PredHidArgs& a, hipStream_t st) {
-  constexpr int NW = 8, S = 2, U = 6;
+  constexpr int NW = 16, U = 8;
   const int nrows = a.r0 + a.r1;
-  const int rpi = NW / S;
-  int blocks = (nrows + rpi - 1) / rpi;
-  const size_t lds = (size_t)(a.d + 2 * NW) * sizeof(float);
-  dim3 grid(blocks, a.B);
+  const dim3 grid(max(1, min(nrows, device_cu_count())), a.B);
+  const size_t lds = (size_t)(a.d + NW) * sizeof(float);
   if (wtype == DV_F16)
-    hipLaunchKernelGGL((k_pred_hidden<_Float16, NW, S, U>), grid, dim3(NW * 64), lds, st, a);
+    hipLaunchKernelGGL((k_pred_hidden<_Float16, NW, U>), grid, dim3(NW * 64), lds, st, a);
   else
-    hipLaunchKernelGGL((k_pred_hidden<float, NW, S, U>), grid, dim3(NW * 64), lds, st, a);
+    hipLaunchKernelGGL((k_pred_hidden<float, NW, U>), grid, dim3(NW * 64), lds, st, a);
   return hipGetLastError();
 }
 

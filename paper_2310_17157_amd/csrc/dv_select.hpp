@@ -21,6 +21,11 @@
 namespace dv {
 
 constexpr int kSelBins = 8192;   // LDS histogram bins (13-bit digits)
+
+// Phase marks for an external timing harness; empty in the library build.
+#ifndef DV_SELECT_MARK
+#define DV_SELECT_MARK(i)
+#endif
 // Scratch ints needed by the selection routines for an NT-thread workgroup.
 constexpr int kSelSm(int NT) { return 2 * (NT / 64) + 8; }
 
@@ -191,39 +196,45 @@ __device__ void wg_select(const float* __restrict__ s, int n, int mode, int k, f
   __syncthreads();
 }
 
-// The same selection with every key held in registers: thread t holds the keys of
-// the contiguous indices [t*IPT, (t+1)*IPT) (IPT % 4 == 0), loaded once with 16-byte
-// loads; all radix passes and the ordered compaction (per-thread counts, two
-// workgroup-wide exclusive scans, then an in-order walk) run on-chip with no further
-// memory round trips. Requires n <= NT * IPT (16-byte loads when s is aligned).
+// The same selection with every key held in registers. Wavefront w owns the
+// contiguous segment [w*64*IPT, (w+1)*64*IPT); within it lane l holds, for each
+// group g < IPT/4, the four keys at w*64*IPT + 256*g + 4*l + (0..3), so every load
+// instruction reads 1 KB of consecutive scores. Index order inside a segment is
+// (group, lane, element). All radix passes and the ordered compaction run on-chip:
+// ranks come from ballot popcounts per group plus the per-wavefront totals; no
+// further memory round trips. Requires n <= NT * IPT.
 //
 // Slots past n hold key 0, which no real score produces (every finite or infinite
 // float maps above 2^22), so they fall in the lowest histogram bin, never match a
 // selected prefix, and need no separate validity test. The selection boundary is
 // re-read from LDS before the write walk so the compiler recomputes the per-key
-// predicates instead of keeping IPT of them live across the scans.
+// predicates instead of keeping them live across the scans.
 template <int NT, int IPT>
 __device__ void wg_select_reg(const float* __restrict__ s, int n, int mode, int k, float thresh,
                               int32_t* __restrict__ out, int cap, int32_t* __restrict__ count_out,
                               int32_t* __restrict__ out2, uint32_t* hist, int* sm) {
   static_assert(IPT % 4 == 0, "IPT must be a multiple of 4");
-  const int tid = threadIdx.x;
-  const int i0 = tid * IPT;
+  constexpr int NW = NT / kWave;
+  constexpr int G = IPT / 4;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wbase = wave * 64 * IPT + 4 * lane;     // index of (g = 0, e = 0) for this lane
   const bool vec = (reinterpret_cast<uintptr_t>(s) & 15u) == 0;
   uint32_t key[IPT];
 #pragma unroll
-  for (int j = 0; j < IPT; j += 4) {
-    if (vec && i0 + j + 3 < n) {
-      const f32x4 v = *reinterpret_cast<const f32x4*>(s + i0 + j);
-      key[j] = fkey(v[0]);
-      key[j + 1] = fkey(v[1]);
-      key[j + 2] = fkey(v[2]);
-      key[j + 3] = fkey(v[3]);
+  for (int g = 0; g < G; ++g) {
+    const int i = wbase + 256 * g;
+    if (vec && i + 3 < n) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(s + i);
+      key[4 * g] = fkey(v[0]);
+      key[4 * g + 1] = fkey(v[1]);
+      key[4 * g + 2] = fkey(v[2]);
+      key[4 * g + 3] = fkey(v[3]);
     } else {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) key[j + e] = i0 + j + e < n ? fkey(s[i0 + j + e]) : 0u;
+      for (int e = 0; e < 4; ++e) key[4 * g + e] = i + e < n ? fkey(s[i + e]) : 0u;
     }
   }
+  DV_SELECT_MARK(10);
   uint32_t prefix = 0u;
   int pbits = 0;
   int eq_take = INT_MAX;
@@ -250,6 +261,7 @@ __device__ void wg_select_reg(const float* __restrict__ s, int n, int mode, int 
         if (shr32(key[j], hi) == prefix) atomicAdd(&hist[(key[j] >> lo) & (uint32_t)(nb - 1)], 1u);
       }
       __syncthreads();
+      DV_SELECT_MARK(11 + 2 * p);
       int dig, above;
       find_digit<NT>(hist, nb, krem, sm, &dig, &above);
       const int cnt = (int)hist[dig];
@@ -257,6 +269,7 @@ __device__ void wg_select_reg(const float* __restrict__ s, int n, int mode, int 
       prefix = (prefix << D) | (uint32_t)dig;
       pbits += D;
       __syncthreads();
+      DV_SELECT_MARK(12 + 2 * p);
       if (cnt == krem) {
         eq_take = INT_MAX;
         break;
@@ -264,40 +277,78 @@ __device__ void wg_select_reg(const float* __restrict__ s, int n, int mode, int 
       eq_take = krem;
     }
   }
-  volatile int* bound = sm + 2 * (NT / kWave) + 4;   // prefix, shift
+  DV_SELECT_MARK(17);
+  volatile int* bound = sm + 2 * NW + 4;   // prefix, shift
   if (tid == 0) {
     bound[0] = (int)prefix;
     bound[1] = 32 - pbits;
   }
+  // Per-wavefront totals (ballots: no cross-lane shuffles).
   int sh = 32 - pbits;
   int ngt = 0, neq = 0;
 #pragma unroll
   for (int j = 0; j < IPT; ++j) {
     const uint32_t u = shr32(key[j], sh);
-    ngt += u > prefix;
-    neq += u == prefix;
+    ngt += __popcll(__ballot(u > prefix));
+    neq += __popcll(__ballot(u == prefix));
   }
-  int tgt, teq;
-  int rg = block_excl_scan<NT>(ngt, sm, &tgt);
-  int re = block_excl_scan<NT>(neq, sm, &teq);
+  if (lane == 0) {
+    sm[2 * wave] = ngt;
+    sm[2 * wave + 1] = neq;
+  }
+  __syncthreads();
+  int rg = 0, re = 0, tgt = 0, teq = 0;
+  for (int w = 0; w < NW; ++w) {
+    const int a = sm[2 * w], b = sm[2 * w + 1];
+    if (w < wave) {
+      rg += a;
+      re += b;
+    }
+    tgt += a;
+    teq += b;
+  }
   const int total = tgt + min(teq, eq_take);
+  DV_SELECT_MARK(18);
   prefix = (uint32_t)bound[0];
   sh = bound[1];
+  // Write walk: group by group; inside a group, lanes in order, then elements. The
+  // rank of (lane l, element e) within the group is the number of selected elements
+  // of lanes below l (popcounts of four ballots under the lane mask) plus those of
+  // lane l before e.
+  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
 #pragma unroll
-  for (int j = 0; j < IPT; ++j) {
-    const uint32_t u = shr32(key[j], sh);
-    const bool gt = u > prefix;
-    const bool eq = u == prefix;
-    if (gt || (eq && re < eq_take)) {
-      const int p = rg + min(re, eq_take);
-      if (p < cap) {
-        out[p] = i0 + j;
-        if (out2) out2[p] = i0 + j;
-      }
+  for (int g = 0; g < G; ++g) {
+    bool gt[4], eq[4];
+    int bgt = 0, beq = 0, tg = 0, te = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const uint32_t u = shr32(key[4 * g + e], sh);
+      gt[e] = u > prefix;
+      eq[e] = u == prefix;
+      const uint64_t mg = __ballot(gt[e]), me = __ballot(eq[e]);
+      bgt += __popcll(mg & below);
+      beq += __popcll(me & below);
+      tg += __popcll(mg);
+      te += __popcll(me);
     }
-    rg += gt;
-    re += eq;
+    int pg = rg + bgt, pe = re + beq;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (gt[e] || (eq[e] && pe < eq_take)) {
+        const int p = pg + min(pe, eq_take);
+        if (p < cap) {
+          const int i = wbase + 256 * g + e;
+          out[p] = i;
+          if (out2) out2[p] = i;
+        }
+      }
+      pg += gt[e];
+      pe += eq[e];
+    }
+    rg += tg;
+    re += te;
   }
+  DV_SELECT_MARK(19);
   if (tid == 0 && count_out) *count_out = total;
   __syncthreads();
 }

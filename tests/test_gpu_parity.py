@@ -181,6 +181,22 @@ def test_sparse_attn_peaky_scores_and_first_position():
     assert rel_l2(host(out)[0], ref) < REL_TOL
 
 
+def test_sparse_attn_long_context_multi_subchunk():
+    """4000 attended positions for one head: each workgroup walks several sub-chunks
+    (online softmax) and the split count stays within the combine limit."""
+    from synth import get_config
+    cfg = get_config("small_f16").with_(L=4000, k_heads=1)
+    from synth import make_layer
+    t = make_layer(cfg, 36, device="cuda", biases=True, kv_scale=4.0)
+    attn, _, _, _, kv, _ = layer_objects(t, cfg.H)
+    x = torch.randn((1, cfg.d), device="cuda")
+    K0, V0 = host(t["K"])[0].copy(), host(t["V"])[0].copy()
+    out = Bd.dv_sparse_attn(attn, x, kv, torch.tensor([[7]], dtype=torch.int32, device="cuda"), 0.09)
+    _sync()
+    ref, *_ = O.mha_sparse(host(x)[0], oracle_attn(t), K0, V0, cfg.L - 1, [7], 0.09)
+    assert rel_l2(host(out)[0], ref) < REL_TOL
+
+
 def test_sparse_attn_all_heads_and_no_heads():
     cfg, t, heads, p, out, ref, *_ = _attn_case("small_f16", 34, heads=list(range(10)))
     assert rel_l2(host(out)[0], ref) < REL_TOL
