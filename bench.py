@@ -42,6 +42,46 @@ def kernel_bytes(cfg, pos):
     }
 
 
+# Sources each kernel is compiled from (with the build flags); the HBM counters committed
+# under profiles/ are valid only for the sources they were taken with.
+_CSRC = os.path.join(ROOT, "paper_2310_17157_amd", "csrc")
+KERNEL_SOURCES = {
+    "pred_hidden": ["dv_predict.hip", "dv_rowdot.hpp", "dv_internal.hpp", "dv_select.hpp"],
+    "pred_scores": ["dv_predict.hip", "dv_rowdot.hpp", "dv_internal.hpp", "dv_select.hpp"],
+    "qkv": ["dv_attn.hip", "dv_rowdot.hpp", "dv_internal.hpp", "dv_select.hpp"],
+    "attn": ["dv_attn.hip", "dv_rowdot.hpp", "dv_internal.hpp", "dv_select.hpp"],
+    "oproj": ["dv_axpy.hip", "dv_internal.hpp", "dv_select.hpp"],
+    "fc2": ["dv_axpy.hip", "dv_internal.hpp", "dv_select.hpp"],
+    "fc1": ["dv_mlp.hip", "dv_rowdot.hpp", "dv_internal.hpp"],
+}
+
+
+def kernel_sources_digest(label):
+    import hashlib
+    h = hashlib.sha256()
+    files = [os.path.join(_CSRC, f) for f in KERNEL_SOURCES[label]]
+    files.append(os.path.join(ROOT, "paper_2310_17157_amd", "build.py"))
+    for f in files:
+        with open(f, "rb") as fh:
+            h.update(os.path.basename(f).encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def counter_traffic(workload, label):
+    """HBM bytes per launch of `label` from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
+    summary, or None if there is none or the kernel's sources changed since."""
+    p = os.path.join(ROOT, "profiles", f"sparse_block_{workload}_hbm_counters.txt")
+    try:
+        with open(p) as fh:
+            line = next(l for l in fh if l.startswith("json: "))
+        rec = json.loads(line[len("json: "):])
+        if rec["sources_sha256"].get(label) != kernel_sources_digest(label):
+            return None
+        return rec["traffic_bytes"].get(label)
+    except (OSError, StopIteration, ValueError, KeyError):
+        return None
+
+
 def cpu_baseline(cfg, t_host, pos, seconds=10.0):
     """The fp64 oracle's predict + sparse block for one token of this workload."""
     import numpy as np
@@ -192,12 +232,13 @@ def main():
     achieved = kb[dom] / dom_avg_s / 1e9
     b = accounting.layer_bytes(cfg)
     roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
-                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": None,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
+                "traffic": counter_traffic(cfg.name, dom),
                 "bytes_per_launch": kb[dom], "avg_launch_us": round(dom_avg_s * 1e6, 2)}
     hbm = {"block_bytes": b.block, "predictor_bytes": b.pred, "total_bytes": b.total,
            "step_GBps": round(b.total / (ms_per_step * 1e-3) / 1e9, 1),
            "step_frac": round(b.total / (ms_per_step * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
-           "sparse_block_kernels_us": round(sum(kernels[k]["avg_us"] for k in ("qkv", "attn", "oproj", "oproj_reduce", "fc1", "fc2", "fc2_reduce")
+           "sparse_block_kernels_us": round(sum(kernels[k]["avg_us"] for k in ("qkv", "attn", "oproj", "fc1", "fc2")
                                                 if k in kernels), 2)}
     hbm["sparse_block_kernels_frac"] = round(
         b.block / (hbm["sparse_block_kernels_us"] * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4) if hbm["sparse_block_kernels_us"] else None

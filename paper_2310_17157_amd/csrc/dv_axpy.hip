@@ -73,11 +73,14 @@ __device__ __noinline__ void axpy_hosted_select(const float* scores, int n, int 
     wg_select<NT>(scores, n, DV_SELECT_TOPK, k, 0.f, idx, k, nullptr, idx_out, hist, sm);
 }
 
-template <typename T, int NW, int TL, int U>
+// HEADS selects the attention form (rows are dh-row blocks of selected heads, the
+// coefficients are combined from split-KV partials, and a selection may be hosted);
+// otherwise rows are single neurons with coefficients given per row.
+template <typename T, int NW, int TL, int U, bool HEADS>
 __global__ void __launch_bounds__(NW * 64) k_axpy(AxpyArgs a) {
   constexpr int NT = NW * 64;
   extern __shared__ float smem[];
-  if (a.sel_n > 0 && blockIdx.x == gridDim.x - 1) {
+  if (HEADS && a.sel_n > 0 && blockIdx.x == gridDim.x - 1) {
     axpy_hosted_select<NT>(a.sel_scores, a.sel_n, a.sel_k, a.sel_idx, a.sel_idx_out, smem);
     return;
   }
@@ -106,11 +109,11 @@ __global__ void __launch_bounds__(NW * 64) k_axpy(AxpyArgs a) {
   // coefficients and row indices fit in LDS.
   for (int rb = 0; rb < a.nrows; rb += a.rows_per_batch) {
     const int nb = min(a.rows_per_batch, a.nrows - rb);
-    const int h0 = a.dh > 0 ? rb / a.dh : 0;
+    const int h0 = HEADS ? rb / a.dh : 0;
     // ---- row indices (they need only the set), then this wavefront's first loads
     for (int i = tid; i < nb; i += NT) {
       const int row = rb + i;
-      if (a.dh == 0) {
+      if (!HEADS) {
         ri[i] = min(max(a.set[row], 0), a.m_rows - 1);
       } else {
         const int h = row / a.dh;
@@ -122,7 +125,7 @@ __global__ void __launch_bounds__(NW * 64) k_axpy(AxpyArgs a) {
     u32x4 wa[U];
     if (on) ax_load<T, TL, U>(wa, Mb, rowb, ri, rfirst, step, nb);
     // ---- coefficients, while those loads are in flight
-    if (a.dh == 0) {
+    if (!HEADS) {
       for (int i = tid; i < nb; i += NT) cf[i] = a.coef[rb + i];
     } else {
       // fac[h][s] = exp(m_s - M_h) / L_h for the heads of this batch (ns <= kAxMaxSplit)
@@ -208,7 +211,7 @@ __global__ void __launch_bounds__(NW * 64) k_axpy(AxpyArgs a) {
   }
 }
 
-template <typename T>
+template <typename T, bool HEADS>
 static hipError_t launch_axpy_t(AxpyArgs a, hipStream_t st) {
   constexpr int E = Chunk<T>::E;
   const int nch = a.d / E;
@@ -217,7 +220,7 @@ static hipError_t launch_axpy_t(AxpyArgs a, hipStream_t st) {
   // the heads a batch touches.
   int rpb = 5120;
   size_t fac = 0;
-  if (a.dh > 0) {
+  if (HEADS) {
     for (;;) {
       fac = (size_t)(rpb / a.dh + 2) * a.n_split * 4;
       if (fac <= 16384 || rpb <= 256) break;
@@ -228,12 +231,15 @@ static hipError_t launch_axpy_t(AxpyArgs a, hipStream_t st) {
   size_t lds = (size_t)a.rows_per_batch * 8 + (size_t)kAxNW * kAxTL * E * 4 + fac + 16;
   if (a.sel_n > 0) lds = max(lds, (size_t)kSelBins * 4 + kSelSm(kAxNW * 64) * sizeof(int));
   const int blocks = tiles + (a.sel_n > 0 ? 1 : 0);
-  hipLaunchKernelGGL((k_axpy<T, kAxNW, kAxTL, kAxU>), dim3(blocks), dim3(kAxNW * 64), lds, st, a);
+  hipLaunchKernelGGL((k_axpy<T, kAxNW, kAxTL, kAxU, HEADS>), dim3(blocks), dim3(kAxNW * 64), lds, st, a);
   return hipGetLastError();
 }
 
 hipError_t launch_axpy(int wtype, const AxpyArgs& a, hipStream_t st) {
-  return wtype == DV_F16 ? launch_axpy_t<_Float16>(a, st) : launch_axpy_t<float>(a, st);
+  if (a.dh > 0)
+    return wtype == DV_F16 ? launch_axpy_t<_Float16, true>(a, st) : launch_axpy_t<float, true>(a, st);
+  if (a.sel_n > 0) return hipErrorInvalidValue;
+  return wtype == DV_F16 ? launch_axpy_t<_Float16, false>(a, st) : launch_axpy_t<float, false>(a, st);
 }
 
 }  // namespace dv
