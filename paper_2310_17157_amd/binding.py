@@ -25,6 +25,8 @@ DV_SELECT_TOPK, DV_SELECT_THRESHOLD = 0, 1
 DV_LOOKAHEAD, DV_SEQUENTIAL = 0, 1
 DV_MLP_UNION, DV_MLP_MASKED = 0, 1
 DV_DETERMINISTIC, DV_VALIDATE = 1, 2
+(DV_OK, DV_ERR_NULL, DV_ERR_SHAPE, DV_ERR_DTYPE, DV_ERR_ALIGN, DV_ERR_WORKSPACE, DV_ERR_INDEX, DV_ERR_HIP,
+ DV_ERR_UNSUPPORTED, DV_ERR_ARG) = range(10)
 
 STATUS = {0: "DV_OK", 1: "DV_ERR_NULL", 2: "DV_ERR_SHAPE", 3: "DV_ERR_DTYPE", 4: "DV_ERR_ALIGN",
           5: "DV_ERR_WORKSPACE", 6: "DV_ERR_INDEX", 7: "DV_ERR_HIP", 8: "DV_ERR_UNSUPPORTED",

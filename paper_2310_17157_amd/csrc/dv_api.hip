@@ -131,13 +131,20 @@ static dv_status check_ln(const dv_ln* ln) {
   return DV_OK;
 }
 
-static dv_status validate_sets(const int32_t* set, int B, int n, int range, int32_t* flag, hipStream_t st) {
+dv_status dv::validate_sets_sync(const int32_t* set, int B, int n, int range, int32_t* flag, hipStream_t st) {
   DV_LAUNCH("validate", st, launch_validate_sets(set, B, n, range, flag, st));
   int32_t bad = 0;
   if (hipMemcpyAsync(&bad, flag, sizeof(bad), hipMemcpyDeviceToHost, st) != hipSuccess) return DV_ERR_HIP;
   if (hipStreamSynchronize(st) != hipSuccess) return DV_ERR_HIP;
   return bad ? DV_ERR_INDEX : DV_OK;
 }
+static dv_status validate_sets(const int32_t* set, int B, int n, int range, int32_t* flag, hipStream_t st) {
+  return validate_sets_sync(set, B, n, range, flag, st);
+}
+
+// The batched path: 2..kMaxBatch sequences, fp16 weights.
+static constexpr int kMaxUnionN = 262144;   // LDS bitmap of the union builder
+static bool batch_ok(int B, int wtype) { return B <= kMaxBatch && wtype == DV_F16; }
 
 static dv_status enqueue_axpy(const char* label, int wtype, const AxpyArgs& ax, hipStream_t hs) {
   DV_LAUNCH(label, hs, launch_axpy(wtype, ax, hs));
@@ -155,8 +162,9 @@ static size_t mlp_ws_layout(const dv_mlp* m, int B, int n_idx, Workspace& w, Mlp
   return w.off;
 }
 
-extern "C" size_t dv_sparse_mlp_workspace_bytes(const dv_mlp* m, int32_t B, int32_t n_idx, int32_t) {
-  if (m == nullptr || m->d <= 0 || B <= 0 || n_idx < 0 || !dtype_ok(m->wtype)) return 0;
+extern "C" size_t dv_sparse_mlp_workspace_bytes(const dv_mlp* m, int32_t B, int32_t n_idx, int32_t idx_per_seq) {
+  if (m == nullptr || m->d <= 0 || m->n <= 0 || B <= 0 || n_idx < 0 || !dtype_ok(m->wtype)) return 0;
+  if (B > 1) return batch_mlp_ws(m, B, n_idx, idx_per_seq);
   Workspace w(nullptr);
   MlpWs o;
   return mlp_ws_layout(m, B, n_idx, w, &o);
@@ -176,12 +184,13 @@ extern "C" dv_status dv_sparse_mlp(const dv_mlp* m, const float* x, int32_t B, c
   if (flags & ~(uint32_t)(DV_DETERMINISTIC | DV_VALIDATE)) return DV_ERR_ARG;
   if (m->b1 != nullptr && !aligned16(m->b1)) return DV_ERR_ALIGN;
   if (m->b2 != nullptr && !aligned16(m->b2)) return DV_ERR_ALIGN;
-  if (B > 1) return DV_ERR_UNSUPPORTED;
+  if (B > 1 && (!batch_ok(B, m->wtype) || m->n > kMaxUnionN)) return DV_ERR_UNSUPPORTED;
   if (!ws_ok(ws)) return DV_ERR_WORKSPACE;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (B > 1) return batch_mlp(m, x, B, idx, n_idx, idx_per_seq, batch_mode, out, ws, ws_bytes, flags, hs);
   Workspace w(ws);
   MlpWs o;
   if (mlp_ws_layout(m, B, n_idx, w, &o) > ws_bytes) return DV_ERR_WORKSPACE;
-  hipStream_t hs = static_cast<hipStream_t>(stream);
   if (flags & DV_VALIDATE) {
     st = validate_sets(idx, 1, n_idx, m->n, o.flag, hs);
     if (st != DV_OK) return st;
@@ -214,9 +223,10 @@ static size_t attn_ws_layout(const dv_attn* a, int cap, int B, int n_heads, Work
 }
 
 extern "C" size_t dv_sparse_attn_workspace_bytes(const dv_attn* a, const dv_kv* kv, int32_t B, int32_t n_heads) {
-  if (a == nullptr || kv == nullptr || a->d <= 0 || a->dh <= 0 || B <= 0 || n_heads < 0 ||
+  if (a == nullptr || kv == nullptr || a->d <= 0 || a->dh <= 0 || a->H <= 0 || B <= 0 || n_heads < 0 ||
       kv->cap <= 0 || !dtype_ok(a->wtype))
     return 0;
+  if (B > 1) return batch_attn_ws(a, B, n_heads);
   Workspace w(nullptr);
   AttnWs o;
   return attn_ws_layout(a, kv->cap, B, n_heads, w, &o);
@@ -226,11 +236,11 @@ static dv_status enqueue_attention(const dv_attn* a, const dv_kv* kv, const Attn
                                    float scale, hipStream_t hs) {
   const int pos = kv->pos[0];
   AttnArgs at{};
-  at.H = a->H; at.dh = a->dh; at.cap = kv->cap; at.pos = pos; at.n_heads = n_heads;
+  at.H = a->H; at.dh = a->dh; at.cap = kv->cap; at.posb[0] = pos; at.n_heads = n_heads;
   at.chunk = attn_chunk(n_heads, pos + 1, a->dh, kv->ktype);
   at.n_split = (pos + 1 + at.chunk - 1) / at.chunk;
   at.q = o.q; at.heads = o.heads; at.K = kv->K; at.V = kv->V; at.scale = scale; at.part = o.part;
-  DV_LAUNCH("attn", hs, launch_attn(kv->ktype, at, hs));
+  DV_LAUNCH("attn", hs, launch_attn(kv->ktype, at, 1, hs));
   return DV_OK;
 }
 
@@ -254,12 +264,13 @@ extern "C" dv_status dv_sparse_attn(const dv_attn* a, const float* x, int32_t B,
   if (flags & ~(uint32_t)(DV_DETERMINISTIC | DV_VALIDATE)) return DV_ERR_ARG;
   if (!isfinite(scale)) return DV_ERR_ARG;
   if (a->bo != nullptr && !aligned16(a->bo)) return DV_ERR_ALIGN;
-  if (B > 1) return DV_ERR_UNSUPPORTED;
+  if (B > 1 && (!batch_ok(B, a->wtype) || a->H > kMaxUnionN)) return DV_ERR_UNSUPPORTED;
   if (!ws_ok(ws)) return DV_ERR_WORKSPACE;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (B > 1) return batch_attn(a, x, B, kv, heads, n_heads, scale, out, ws, ws_bytes, flags, hs);
   Workspace w(ws);
   AttnWs o;
   if (attn_ws_layout(a, kv->cap, B, n_heads, w, &o) > ws_bytes) return DV_ERR_WORKSPACE;
-  hipStream_t hs = static_cast<hipStream_t>(stream);
   if (flags & DV_VALIDATE) {
     st = validate_sets(heads, 1, n_heads, a->H, o.flag, hs);
     if (st != DV_OK) return st;
@@ -319,6 +330,7 @@ extern "C" size_t dv_sparse_block_workspace_bytes(const dv_attn* a, const dv_mlp
       k_heads < 0 || k_mlp < 0 || a->d <= 0 || a->dh <= 0 || kv->cap <= 0 || pa->r <= 0 || pm->r <= 0 ||
       pa->n_out <= 0 || pm->n_out <= 0 || !dtype_ok(a->wtype) || !dtype_ok(m->wtype))
     return 0;
+  if (B > 1) return batch_block_ws(a, m, pa, pm, B, k_heads, k_mlp);
   Workspace w(nullptr);
   BlockWs o;
   return block_ws_layout(a, m, pa, pm, kv->cap, B, k_heads, k_mlp, w, &o);
@@ -360,7 +372,14 @@ extern "C" dv_status dv_sparse_block(const dv_attn* a, const dv_mlp* m, const dv
   if (!isfinite(scale)) return DV_ERR_ARG;
   if (!aligned16(x_in) || !aligned16(x_out)) return DV_ERR_ALIGN;
   if ((a->bo && !aligned16(a->bo)) || (m->b2 && !aligned16(m->b2))) return DV_ERR_ALIGN;
-  if (B > 1) return DV_ERR_UNSUPPORTED;
+  if (B > 1) {
+    if (!batch_ok(B, a->wtype) || m->wtype != DV_F16 || pa->wtype != DV_F16 || m->n > kMaxUnionN ||
+        pa->r > batch_max_rank(B) || pm->r > batch_max_rank(B))
+      return DV_ERR_UNSUPPORTED;
+    if (!ws_ok(ws)) return DV_ERR_WORKSPACE;
+    return batch_block(a, m, pa, pm, ln, kv, x_in, x_out, B, k_heads, k_mlp, mode, batch_mode, scale, heads_out,
+                       idx_out, ws, ws_bytes, static_cast<hipStream_t>(stream));
+  }
   if (!ws_ok(ws)) return DV_ERR_WORKSPACE;
   Workspace w(ws);
   BlockWs o;

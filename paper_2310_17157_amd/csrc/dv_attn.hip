@@ -6,8 +6,8 @@
 //           and W^V_i (contiguous row blocks) against the staged x-hat; q goes to the
 //           workspace, k and v to cache row pos. Optionally selects the head set
 //           itself from the head predictor's scores (ranked in every workgroup).
-//   k_attn  split-KV decode attention: one workgroup per (selected head, position
-//           chunk) computes the chunk's max logit, sum of exponentials and
+//   k_attn  split-KV decode attention: one workgroup per (sequence, selected head,
+//           position chunk) computes the chunk's max logit, sum of exponentials and
 //           unnormalised value sum; the out-projection kernel combines the chunks.
 #include <math.h>
 
@@ -96,20 +96,22 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   constexpr int SUB = NSTEP * NW * PPW;
   __shared__ float sm_m[NW], sm_l[NW];
   __shared__ float sm_o[NW][256];
-  const int j = blockIdx.y, c = blockIdx.x;
-  const int head = min(max(a.heads[j], 0), a.H - 1);
+  const int j = blockIdx.y, c = blockIdx.x, b = blockIdx.z;
+  const int jb = b * a.n_heads + j;               // (sequence, selected head)
+  const int head = min(max(a.heads[jb], 0), a.H - 1);
   const int t0 = c * a.chunk;
-  const int tend = min(t0 + a.chunk, a.pos + 1);
+  const int tend = min(t0 + a.chunk, a.posb[b] + 1);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int grp = lane / LPP, gl = lane % LPP;
   const int nchr = a.dh / E;
   const bool lane_on = gl < nchr;
   float qv[E];
 #pragma unroll
-  for (int e = 0; e < E; ++e) qv[e] = lane_on ? a.q[(size_t)j * a.dh + gl * E + e] : 0.f;
+  for (int e = 0; e < E; ++e) qv[e] = lane_on ? a.q[(size_t)jb * a.dh + gl * E + e] : 0.f;
   const size_t rowb = (size_t)a.dh * sizeof(KT);
-  const char* Kb = static_cast<const char*>(a.K) + (size_t)head * a.cap * rowb + (size_t)gl * 16;
-  const char* Vb = static_cast<const char*>(a.V) + (size_t)head * a.cap * rowb + (size_t)gl * 16;
+  const size_t hoff = ((size_t)b * a.H + head) * a.cap * rowb + (size_t)gl * 16;
+  const char* Kb = static_cast<const char*>(a.K) + hoff;
+  const char* Vb = static_cast<const char*>(a.V) + hoff;
 
   float m = -INFINITY, l = 0.f;
   float o[E];
@@ -181,7 +183,7 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   float M = -INFINITY;
 #pragma unroll
   for (int w = 0; w < NW; ++w) M = fmaxf(M, sm_m[w]);
-  float* out = a.part + ((size_t)j * a.n_split + c) * (a.dh + 2);
+  float* out = a.part + ((size_t)jb * a.n_split + c) * (a.dh + 2);
   if (M == -INFINITY) {
     for (int t = threadIdx.x; t < a.dh + 2; t += 256) out[t] = t == 0 ? -INFINITY : 0.f;
     return;
@@ -226,23 +228,23 @@ int attn_chunk(int n_heads, int attended, int dh, int kvtype) {
 }
 
 template <typename KT, int LPP>
-static hipError_t launch_attn_l(const AttnArgs& a, hipStream_t st) {
-  dim3 grid(a.n_split, a.n_heads);
+static hipError_t launch_attn_l(const AttnArgs& a, int B, hipStream_t st) {
+  dim3 grid(a.n_split, a.n_heads, B);
   hipLaunchKernelGGL((k_attn<KT, LPP, kAttnNStep>), grid, dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
 template <typename KT>
-static hipError_t launch_attn_t(const AttnArgs& a, hipStream_t st) {
+static hipError_t launch_attn_t(const AttnArgs& a, int B, hipStream_t st) {
   switch (attn_lpp(a.dh, sizeof(KT) == 2 ? DV_F16 : DV_F32)) {
-    case 16: return launch_attn_l<KT, 16>(a, st);
-    case 32: return launch_attn_l<KT, 32>(a, st);
-    default: return launch_attn_l<KT, 64>(a, st);
+    case 16: return launch_attn_l<KT, 16>(a, B, st);
+    case 32: return launch_attn_l<KT, 32>(a, B, st);
+    default: return launch_attn_l<KT, 64>(a, B, st);
   }
 }
 
-hipError_t launch_attn(int kvtype, const AttnArgs& a, hipStream_t st) {
-  return kvtype == DV_F16 ? launch_attn_t<_Float16>(a, st) : launch_attn_t<float>(a, st);
+hipError_t launch_attn(int kvtype, const AttnArgs& a, int B, hipStream_t st) {
+  return kvtype == DV_F16 ? launch_attn_t<_Float16>(a, B, st) : launch_attn_t<float>(a, B, st);
 }
 
 }  // namespace dv

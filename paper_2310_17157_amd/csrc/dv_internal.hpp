@@ -381,13 +381,20 @@ struct QkvArgs {
 };
 hipError_t launch_qkv(int wtype, int kvtype, const QkvArgs& a, hipStream_t st);
 
-// Split-KV decode attention for the selected heads (B = 1).
+// Largest batch of the batched (matrix-core) path: token columns of one MFMA tile pair.
+constexpr int kMaxBatch = 32;
+
+// Split-KV decode attention for the selected heads of B sequences (grid z = sequence).
 struct AttnArgs {
-  int H, dh, cap, pos, n_heads, n_split, chunk;
-  const float* q; const int32_t* heads; const void* K; const void* V; float scale;
-  float* part;                      // [n_heads][n_split][dh + 2]
+  int H, dh, cap, n_heads, n_split, chunk;
+  int posb[kMaxBatch];              // row of the current token, per sequence
+  const float* q;                   // [B][n_heads][dh]
+  const int32_t* heads;             // [B][n_heads]
+  const void* K; const void* V;     // [B][H][cap][dh]
+  float scale;
+  float* part;                      // [B][n_heads][n_split][dh + 2]
 };
-hipError_t launch_attn(int kvtype, const AttnArgs& a, hipStream_t st);
+hipError_t launch_attn(int kvtype, const AttnArgs& a, int B, hipStream_t st);
 
 // Gathered row-axpy: out = resid + bias + sum_rows coef[row] * M[rowidx(row)], tiled by
 // 128-byte column tiles; every workgroup sums all selected rows of its tile.
@@ -416,6 +423,109 @@ struct Fc1Args {
   float* h;
 };
 hipError_t launch_fc1(int wtype, const Fc1Args& a, hipStream_t st);
+
+// ------------------------------------------------ batched (matrix-core) path
+// Union of B ascending sets (one workgroup): U ascending, *count, optional rank map
+// pos[n] (-1 outside) and membership bits mask[u] (bit b: U[u] is in set b).
+hipError_t launch_union(const int32_t* sets, int B, int k, int n, int32_t* U, int32_t* count, int32_t* pos,
+                        uint32_t* mask, hipStream_t st);
+
+// X16[NB][Kpad] = fp16(LN(x)) (g NULL: x), zero rows b >= B and columns k >= d.
+hipError_t launch_ln_cast(const float* x, int B, int NB, int d, int Kpad, const float* g, const float* be, float eps,
+                          _Float16* X16, hipStream_t st);
+
+enum { kRowsList = 0, kRowsHeads = 1, kRowsIdentity = 2 };
+
+// Gathered rows times the token batch on the matrix cores, split over K:
+// P[s][r][b] = sum_{k in split s} W(r)[k] X16[b][k]. Rows: kRowsList W0[list[r]];
+// kRowsHeads r = (m * nu + p) * dh + t -> row list[p] * dh + t of W0/W1/W2 (m = 0, 1, 2);
+// kRowsIdentity r < n0 -> W0[r], else W1[r - n0]. With out0 set (and S == 1) the
+// result goes straight to out0[b][r] (r < n0) / out1[b][r - n0] for b < B.
+struct MrowsArgs {
+  int d, Kpad, Ks, S;
+  const _Float16* X;                 // [NB][Kpad]
+  int mode;
+  const void* W0; const void* W1; const void* W2;   // fp16 rows of d elements
+  const int32_t* list; const int32_t* list_count; int list_max; int dh;
+  int list_range;                    // list entries are clamped to [0, list_range)
+  int nrows, n0;                     // kRowsIdentity: rows in all, rows of W0
+  float* P; int nrows_pad;           // [S][nrows_pad][NB]
+  float* out0; int ld0; float* out1; int ld1; int B;
+};
+void mrows_split(int Kpad, int NB, int* S, int* Ks);
+hipError_t launch_mrows(int NB, const MrowsArgs& a, hipStream_t st);
+
+// Token-batch coefficients times gathered rows, contracted over the rows:
+// P[s][b][c] = sum_{u in split s} C[b][u] M[row(u)][c], row(u) = list[u] (dh == 0) or
+// list[u / dh] * dh + u % dh. C is fp16 [NB][ldc], zero beyond the rows in use.
+struct McolsArgs {
+  int d;
+  const void* M;
+  const int32_t* list; const int32_t* list_count; int list_max; int dh;
+  int list_range;                    // list entries are clamped to [0, list_range)
+  const _Float16* C; int ldc;
+  int S, B;
+  float* P;                          // [S][B][d]
+};
+int mcols_split(int d, int nmax);
+hipError_t launch_mcols(int NB, const McolsArgs& a, hipStream_t st);
+
+// C[b][u] = fp16(ReLU(sum_s P[s][u][b] + b1[list[u]])), masked by membership bits.
+struct Fc1FinishArgs {
+  const float* P; int S, nrows_pad;
+  const int32_t* list; const int32_t* list_count; int list_max; int list_range;
+  const float* b1; const uint32_t* mask; int B;
+  _Float16* C; int ldc;
+};
+hipError_t launch_fc1_finish(int NB, const Fc1FinishArgs& a, hipStream_t st);
+
+// out[b][c] = sum_s P[s][b][c] + bias[c] + resid[b][c].
+struct ColsFinishArgs {
+  const float* P; int S, B, d;
+  const float* bias; const float* resid; float* out;
+};
+hipError_t launch_cols_finish(const ColsFinishArgs& a, hipStream_t st);
+
+// C[b][j] = fp16(sum_s P[s][row0 + j][b]) for j < r, zero padded to [NB][ldc].
+hipError_t launch_sum_cast(int NB, const float* P, int S, int nrows_pad, int row0, int r, int B, _Float16* C, int ldc,
+                           hipStream_t st);
+
+// Q/K/V from kRowsHeads partials: q[b][j][t] and cache rows pos[b] of the selected heads.
+struct QkvFinishArgs {
+  const float* P; int S, nrows_pad;
+  const int32_t* heads; int n_heads, H, dh, cap, B;
+  const int32_t* hpos; const int32_t* hcount;
+  const float* bq; const float* bk; const float* bv;
+  float* q; void* K; void* V;
+  int posb[kMaxBatch];
+};
+hipError_t launch_qkv_finish(int NB, int kvtype, const QkvFinishArgs& a, hipStream_t st);
+
+// Out-projection coefficients C[b][p*dh + t] from the split-KV partials.
+struct AttnFinishArgs {
+  const float* part; int n_split, n_heads, dh, B;
+  const int32_t* heads; const int32_t* list; const int32_t* hcount;
+  _Float16* C; int ldc;
+};
+hipError_t launch_attn_finish(int NB, const AttnFinishArgs& a, hipStream_t st);
+
+// Host side of the batched path (dv_batch_api.hip); arguments already validated.
+int batch_nb(int B);
+int batch_max_rank(int B);
+size_t batch_mlp_ws(const dv_mlp* m, int B, int n_idx, int per_seq);
+size_t batch_attn_ws(const dv_attn* a, int B, int n_heads);
+size_t batch_block_ws(const dv_attn* a, const dv_mlp* m, const dv_predictor* pa, const dv_predictor* pm, int B,
+                      int kh, int km);
+dv_status batch_mlp(const dv_mlp* m, const float* x, int B, const int32_t* idx, int n_idx, int per_seq,
+                    int batch_mode, float* out, void* ws, size_t ws_bytes, uint32_t flags, hipStream_t hs);
+dv_status batch_attn(const dv_attn* a, const float* x, int B, const dv_kv* kv, const int32_t* heads, int n_heads,
+                     float scale, float* out, void* ws, size_t ws_bytes, uint32_t flags, hipStream_t hs);
+dv_status batch_block(const dv_attn* a, const dv_mlp* m, const dv_predictor* pa, const dv_predictor* pm,
+                      const dv_ln* ln, const dv_kv* kv, const float* x_in, float* x_out, int B, int kh, int km,
+                      int mode, int batch_mode, float scale, int32_t* heads_out, int32_t* idx_out, void* ws,
+                      size_t ws_bytes, hipStream_t hs);
+// DV_VALIDATE: check B ascending sets of n indices in [0, range) (synchronises `st`).
+dv_status validate_sets_sync(const int32_t* set, int B, int n, int range, int32_t* flag, hipStream_t st);
 
 // Split-KV chunk length (positions per attention workgroup); at most kAttnMaxSplit
 // chunks per head.

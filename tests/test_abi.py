@@ -128,3 +128,21 @@ def test_predict_and_block_validation(lib):
     assert blk(mode=4) == 9
     assert blk(pm=B.CPredictor(64, 16, 128, B.DV_F32, FAKE, FAKE)) == 3  # predictor dtypes differ
     assert blk(ws_bytes=1) == 5
+
+
+def test_batched_path_limits(lib):
+    """B > 1 runs on the matrix cores: up to 32 sequences, fp16 weights; the rest is
+    DV_ERR_UNSUPPORTED before any device work."""
+    assert _call_mlp(lib, _mlp(), Bn=33, per_seq=1) == B.DV_ERR_UNSUPPORTED
+    assert _call_mlp(lib, _mlp(wtype=B.DV_F32), Bn=2, per_seq=1) == B.DV_ERR_UNSUPPORTED
+    assert _call_mlp(lib, _mlp(), Bn=2, per_seq=1, ws=None) == B.DV_ERR_WORKSPACE
+    m = _mlp()
+    one = lib.dv_sparse_mlp_workspace_bytes(ctypes.byref(m), 1, 8, 1)
+    many = lib.dv_sparse_mlp_workspace_bytes(ctypes.byref(m), 32, 8, 1)
+    assert many > one > 0 and many % 256 == 0
+    a = _attn()
+    kv33 = _kv(Bn=33, pos=tuple([3] * 33))
+    assert lib.dv_sparse_attn(ctypes.byref(a), FAKE, 33, ctypes.byref(kv33), FAKE, 2, 0.25, FAKE, FAKE,
+                              1 << 30, 0, None) == B.DV_ERR_UNSUPPORTED
+    kv2 = _kv(Bn=2, pos=(3, 9))
+    assert lib.dv_sparse_attn_workspace_bytes(ctypes.byref(a), ctypes.byref(kv2), 2, 2) > 0

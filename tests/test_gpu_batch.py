@@ -1,0 +1,256 @@
+"""GPU parity of the batched path (B > 1 sequences, one token each, on the matrix cores)
+against the fp64 oracle on the same seeded inputs.
+
+The MLP runs on the union of the sequences' neuron sets (Section 5.2) or, masked, on
+each sequence's own set; attention keeps a head set, a cache and a position per
+sequence. Outputs: max relative L2 error <= 2e-3 per sequence. The batched path rounds
+its MFMA operands (x-hat, ReLU outputs, attention outputs) to fp16, whose relative
+error (2^-11 per operand, uncorrelated over thousands of terms) stays an order of
+magnitude inside that bound. Cache rows of non-selected heads stay bit-identical.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import dejavu as O
+from paper_2310_17157_amd import binding as Bd
+from paper_2310_17157_amd.workload import layer_objects
+from synth import get_config, make_layer, uniform_head_sets, zipf_mlp_sets
+from tests.gpu_util import REL_TOL, check_topk_set, host, oracle_attn, oracle_ln, oracle_mlp, rel_l2
+
+pytestmark = pytest.mark.gpu
+
+
+def _sync():
+    torch.cuda.synchronize()
+
+
+def _cfg(name, B=None):
+    cfg = get_config(name)
+    if B is not None and B != cfg.B:
+        cfg = cfg.with_(B=B, name=f"{cfg.name}_B{B}")
+    return cfg
+
+
+def _mlp(t, biases=True):
+    return Bd.MLP(t["W1T"], t["W2T"], t["b1"] if biases else None, t["b2"] if biases else None)
+
+
+# ------------------------------------------------------------------------ MLP
+@pytest.mark.parametrize("B", [2, 8, 17, 32])
+@pytest.mark.parametrize("mode", ["union", "masked"])
+def test_batch_mlp_per_sequence_sets(B, mode):
+    cfg = _cfg("small_b8", B)
+    t = make_layer(cfg, 21, device="cuda", biases=True, with_predictors=False)
+    sets = zipf_mlp_sets(cfg, 21)
+    idx = torch.tensor(sets, dtype=torch.int32, device="cuda")
+    bm = Bd.DV_MLP_UNION if mode == "union" else Bd.DV_MLP_MASKED
+    out = Bd.dv_sparse_mlp(_mlp(t), t["x"], idx, idx_per_seq=1, batch_mode=bm, flags=Bd.DV_VALIDATE)
+    _sync()
+    m = oracle_mlp(t)
+    ref = O.mlp_batch(host(t["x"]), m["W1T"], m["b1"], m["W2T"], m["b2"], [s.tolist() for s in sets], mode)
+    got = host(out)
+    for b in range(B):
+        assert rel_l2(got[b], ref[b]) < REL_TOL, (b, rel_l2(got[b], ref[b]))
+
+
+def test_batch_mlp_union_differs_from_masked():
+    """The two batch semantics give different outputs (the union adds other sequences' neurons)."""
+    cfg = _cfg("small_b8")
+    t = make_layer(cfg, 22, device="cuda", biases=True, with_predictors=False)
+    idx = torch.tensor(zipf_mlp_sets(cfg, 22), dtype=torch.int32, device="cuda")
+    u = Bd.dv_sparse_mlp(_mlp(t), t["x"], idx, idx_per_seq=1, batch_mode=Bd.DV_MLP_UNION)
+    m = Bd.dv_sparse_mlp(_mlp(t), t["x"], idx, idx_per_seq=1, batch_mode=Bd.DV_MLP_MASKED)
+    _sync()
+    assert rel_l2(host(u)[0], host(m)[0]) > 10 * REL_TOL
+
+
+def test_batch_mlp_shared_set_and_full_set():
+    cfg = _cfg("small_b8")
+    t = make_layer(cfg, 23, device="cuda", biases=True, with_predictors=False)
+    m = oracle_mlp(t)
+    x = host(t["x"])
+    S = np.sort(np.random.default_rng(23).permutation(cfg.N)[: cfg.k_mlp]).astype(np.int32)
+    out = Bd.dv_sparse_mlp(_mlp(t), t["x"], torch.tensor(S, device="cuda"), idx_per_seq=0)
+    full = Bd.dv_sparse_mlp(_mlp(t), t["x"], torch.arange(cfg.N, dtype=torch.int32, device="cuda"), idx_per_seq=0)
+    _sync()
+    for b in range(cfg.B):
+        assert rel_l2(host(out)[b], O.mlp_sparse(x[b], m["W1T"], m["b1"], m["W2T"], m["b2"], S)) < REL_TOL
+        assert rel_l2(host(full)[b], O.mlp_dense(x[b], m["W1T"], m["b1"], m["W2T"], m["b2"])) < REL_TOL
+
+
+def test_batch_mlp_empty_set_is_bias():
+    cfg = _cfg("small_b8")
+    t = make_layer(cfg, 24, device="cuda", biases=True, with_predictors=False)
+    idx = torch.zeros((cfg.B, 0), dtype=torch.int32, device="cuda")
+    out = Bd.dv_sparse_mlp(_mlp(t), t["x"], idx, idx_per_seq=1)
+    _sync()
+    for b in range(cfg.B):
+        assert np.array_equal(host(out)[b].astype(np.float32), host(t["b2"]).astype(np.float32))
+
+
+def test_batch_mlp_rejects_bad_sets_under_validate():
+    cfg = _cfg("small_b8")
+    t = make_layer(cfg, 25, device="cuda", with_predictors=False)
+    sets = zipf_mlp_sets(cfg, 25)
+    sets[3, 5] = sets[3, 4]          # duplicate -> not strictly ascending
+    idx = torch.tensor(sets, dtype=torch.int32, device="cuda")
+    with pytest.raises(Bd.DvError) as e:
+        Bd.dv_sparse_mlp(_mlp(t), t["x"], idx, idx_per_seq=1, flags=Bd.DV_VALIDATE)
+    assert e.value.status == Bd.DV_ERR_INDEX
+
+
+# ------------------------------------------------------------------ attention
+def _check_attn(cfg, t, heads, out, K0, V0, biases=True):
+    a = oracle_attn(t, biases)
+    pos = [int(p) for p in t["pos"]]
+    ref, Kn, Vn = O.mha_batch(host(t["x"]), a, K0, V0, pos, [h.tolist() for h in heads], 1.0 / np.sqrt(cfg.dh))
+    got = host(out)
+    K1, V1 = host(t["K"]), host(t["V"])
+    for b in range(cfg.B):
+        assert rel_l2(got[b], ref[b]) < REL_TOL, (b, rel_l2(got[b], ref[b]))
+        for h in range(cfg.H):
+            if h in set(heads[b].tolist()):
+                for C1, Cn in ((K1, Kn), (V1, Vn)):
+                    assert rel_l2(C1[b, h, pos[b]], Cn[b, h, pos[b]]) < 2e-3
+            else:
+                assert np.array_equal(K1[b, h, pos[b]], K0[b, h, pos[b]])
+                assert np.array_equal(V1[b, h, pos[b]], V0[b, h, pos[b]])
+        # every other position of every head is untouched
+        mask = np.ones(K1.shape[2], dtype=bool)
+        mask[pos[b]] = False
+        assert np.array_equal(K1[b][:, mask], K0[b][:, mask])
+        assert np.array_equal(V1[b][:, mask], V0[b][:, mask])
+
+
+@pytest.mark.parametrize("B", [2, 8, 32])
+@pytest.mark.parametrize("kv_scale", [1.0, 30.0])
+def test_batch_attn(B, kv_scale):
+    cfg = _cfg("small_b8", B)
+    t = make_layer(cfg, 31, device="cuda", biases=True, kv_scale=kv_scale)
+    K0, V0 = host(t["K"]).copy(), host(t["V"]).copy()
+    heads = uniform_head_sets(cfg, 31)
+    attn, _, _, _, kv, _ = layer_objects(t, cfg.H)
+    out = Bd.dv_sparse_attn(attn, t["x"], kv, torch.tensor(heads, device="cuda"), 1.0 / np.sqrt(cfg.dh),
+                            flags=Bd.DV_VALIDATE)
+    _sync()
+    _check_attn(cfg, t, heads, out, K0, V0)
+
+
+def test_batch_attn_all_heads_and_pos0():
+    cfg = _cfg("small_b8").with_(k_heads=10, L_range=(1, 2))
+    t = make_layer(cfg, 32, device="cuda", biases=True)
+    K0, V0 = host(t["K"]).copy(), host(t["V"]).copy()
+    heads = np.tile(np.arange(cfg.H, dtype=np.int32), (cfg.B, 1))
+    attn, _, _, _, kv, _ = layer_objects(t, cfg.H)
+    out = Bd.dv_sparse_attn(attn, t["x"], kv, torch.tensor(heads, device="cuda"), 1.0 / np.sqrt(cfg.dh))
+    _sync()
+    assert min(int(p) for p in t["pos"]) == 0
+    _check_attn(cfg, t, heads, out, K0, V0)
+
+
+def test_batch_attn_no_heads_is_bias():
+    cfg = _cfg("small_b8")
+    t = make_layer(cfg, 33, device="cuda", biases=True)
+    attn, _, _, _, kv, _ = layer_objects(t, cfg.H)
+    out = Bd.dv_sparse_attn(attn, t["x"], kv, torch.zeros((cfg.B, 0), dtype=torch.int32, device="cuda"), 0.1)
+    _sync()
+    for b in range(cfg.B):
+        assert np.array_equal(host(out)[b].astype(np.float32), host(t["bo"]).astype(np.float32))
+
+
+# ---------------------------------------------------------------------- layer
+def _check_block(cfg, t, out, hs, ms, K0, V0, mode, batch_mode):
+    """Sets against the oracle's scores (near-ties allowed); the output against the oracle
+    layer rerun on the GPU's sets with the same batch semantics."""
+    a, m, ln = oracle_attn(t), oracle_mlp(t), oracle_ln(t)
+    x = host(t["x"])
+    pos = [int(p) for p in t["pos"]]
+    hs, ms = host(hs), host(ms)
+    scale = 1.0 / np.sqrt(cfg.dh)
+    AT_h, BT_h, AT_m, BT_m = (host(t[k]) for k in ("AT_h", "BT_h", "AT_m", "BT_m"))
+    U = O.union_of_sets([s.tolist() for s in ms])
+    got = host(out)
+    for b in range(cfg.B):
+        xh = O.layer_norm(x[b], ln["g1"], ln["be1"], ln["eps"])
+        check_topk_set(hs[b], O.predictor_scores(xh, AT_h, BT_h), cfg.k_heads)
+        S_M = U if batch_mode == "union" else ms[b]
+        r = O.sparse_block(x[b], a, m, K0[b], V0[b], pos[b], scale, S_A=hs[b], S_M=S_M, ln=ln)
+        if mode == "lookahead":
+            s_m = O.predictor_scores(xh, AT_m, BT_m)
+        else:
+            s_m = O.predictor_scores(O.layer_norm(r["y_tilde"], ln["g2"], ln["be2"], ln["eps"]), AT_m, BT_m)
+        check_topk_set(ms[b], s_m, cfg.k_mlp)
+        assert rel_l2(got[b], r["out"]) < REL_TOL, (b, rel_l2(got[b], r["out"]))
+
+
+@pytest.mark.parametrize("B", [8, 32])
+@pytest.mark.parametrize("mode", ["lookahead", "sequential"])
+@pytest.mark.parametrize("batch_mode", ["union", "masked"])
+def test_batch_block(B, mode, batch_mode):
+    cfg = _cfg("small_b8", B)
+    t = make_layer(cfg, 41, device="cuda", biases=True, ln_random=True)
+    K0, V0 = host(t["K"]).copy(), host(t["V"]).copy()
+    attn, mlp, ph, pm, kv, ln = layer_objects(t, cfg.H)
+    out, hs, ms = Bd.dv_sparse_block(attn, mlp, ph, pm, ln, kv, t["x"], cfg.k_heads, cfg.k_mlp,
+                                     1.0 / np.sqrt(cfg.dh),
+                                     mode=Bd.DV_LOOKAHEAD if mode == "lookahead" else Bd.DV_SEQUENTIAL,
+                                     batch_mode=Bd.DV_MLP_UNION if batch_mode == "union" else Bd.DV_MLP_MASKED)
+    _sync()
+    _check_block(cfg, t, out, hs, ms, K0, V0, mode, batch_mode)
+
+
+def test_batch_block_deterministic():
+    cfg = _cfg("small_b8")
+    t = make_layer(cfg, 42, device="cuda", biases=True, ln_random=True)
+    attn, mlp, ph, pm, kv, ln = layer_objects(t, cfg.H)
+    outs = []
+    for _ in range(2):
+        o, h, m = Bd.dv_sparse_block(attn, mlp, ph, pm, ln, kv, t["x"], cfg.k_heads, cfg.k_mlp, 0.1)
+        outs.append((o.clone(), h.clone(), m.clone()))
+    _sync()
+    for a, b in zip(outs[0], outs[1]):
+        assert torch.equal(a, b)
+
+
+# ------------------------------------------------------------ OPT-175B, batch 32
+@pytest.fixture(scope="module")
+def b32():
+    cfg = get_config("opt175b_b32")
+    t = make_layer(cfg, 4, device="cuda", biases=False)
+    return cfg, t
+
+
+def test_opt175b_b32_union_mlp(b32):
+    """The union MLP at full size; sampled sequences checked against the oracle."""
+    cfg, t = b32
+    sets = zipf_mlp_sets(cfg, 4)
+    idx = torch.tensor(sets, dtype=torch.int32, device="cuda")
+    out = Bd.dv_sparse_mlp(_mlp(t, biases=False), t["x"], idx, idx_per_seq=1)
+    _sync()
+    U = O.union_of_sets([s.tolist() for s in sets])
+    assert 20000 < len(U) < 30000
+    W1T, W2T = host(t["W1T"]), host(t["W2T"])
+    x = host(t["x"])
+    for b in (0, 31):
+        ref = O.mlp_sparse(x[b], W1T, None, W2T, None, U)
+        assert rel_l2(host(out)[b], ref) < REL_TOL
+
+
+def test_opt175b_b32_attention(b32):
+    cfg, t = b32
+    heads = uniform_head_sets(cfg, 4)
+    pos = [int(p) for p in t["pos"]]
+    assert 511 <= min(pos) and max(pos) <= 2047
+    Ks = {b: host(t["K"][b]).copy() for b in (0, 17)}
+    Vs = {b: host(t["V"][b]).copy() for b in (0, 17)}
+    attn, _, _, _, kv, _ = layer_objects(t, cfg.H, biases=False)
+    out = Bd.dv_sparse_attn(attn, t["x"], kv, torch.tensor(heads, device="cuda"), 1.0 / np.sqrt(cfg.dh))
+    _sync()
+    a = oracle_attn(t, biases=False)
+    x = host(t["x"])
+    for b in (0, 17):
+        ref, Kn, Vn, _ = O.mha_sparse(x[b], a, Ks[b], Vs[b], pos[b], heads[b], 1.0 / np.sqrt(cfg.dh))
+        assert rel_l2(host(out)[b], ref) < REL_TOL
+        for h in heads[b]:
+            assert rel_l2(host(t["K"][b, h, pos[b]]), Kn[h, pos[b]]) < 2e-3
