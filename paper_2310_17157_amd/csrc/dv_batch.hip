@@ -32,12 +32,12 @@ __device__ __forceinline__ f32x4 mfma16x16x32(f16x8 a, f16x8 b, f32x4 c) {
 
 // ------------------------------------------------------------------ union
 // One workgroup. sets[b][0..k) ascending in [0, n). U receives the union in
-// ascending order and *count its size; pos (optional) [n] the rank of i in U or -1;
-// mask (optional) [>= |U|] bit b set iff U[u] is in set b.
+// ascending order and *count its size; mask (optional) [>= |U|] bit b set iff U[u] is
+// in set b.
 template <int NT>
 __global__ void __launch_bounds__(NT) k_union(const int32_t* __restrict__ sets, int B, int k, int n,
                                               int32_t* __restrict__ U, int32_t* __restrict__ count,
-                                              int32_t* __restrict__ pos, uint32_t* __restrict__ mask) {
+                                              uint32_t* __restrict__ mask) {
   extern __shared__ uint32_t usm[];
   const int nw = (n + 31) >> 5;
   uint32_t* bits = usm;
@@ -47,9 +47,22 @@ __global__ void __launch_bounds__(NT) k_union(const int32_t* __restrict__ sets, 
   for (int w = tid; w < nw; w += NT) bits[w] = 0u;
   __syncthreads();
   const int tot = B * k;
-  for (int e = tid; e < tot; e += NT) {
-    const int i = min(max(sets[e], 0), n - 1);
-    atomicOr(&bits[i >> 5], 1u << (i & 31));
+  // 8 loads in flight per thread before their LDS atomics (one set entry each)
+  constexpr int UL = 8;
+  for (int e0 = 0; e0 < tot; e0 += NT * UL) {
+    int v[UL];
+#pragma unroll
+    for (int u = 0; u < UL; ++u) {
+      const int e = e0 + u * NT + tid;
+      v[u] = e < tot ? sets[e] : -1;
+    }
+#pragma unroll
+    for (int u = 0; u < UL; ++u) {
+      if (e0 + u * NT + tid < tot) {
+        const int i = min(max(v[u], 0), n - 1);
+        atomicOr(&bits[i >> 5], 1u << (i & 31));
+      }
+    }
   }
   __syncthreads();
   const int per = (nw + NT - 1) / NT;
@@ -60,121 +73,159 @@ __global__ void __launch_bounds__(NT) k_union(const int32_t* __restrict__ sets, 
   int base = block_excl_scan<NT>(c, red, &total);
   for (int w = w0; w < w1; ++w) {
     off[w] = base;
-    uint32_t m = bits[w];
-    while (m) {
-      const int b = __ffs(m) - 1;
-      U[base++] = w * 32 + b;
-      m &= m - 1u;
-    }
+    base += __popc(bits[w]);
   }
   if (tid == 0) *count = total;
   __syncthreads();
-  if (pos != nullptr) {
-    for (int i = tid; i < n; i += NT) {
-      const uint32_t m = bits[i >> 5];
-      const uint32_t below = m & ((1u << (i & 31)) - 1u);
-      pos[i] = ((m >> (i & 31)) & 1u) ? off[i >> 5] + __popc(below) : -1;
-    }
+  // member i goes to U[rank(i)]: consecutive lanes write consecutive ranks
+  for (int i = tid; i < n; i += NT) {
+    const uint32_t m = bits[i >> 5];
+    if ((m >> (i & 31)) & 1u) U[off[i >> 5] + __popc(m & ((1u << (i & 31)) - 1u))] = i;
   }
   if (mask != nullptr) {
     for (int u = tid; u < total; u += NT) mask[u] = 0u;
     __syncthreads();
-    for (int e = tid; e < tot; e += NT) {
-      const int i = min(max(sets[e], 0), n - 1);
-      const uint32_t m = bits[i >> 5];
-      const int r = off[i >> 5] + __popc(m & ((1u << (i & 31)) - 1u));
-      atomicOr(&mask[r], 1u << (e / k));
+    for (int e0 = 0; e0 < tot; e0 += NT * UL) {
+      int v[UL];
+#pragma unroll
+      for (int u = 0; u < UL; ++u) {
+        const int e = e0 + u * NT + tid;
+        v[u] = e < tot ? sets[e] : -1;
+      }
+#pragma unroll
+      for (int u = 0; u < UL; ++u) {
+        const int e = e0 + u * NT + tid;
+        if (e < tot) {
+          const int i = min(max(v[u], 0), n - 1);
+          const uint32_t m = bits[i >> 5];
+          const int r = off[i >> 5] + __popc(m & ((1u << (i & 31)) - 1u));
+          atomicOr(&mask[r], 1u << (e / k));
+        }
+      }
     }
   }
 }
 
-hipError_t launch_union(const int32_t* sets, int B, int k, int n, int32_t* U, int32_t* count, int32_t* pos,
-                        uint32_t* mask, hipStream_t st) {
+hipError_t launch_union(const int32_t* sets, int B, int k, int n, int32_t* U, int32_t* count, uint32_t* mask,
+                        hipStream_t st) {
   constexpr int NT = 1024;
   const int nw = (n + 31) >> 5;
   const size_t lds = (size_t)nw * 8 + (NT / 64 + 2) * sizeof(int);
-  hipLaunchKernelGGL(k_union<NT>, dim3(1), dim3(NT), lds, st, sets, B, k, n, U, count, pos, mask);
+  hipLaunchKernelGGL(k_union<NT>, dim3(1), dim3(NT), lds, st, sets, B, k, n, U, count, mask);
   return hipGetLastError();
 }
 
 // --------------------------------------------------------------- x-hat cast
 // X16[b][0..Kpad) = fp16(LN(x[b])) (g == NULL: x[b]) for b < B; zero for b >= B
-// and for k >= d. One workgroup per row b of NB.
-__global__ void __launch_bounds__(256) k_ln_cast(const float* __restrict__ x, int B, int d, int Kpad,
-                                                 const float* __restrict__ g, const float* __restrict__ be,
-                                                 float eps, _Float16* __restrict__ X16) {
-  __shared__ float red[8];
+// and for k >= d. One workgroup per row b of NB; d % 4 == 0, so rows move as float4.
+__global__ void __launch_bounds__(1024) k_ln_cast(const float* __restrict__ x, int B, int d, int Kpad,
+                                                  const float* __restrict__ g, const float* __restrict__ be,
+                                                  float eps, _Float16* __restrict__ X16) {
+  __shared__ float red[16];
   const int b = blockIdx.x;
   _Float16* o = X16 + (size_t)b * Kpad;
+  const int n4 = d >> 2;
   if (b >= B) {
-    for (int k = threadIdx.x; k < Kpad; k += 256) o[k] = (_Float16)0.f;
+    for (int k = threadIdx.x; k < Kpad; k += 1024) o[k] = (_Float16)0.f;
     return;
   }
-  const float* xr = x + (size_t)b * d;
+  const f32x4* xr = reinterpret_cast<const f32x4*>(x + (size_t)b * d);
   float mean = 0.f, rstd = 1.f;
   if (g != nullptr) {
-    float s = 0.f;
-    for (int k = threadIdx.x; k < d; k += 256) s += xr[k];
-    mean = block_sum<256>(s, red) / (float)d;
+    float sum = 0.f;
+    for (int i = threadIdx.x; i < n4; i += 1024) {
+      const f32x4 v = xr[i];
+      sum += (v[0] + v[1]) + (v[2] + v[3]);
+    }
+    mean = block_sum<1024>(sum, red) / (float)d;
     float q = 0.f;
-    for (int k = threadIdx.x; k < d; k += 256) {
-      const float a = xr[k] - mean;
-      q += a * a;
+    for (int i = threadIdx.x; i < n4; i += 1024) {
+      const f32x4 v = xr[i];
+      const float a0 = v[0] - mean, a1 = v[1] - mean, a2 = v[2] - mean, a3 = v[3] - mean;
+      q += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
     }
-    rstd = 1.0f / sqrtf(block_sum<256>(q, red) / (float)d + eps);
+    rstd = 1.0f / sqrtf(block_sum<1024>(q, red) / (float)d + eps);
   }
-  for (int k = threadIdx.x; k < Kpad; k += 256) {
-    float v = 0.f;
-    if (k < d) {
-      v = xr[k];
-      if (g != nullptr) v = (v - mean) * rstd * g[k] + (be ? be[k] : 0.f);
+  for (int i = threadIdx.x; i < (Kpad >> 2); i += 1024) {
+    f32x4 v = {0.f, 0.f, 0.f, 0.f};
+    if (i < n4) {
+      v = xr[i];
+      if (g != nullptr) {
+        const f32x4 gg = reinterpret_cast<const f32x4*>(g)[i];
+        const f32x4 bb = be ? reinterpret_cast<const f32x4*>(be)[i] : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = (v[e] - mean) * rstd * gg[e] + bb[e];
+      }
     }
-    o[k] = (_Float16)v;
+    typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+    f16x4 h;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) h[e] = (_Float16)v[e];
+    reinterpret_cast<f16x4*>(o)[i] = h;
   }
 }
 
 hipError_t launch_ln_cast(const float* x, int B, int NB, int d, int Kpad, const float* g, const float* be, float eps,
                           _Float16* X16, hipStream_t st) {
-  hipLaunchKernelGGL(k_ln_cast, dim3(NB), dim3(256), 0, st, x, B, d, Kpad, g, be, eps, X16);
+  hipLaunchKernelGGL(k_ln_cast, dim3(NB), dim3(1024), 0, st, x, B, d, Kpad, g, be, eps, X16);
   return hipGetLastError();
 }
 
 // ------------------------------------------------------------ k_mfma_rows
+template <int MODE>
 __device__ __forceinline__ int rows_count(const MrowsArgs& a) {
-  if (a.mode == kRowsIdentity) return a.nrows;
-  const int c = a.list_count ? min(*a.list_count, a.list_max) : a.list_max;
-  return a.mode == kRowsList ? c : 3 * c * a.dh;
+  if constexpr (MODE == kRowsIdentity) {
+    return a.nrows;
+  } else {
+    const int c = a.list_count ? min(*a.list_count, a.list_max) : a.list_max;
+    return MODE == kRowsList ? c : 3 * c * a.dh;
+  }
 }
 
-// Byte offset of row r's first element and its matrix (0..2).
-__device__ __forceinline__ const char* rows_ptr(const MrowsArgs& a, int r, int nrows) {
-  if (a.mode == kRowsIdentity) {
+// Rows are addressed in two steps so that the index load of a tile can be issued well
+// ahead: rows_key(r) loads the list entry row r depends on (nothing for identity
+// rows), rows_addr(r, key) forms the address without further loads.
+template <int MODE>
+__device__ __forceinline__ int rows_key(const MrowsArgs& a, int r, int nrows) {
+  if constexpr (MODE == kRowsIdentity) {
+    return 0;
+  } else if constexpr (MODE == kRowsList) {
+    return a.list[r];
+  } else {
+    const int per = nrows / 3;
+    return a.list[(r % per) / a.dh];
+  }
+}
+template <int MODE>
+__device__ __forceinline__ const char* rows_addr(const MrowsArgs& a, int r, int key, int nrows) {
+  if constexpr (MODE == kRowsIdentity) {
     return r < a.n0 ? static_cast<const char*>(a.W0) + (size_t)r * a.d * 2
                     : static_cast<const char*>(a.W1) + (size_t)(r - a.n0) * a.d * 2;
-  }
-  if (a.mode == kRowsList)
-    return static_cast<const char*>(a.W0) + (size_t)min(max(a.list[r], 0), a.list_range - 1) * a.d * 2;
-  const int per = nrows / 3;
-  const int m = r / per;
-  const int rem = r - m * per;
-  const int p = rem / a.dh, t = rem - p * a.dh;
-  const void* W = m == 0 ? a.W0 : (m == 1 ? a.W1 : a.W2);
-  const int h = min(max(a.list[p], 0), a.list_range - 1);
-  return static_cast<const char*>(W) + ((size_t)h * a.dh + t) * a.d * 2;
-}
-
-template <int NB, int U>
-__device__ __forceinline__ void mr_load(u32x4 (&w)[U], const char* rp, bool rv, int kbyte0, int kvalid_bytes,
-                                        int lg) {
-#pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int kb = kbyte0 + u * 64 + lg * 16;
-    w[u] = (rv && kb < kvalid_bytes) ? ld_stream(rp + kb) : u32x4{0u, 0u, 0u, 0u};
+  } else {
+    const int k = min(max(key, 0), a.list_range - 1);
+    if constexpr (MODE == kRowsList) {
+      return static_cast<const char*>(a.W0) + (size_t)k * a.d * 2;
+    } else {
+      const int per = nrows / 3;
+      const int m = r / per;
+      const int t = (r - m * per) % a.dh;
+      const void* W = m == 0 ? a.W0 : (m == 1 ? a.W1 : a.W2);
+      return static_cast<const char*>(W) + ((size_t)k * a.dh + t) * a.d * 2;
+    }
   }
 }
 
-template <int NB, int NW, int U>
+// One workgroup per CU. Per wavefront and 16-row tile, each load instruction fetches
+// whole 128-byte lines (8 rows x 8 lanes x 16 bytes): fetching the MFMA operand layout
+// straight from memory (16 rows x 64 bytes per instruction) runs at about 70% of the
+// bandwidth of whole-line loads. Each 64-element block of the tile's 16 rows is then
+// re-laid through a 2 KB per-wavefront LDS tile (16-byte chunk c of row r stored at
+// c ^ (r & 7), conflict-free both ways) into the A operand: lane (lr, lg) takes row lr,
+// chunk 4h + lg for k-step h of the block, which is exactly the k-range the B operand
+// (x-hat from LDS) supplies for that lane group.
+template <int NB, int NW, int U, int MODE>
 __global__ void __launch_bounds__(NW * 64) k_mfma_rows(MrowsArgs a) {
+  static_assert(U % 2 == 0, "a batch is whole 64-element blocks");
   constexpr int NT = NW * 64;
   constexpr int NBT = NB / 16;
   extern __shared__ __attribute__((aligned(16))) _Float16 xs[];
@@ -192,83 +243,91 @@ __global__ void __launch_bounds__(NW * 64) k_mfma_rows(MrowsArgs a) {
   }
   __syncthreads();
 
-  const int n = rows_count(a);
+  const int n = rows_count<MODE>(a);
   const int ntiles = (n + 15) >> 4;
   const int wave = tid >> 6, lane = tid & 63;
   const int lr = lane & 15, lg = lane >> 4;
+  _Float16* at = xs + NB * ldx + wave * (16 * 64);    // this wavefront's re-layout tile
   const int tstride = G * NW;
   int tile = g * NW + wave;
   if (tile >= ntiles) return;                    // no barrier follows
-  const int nbat = a.Ks / (32 * U);              // batches of U k-steps per tile
-  const int kvalid = min(a.Ks, a.d - k0) * 2;    // valid bytes of this split in a row
-  const int kb0 = k0 * 2;
+  const int nbat = a.Ks / (32 * U);              // batches of U instructions (U/2 blocks)
+  const int kvalid = min(a.Ks, a.d - k0) * 2;    // valid bytes of this split in a row (>= 16)
+  const int cb = (lane & 7) * 16;                // this lane's 16 bytes of a 128-byte block
+  const int rl0 = lane >> 3, rl1 = 8 + (lane >> 3);   // its rows of a tile (even / odd loads)
 
-  auto row_of = [&](int t, const char** rp, bool* rv) {
-    const int r = t * 16 + lr;
-    *rv = r < n;
-    *rp = rows_ptr(a, *rv ? r : 0, n) + kb0;
-  };
-  f32x4 acc[NBT];
+  auto key_of = [&](int t, int rl) { return rows_key<MODE>(a, min(t * 16 + rl, n - 1), n); };
+  int key0 = key_of(tile, rl0), key1 = key_of(tile, rl1);
+  for (; tile < ntiles; tile += tstride) {
+    const int r0 = tile * 16 + rl0, r1 = tile * 16 + rl1;
+    const char* p0 = rows_addr<MODE>(a, min(r0, n - 1), key0, n) + k0 * 2;
+    const char* p1 = rows_addr<MODE>(a, min(r1, n - 1), key1, n) + k0 * 2;
+    // the next tile's row keys, loaded a whole tile ahead (clamped, unconditional)
+    const int tn = min(tile + tstride, ntiles - 1);
+    key0 = key_of(tn, rl0);
+    key1 = key_of(tn, rl1);
+    f32x4 acc[NBT];
 #pragma unroll
-  for (int j = 0; j < NBT; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  const char* rp;
-  bool rv;
-  row_of(tile, &rp, &rv);
-  int bi = 0;
-  u32x4 wa[U];
-  mr_load<NB, U>(wa, rp, rv, 0, kvalid, lg);
-  for (;;) {
-    int ntile = tile, nbi = bi + 1;
-    const char* nrp = rp;
-    bool nrv = rv;
-    if (nbi == nbat) {
-      nbi = 0;
-      ntile = tile + tstride;
-      if (ntile < ntiles) row_of(ntile, &nrp, &nrv);
-    }
-    const bool more = ntile < ntiles;
-    u32x4 wb[U];
-    if (more) mr_load<NB, U>(wb, nrp, nrv, nbi * U * 64, kvalid, lg);
+    for (int j = 0; j < NBT; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int bi = 0; bi < nbat; ++bi) {
+      // All U loads are issued before any result is touched; chunks past the row or
+      // past n (clamped, in-bounds loads) are zeroed only when written to LDS, so that
+      // no select waits on a load right after issuing it.
+      u32x4 w[U];
+      unsigned okm = 0u;
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int ks = bi * U + u;
-      const f16x8 av = __builtin_bit_cast(f16x8, wa[u]);
-#pragma unroll
-      for (int j = 0; j < NBT; ++j) {
-        const f16x8 bv = *reinterpret_cast<const f16x8*>(xs + (lr + 16 * j) * ldx + 32 * ks + 8 * lg);
-        acc[j] = mfma16x16x32(av, bv, acc[j]);
+      for (int u = 0; u < U; ++u) {
+        const int off = (bi * (U / 2) + (u >> 1)) * 128 + cb;
+        okm |= (off < kvalid && ((u & 1) ? r1 : r0) < n) ? (1u << u) : 0u;
+        w[u] = ld_stream(((u & 1) ? p1 : p0) + min(off, kvalid - 16));
       }
-    }
-    if (bi == nbat - 1) {
-      // tile done: lane holds rows tile*16 + 4*lg + i, token columns lr + 16*j
 #pragma unroll
-      for (int j = 0; j < NBT; ++j) {
-        const int b = lr + 16 * j;
+      for (int blk = 0; blk < U / 2; ++blk) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int r = tile * 16 + 4 * lg + i;
-          if (r < n) {
-            if (a.out0 != nullptr) {
-              if (b < a.B) {
-                if (r < a.n0) a.out0[(size_t)b * a.ld0 + r] = acc[j][i];
-                else a.out1[(size_t)b * a.ld1 + (r - a.n0)] = acc[j][i];
-              }
-            } else {
-              a.P[((size_t)s * a.nrows_pad + r) * NB + b] = acc[j][i];
-            }
+        for (int i = 0; i < 2; ++i) {
+          const int r = rl0 + 8 * i, c = lane & 7;
+          const int u = 2 * blk + i;
+          *reinterpret_cast<u32x4*>(at + r * 64 + ((c ^ (r & 7)) << 3)) =
+              ((okm >> u) & 1u) ? w[u] : u32x4{0u, 0u, 0u, 0u};
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int c = 4 * h + lg;
+          const f16x8 av = *reinterpret_cast<const f16x8*>(at + lr * 64 + ((c ^ (lr & 7)) << 3));
+          const int ks = 2 * (bi * (U / 2) + blk) + h;
+#pragma unroll
+          for (int j = 0; j < NBT; ++j) {
+            const f16x8 bv = *reinterpret_cast<const f16x8*>(xs + (lr + 16 * j) * ldx + 32 * ks + 8 * lg);
+            acc[j] = mfma16x16x32(av, bv, acc[j]);
           }
         }
-        acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
       }
     }
-    if (!more) break;
+    // lane holds rows tile*16 + 4*lg + i, token columns lr + 16*j
 #pragma unroll
-    for (int u = 0; u < U; ++u) wa[u] = wb[u];
-    tile = ntile;
-    bi = nbi;
-    rp = nrp;
-    rv = nrv;
+    for (int j = 0; j < NBT; ++j) {
+      const int b = lr + 16 * j;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = tile * 16 + 4 * lg + i;
+        if (r < n) {
+          if (a.out0 != nullptr) {
+            if (b < a.B) {
+              if (r < a.n0) a.out0[(size_t)b * a.ld0 + r] = acc[j][i];
+              else a.out1[(size_t)b * a.ld1 + (r - a.n0)] = acc[j][i];
+            }
+          } else {
+            a.P[((size_t)s * a.nrows_pad + r) * NB + b] = acc[j][i];
+          }
+        }
+      }
+    }
   }
 }
 
@@ -284,10 +343,11 @@ static int lds_budget() {
 }
 
 // K per split for k_mfma_rows: a multiple of 32 * kMrU halves whose staged slice of
-// NB rows fits the LDS budget (at most 128 KB).
-static constexpr int kMrU = 8;
+// NB rows fits 96 KB of LDS (with the re-layout tiles, one workgroup per CU).
+static constexpr int kMrU = 8, kMrNW = 8;
+static constexpr int kMrTileBytes = kMrNW * 16 * 64 * 2;
 void mrows_split(int Kpad, int NB, int* S, int* Ks) {
-  const int budget = min(lds_budget(), 131072);
+  const int budget = min(lds_budget() - kMrTileBytes, 98304 + NB * 16);
   const int unit = 32 * kMrU;
   int kmax = ((budget / (NB * 2) - 8) / unit) * unit;
   if (kmax < unit) kmax = unit;
@@ -297,24 +357,32 @@ void mrows_split(int Kpad, int NB, int* S, int* Ks) {
   *Ks = ks;
 }
 
-template <int NB>
+template <int NB, int MODE>
 static hipError_t launch_mrows_t(MrowsArgs a, hipStream_t st) {
-  constexpr int NW = 8;
-  const size_t lds = (size_t)NB * (a.Ks + 8) * 2;
-  const auto kern = k_mfma_rows<NB, NW, kMrU>;
+  const size_t lds = (size_t)NB * (a.Ks + 8) * 2 + kMrTileBytes;
+  const auto kern = k_mfma_rows<NB, kMrNW, kMrU, MODE>;
   static bool attr = false;
   if (!attr) {
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
-                              (int)min(lds_budget(), 131072));
+                              lds_budget());
     attr = true;
   }
   const int G = max(1, device_cu_count() / a.S);
-  hipLaunchKernelGGL(kern, dim3(G * a.S), dim3(NW * 64), lds, st, a);
+  hipLaunchKernelGGL(kern, dim3(G * a.S), dim3(kMrNW * 64), lds, st, a);
   return hipGetLastError();
 }
 
+template <int NB>
+static hipError_t launch_mrows_nb(const MrowsArgs& a, hipStream_t st) {
+  switch (a.mode) {
+    case kRowsList: return launch_mrows_t<NB, kRowsList>(a, st);
+    case kRowsHeads: return launch_mrows_t<NB, kRowsHeads>(a, st);
+    default: return launch_mrows_t<NB, kRowsIdentity>(a, st);
+  }
+}
+
 hipError_t launch_mrows(int NB, const MrowsArgs& a, hipStream_t st) {
-  return NB <= 16 ? launch_mrows_t<16>(a, st) : launch_mrows_t<32>(a, st);
+  return NB <= 16 ? launch_mrows_nb<16>(a, st) : launch_mrows_nb<32>(a, st);
 }
 
 // ------------------------------------------------------------ k_mfma_cols
@@ -332,33 +400,58 @@ __device__ __forceinline__ size_t cols_row(const McolsArgs& a, int u) {
 // Wavefront tile in LDS: 32 rows x 64 columns fp16, 16-byte chunk c of row r stored at
 // chunk c ^ (2 * ((r >> 3) & 3)) so that both the row-wise 16-byte writes and the
 // column-wise 2-byte reads of the transpose are free of bank conflicts.
+//
+// Load pipeline of a wavefront: the row indices of batch k+2, the weights and
+// coefficients of batch k+1 and the MFMAs of batch k are in flight together. Indices
+// are always loaded one batch before the weights that need them, so no wait for an
+// index ever drains the weight loads behind it.
 template <int NB, int U>
 struct ColsStep {
   u32x4 w[U][4];        // weights: rows (lane >> 3) + 8*i, 16-byte chunk lane & 7
   u32x4 h[U][NB / 16];  // coefficients: token lr + 16*j, rows 8*lg .. 8*lg + 7
+  unsigned ok;          // bit 4u + i: weight chunk w[u][i] is wanted (else written as 0)
 };
 
-template <int NB, int U>
-__device__ __forceinline__ void mc_load(ColsStep<NB, U>& st, const McolsArgs& a, const char* Mb, int q0, int qend,
-                                        int qstride, int uend, bool col_on, int lane) {
-  const int lr = lane & 15, lg = lane >> 4;
-  const size_t rowb = (size_t)a.d * 2;
+// Row of M for contraction row `row` (clamped into [0, uend) so that every load is in
+// bounds; rows past uend are zeroed after the load).
+template <bool HEADS, int U>
+__device__ __forceinline__ void mc_index(int (&ix)[U][4], const McolsArgs& a, int q0, int qstride, int uend,
+                                         int lane) {
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int q = q0 + u * qstride;
-    const bool on = q < qend;
+  for (int u = 0; u < U; ++u)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int row = 32 * q + (lane >> 3) + 8 * i;
-      st.w[u][i] = (on && col_on && row < uend) ? ld_stream(Mb + cols_row(a, row) * rowb) : u32x4{0u, 0u, 0u, 0u};
+      const int row = min(32 * (q0 + u * qstride) + (lane >> 3) + 8 * i, uend - 1);
+      if (HEADS) {
+        const int p = row / a.dh;
+        ix[u][i] = min(max(a.list[p], 0), a.list_range - 1) * a.dh + (row - p * a.dh);
+      } else {
+        ix[u][i] = min(max(a.list[row], 0), a.list_range - 1);
+      }
+    }
+}
+
+template <int NB, int U>
+__device__ __forceinline__ void mc_load(ColsStep<NB, U>& st, const int (&ix)[U][4], const McolsArgs& a,
+                                        const char* Mb, int q0, int qstride, int uend, bool col_on, int lane) {
+  const int lr = lane & 15, lg = lane >> 4;
+  const size_t rowb = (size_t)a.d * 2;
+  st.ok = 0u;
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int q = min(q0 + u * qstride, (uend - 1) >> 5);     // clamped: loads stay in bounds
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = 32 * (q0 + u * qstride) + (lane >> 3) + 8 * i;
+      st.ok |= (col_on && row < uend) ? (1u << (4 * u + i)) : 0u;
+      st.w[u][i] = ld_stream(Mb + (size_t)ix[u][i] * rowb);
     }
 #pragma unroll
-    for (int j = 0; j < NB / 16; ++j)
-      st.h[u][j] = on ? ld_plain(a.C + (size_t)(lr + 16 * j) * a.ldc + 32 * q + 8 * lg) : u32x4{0u, 0u, 0u, 0u};
+    for (int j = 0; j < NB / 16; ++j) st.h[u][j] = ld_plain(a.C + (size_t)(lr + 16 * j) * a.ldc + 32 * q + 8 * lg);
   }
 }
 
-template <int NB, int NW, int U>
+template <int NB, int NW, int U, bool HEADS>
 __global__ void __launch_bounds__(NW * 64) k_mfma_cols(McolsArgs a) {
   constexpr int NBT = NB / 16;
   extern __shared__ __attribute__((aligned(16))) _Float16 csm[];
@@ -382,13 +475,22 @@ __global__ void __launch_bounds__(NW * 64) k_mfma_cols(McolsArgs a) {
     for (int t = 0; t < 4; ++t) acc[j][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int qstride = NW;
+  const int bstep = qstride * U;                 // k-steps per batch of this wavefront
   int q = qbeg + wave;
-  ColsStep<NB, U> cur;
-  mc_load<NB, U>(cur, a, Mb, q, qend, qstride, uend, col_on, lane);
-  for (; q < qend; q += qstride * U) {
+  if (q < qend) {
+    int ix0[U][4], ix1[U][4];
+    mc_index<HEADS, U>(ix0, a, q, qstride, uend, lane);
+    mc_index<HEADS, U>(ix1, a, q + bstep, qstride, uend, lane);
+    ColsStep<NB, U> cur;
+    mc_load<NB, U>(cur, ix0, a, Mb, q, qstride, uend, col_on, lane);
+  for (; q < qend; q += bstep) {
     ColsStep<NB, U> nxt;
-    const bool more = q + qstride * U < qend;
-    if (more) mc_load<NB, U>(nxt, a, Mb, q + qstride * U, qend, qstride, uend, col_on, lane);
+    const bool more = q + bstep < qend;
+    // issued unconditionally (clamped in-bounds past the end, then discarded) so that
+    // the waits below never have to drain them
+    mc_index<HEADS, U>(ix0, a, q + 2 * bstep, qstride, uend, lane);          // batch k+2
+    mc_load<NB, U>(nxt, ix1, a, Mb, q + bstep, qstride, uend, col_on, lane);  // batch k+1
+    __builtin_amdgcn_sched_barrier(0);          // keep the prefetch ahead of the MFMAs
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       if (q + u * qstride >= qend) break;
@@ -397,7 +499,8 @@ __global__ void __launch_bounds__(NW * 64) k_mfma_cols(McolsArgs a) {
       for (int i = 0; i < 4; ++i) {
         const int r = (lane >> 3) + 8 * i;
         const int c = (lane & 7) ^ (2 * i);
-        *reinterpret_cast<u32x4*>(tile + r * 64 + c * 8) = cur.w[u][i];
+        *reinterpret_cast<u32x4*>(tile + r * 64 + c * 8) =
+            ((cur.ok >> (4 * u + i)) & 1u) ? cur.w[u][i] : u32x4{0u, 0u, 0u, 0u};
       }
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
@@ -423,6 +526,11 @@ __global__ void __launch_bounds__(NW * 64) k_mfma_cols(McolsArgs a) {
     }
     if (!more) break;
     cur = nxt;
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) ix1[u][i] = ix0[u][i];
+  }
   }
   // ---- reduce the wavefronts' partials in a fixed order
 #pragma unroll
@@ -458,7 +566,10 @@ template <int NB>
 static hipError_t launch_mcols_t(const McolsArgs& a, hipStream_t st) {
   const size_t lds = (size_t)kMcNW * 32 * 64 * 2 + (size_t)kMcNW * NB * 64 * 4;
   dim3 grid((a.d + 63) / 64, a.S);
-  hipLaunchKernelGGL((k_mfma_cols<NB, kMcNW, kMcU>), grid, dim3(kMcNW * 64), lds, st, a);
+  if (a.dh > 0)
+    hipLaunchKernelGGL((k_mfma_cols<NB, kMcNW, kMcU, true>), grid, dim3(kMcNW * 64), lds, st, a);
+  else
+    hipLaunchKernelGGL((k_mfma_cols<NB, kMcNW, kMcU, false>), grid, dim3(kMcNW * 64), lds, st, a);
   return hipGetLastError();
 }
 
@@ -467,6 +578,19 @@ hipError_t launch_mcols(int NB, const McolsArgs& a, hipStream_t st) {
 }
 
 // --------------------------------------------------------------- finishers
+// sum_{s < S} P[s * stride + e] in split order, with up to 8 loads in flight.
+__device__ __forceinline__ float sum_splits(const float* __restrict__ P, int S, size_t stride, size_t e) {
+  float v = 0.f;
+  for (int s0 = 0; s0 < S; s0 += 8) {
+    float t[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) t[u] = s0 + u < S ? P[(size_t)(s0 + u) * stride + e] : 0.f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v += t[u];
+  }
+  return v;
+}
+
 // fc1: C[b][u] = fp16(ReLU(sum_s P[s][u][b] + b1[list[u]])) for b < B and u < n (and,
 // with a mask, only where bit b of mask[u] is set); zero elsewhere up to a multiple
 // of 64 rows. One workgroup per 64 rows.
@@ -481,7 +605,7 @@ __global__ void __launch_bounds__(256) k_fc1_finish(Fc1FinishArgs a) {
     const int u = u0 + ul;
     float v = 0.f;
     if (u < n && b < a.B) {
-      for (int s = 0; s < a.S; ++s) v += a.P[((size_t)s * a.nrows_pad + u) * NB + b];
+      v = sum_splits(a.P, a.S, (size_t)a.nrows_pad * NB, (size_t)u * NB + b);
       if (a.b1) v += a.b1[min(max(a.list[u], 0), a.list_range - 1)];
       v = v > 0.f ? v : 0.f;
       if (a.mask && !((a.mask[u] >> b) & 1u)) v = 0.f;
@@ -509,8 +633,7 @@ __global__ void __launch_bounds__(256) k_cols_finish(ColsFinishArgs a) {
   const long total = (long)a.B * a.d;
   for (long e = (long)blockIdx.x * 256 + threadIdx.x; e < total; e += (long)gridDim.x * 256) {
     const int c = (int)(e % a.d);
-    float v = 0.f;
-    for (int s = 0; s < a.S; ++s) v += a.P[(size_t)s * total + e];
+    float v = sum_splits(a.P, a.S, (size_t)total, (size_t)e);
     if (a.bias) v += a.bias[c];
     if (a.resid) v += a.resid[e];
     a.out[e] = v;
@@ -534,8 +657,7 @@ __global__ void __launch_bounds__(256) k_sum_cast(const float* __restrict__ P, i
   for (int e = blockIdx.x * 256 + threadIdx.x; e < total; e += gridDim.x * 256) {
     const int b = e / ldc, j = e - b * ldc;
     float v = 0.f;
-    if (b < B && j < r)
-      for (int s = 0; s < S; ++s) v += P[((size_t)s * nrows_pad + row0 + j) * NB + b];
+    if (b < B && j < r) v = sum_splits(P, S, (size_t)nrows_pad * NB, (size_t)(row0 + j) * NB + b);
     C[e] = (_Float16)v;
   }
 }
@@ -550,41 +672,65 @@ hipError_t launch_sum_cast(int NB, const float* P, int S, int nrows_pad, int row
   return hipGetLastError();
 }
 
-// Q/K/V of the batch: for sequence b and its j-th selected head h (union rank p),
-// value of projection m at t = sum_s P[s][(m*nu + p)*dh + t][b] + bias; q goes to
-// q[b][j][t], k and v to the cache at row pos[b] of head h (round to nearest even).
+// Q/K/V of the batch. One workgroup per (union head p, projection m): the dh x NB
+// partial sums of its rows are read contiguously, summed over the splits in order and
+// biased; then for every sequence b whose set holds h = list[p] (as its j-th head) the
+// query goes to q[b][j][:] (m = 0) or the key/value to cache row pos[b] of head h
+// (m = 1, 2; round to nearest even).
 template <int NB, typename KT>
 __global__ void __launch_bounds__(256) k_qkv_finish(QkvFinishArgs a) {
-  const int j = blockIdx.x, b = blockIdx.y;
-  const int h = min(max(a.heads[(size_t)b * a.n_heads + j], 0), a.H - 1);
-  const int p = a.hpos[h];
+  extern __shared__ float qsm[];                  // [dh][NB + 1]
+  __shared__ int jsel[NB];
+  const int p = blockIdx.x, m = blockIdx.y;
   const int nu = *a.hcount;
-  const int pos = a.posb[b];
-  if (p < 0 || p >= nu) return;
-  for (int e = threadIdx.x; e < 3 * a.dh; e += 256) {
-    const int m = e / a.dh, t = e - m * a.dh;
-    const int r = (m * nu + p) * a.dh + t;
-    float v = 0.f;
-    for (int s = 0; s < a.S; ++s) v += a.P[((size_t)s * a.nrows_pad + r) * NB + b];
-    const float* bias = m == 0 ? a.bq : (m == 1 ? a.bk : a.bv);
+  if (p >= nu) return;
+  const int h = min(max(a.hlist[p], 0), a.H - 1);
+  if (threadIdx.x < NB) {
+    int jj = -1;
+    const int b = threadIdx.x;
+    if (b < a.B) {
+      const int32_t* hs = a.heads + (size_t)b * a.n_heads;
+      int lo = 0, hi = a.n_heads - 1;
+      while (lo <= hi) {
+        const int mid = (lo + hi) >> 1;
+        if (hs[mid] == h) { jj = mid; break; }
+        if (hs[mid] < h) lo = mid + 1; else hi = mid - 1;
+      }
+    }
+    jsel[b] = jj;
+  }
+  const size_t r0 = ((size_t)m * nu + p) * a.dh;
+  const float* bias = m == 0 ? a.bq : (m == 1 ? a.bk : a.bv);
+  for (int e = threadIdx.x; e < a.dh * NB; e += 256) {
+    const int t = e / NB, b = e - t * NB;
+    float v = sum_splits(a.P, a.S, (size_t)a.nrows_pad * NB, (r0 + t) * NB + b);
     if (bias) v += bias[(size_t)h * a.dh + t];
+    qsm[t * (NB + 1) + b] = v;
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < a.dh * NB; e += 256) {
+    const int b = e / a.dh, t = e - b * a.dh;
+    const int jj = jsel[b];
+    if (jj < 0) continue;
+    const float v = qsm[t * (NB + 1) + b];
     if (m == 0) {
-      a.q[((size_t)b * a.n_heads + j) * a.dh + t] = v;
+      a.q[((size_t)b * a.n_heads + jj) * a.dh + t] = v;
     } else {
       KT* Cc = static_cast<KT*>(m == 1 ? a.K : a.V);
-      Cc[(((size_t)b * a.H + h) * a.cap + pos) * a.dh + t] = (KT)v;
+      Cc[(((size_t)b * a.H + h) * a.cap + a.posb[b]) * a.dh + t] = (KT)v;
     }
   }
 }
 
 hipError_t launch_qkv_finish(int NB, int kvtype, const QkvFinishArgs& a, hipStream_t st) {
-  dim3 grid(a.n_heads, a.B);
+  dim3 grid(a.H, 3);
+  const size_t lds = (size_t)a.dh * (NB + 1) * sizeof(float);
   if (NB <= 16) {
-    if (kvtype == DV_F16) hipLaunchKernelGGL((k_qkv_finish<16, _Float16>), grid, dim3(256), 0, st, a);
-    else hipLaunchKernelGGL((k_qkv_finish<16, float>), grid, dim3(256), 0, st, a);
+    if (kvtype == DV_F16) hipLaunchKernelGGL((k_qkv_finish<16, _Float16>), grid, dim3(256), lds, st, a);
+    else hipLaunchKernelGGL((k_qkv_finish<16, float>), grid, dim3(256), lds, st, a);
   } else {
-    if (kvtype == DV_F16) hipLaunchKernelGGL((k_qkv_finish<32, _Float16>), grid, dim3(256), 0, st, a);
-    else hipLaunchKernelGGL((k_qkv_finish<32, float>), grid, dim3(256), 0, st, a);
+    if (kvtype == DV_F16) hipLaunchKernelGGL((k_qkv_finish<32, _Float16>), grid, dim3(256), lds, st, a);
+    else hipLaunchKernelGGL((k_qkv_finish<32, float>), grid, dim3(256), lds, st, a);
   }
   return hipGetLastError();
 }

@@ -59,7 +59,7 @@ static dv_status bmlp_run(const dv_mlp* m, const BMlp& o, int B, const int32_t* 
   const int32_t* list_count = nullptr;
   int list_max = n_idx;
   if (per_seq) {
-    DV_LAUNCH("union", hs, launch_union(idx, B, n_idx, m->n, o.U, o.cnt, nullptr, masked ? o.mask : nullptr, hs));
+    DV_LAUNCH("union", hs, launch_union(idx, B, n_idx, m->n, o.U, o.cnt, masked ? o.mask : nullptr, hs));
     list = o.U;
     list_count = o.cnt;
     list_max = o.umax;
@@ -100,7 +100,7 @@ dv_status batch_mlp(const dv_mlp* m, const float* x, int B, const int32_t* idx, 
 
 // ---------------------------------------------------------------- attention
 struct BAttn {
-  _Float16* X16; int32_t* Uh; int32_t* hcnt; int32_t* hpos; float* P; float* q; float* part; _Float16* C;
+  _Float16* X16; int32_t* Uh; int32_t* hcnt; float* P; float* q; float* part; _Float16* C;
   float* P2;
   int Kpad, S, Ks, nrows_pad, ldc, S2;
 };
@@ -115,7 +115,6 @@ static size_t battn_layout(const dv_attn* a, int B, int n_heads, Workspace& w, B
   o->X16 = w.take<_Float16>((size_t)NB * o->Kpad * 2);
   o->Uh = w.take<int32_t>((size_t)a->H * 4);
   o->hcnt = w.take<int32_t>(4);
-  o->hpos = w.take<int32_t>((size_t)a->H * 4);
   o->P = w.take<float>((size_t)o->S * o->nrows_pad * NB * 4);
   o->q = w.take<float>((size_t)B * std::max(n_heads, 1) * a->dh * 4);
   o->part = w.take<float>((size_t)B * std::max(n_heads, 1) * kAttnMaxSplit * (a->dh + 2) * 4);
@@ -141,7 +140,7 @@ static dv_status battn_run(const dv_attn* a, const dv_kv* kv, const BAttn& o, in
     DV_LAUNCH("oproj_finish", hs, launch_cols_finish(e, hs));
     return DV_OK;
   }
-  DV_LAUNCH("union_heads", hs, launch_union(heads, B, n_heads, a->H, o.Uh, o.hcnt, o.hpos, nullptr, hs));
+  DV_LAUNCH("union_heads", hs, launch_union(heads, B, n_heads, a->H, o.Uh, o.hcnt, nullptr, hs));
   MrowsArgs r{};
   r.d = a->d; r.Kpad = o.Kpad; r.Ks = o.Ks; r.S = o.S; r.X = o.X16; r.mode = kRowsHeads;
   r.W0 = a->Wq; r.W1 = a->Wk; r.W2 = a->Wv; r.list = o.Uh; r.list_count = o.hcnt; r.list_max = a->H;
@@ -150,7 +149,7 @@ static dv_status battn_run(const dv_attn* a, const dv_kv* kv, const BAttn& o, in
   DV_LAUNCH("qkv", hs, launch_mrows(NB, r, hs));
   QkvFinishArgs qf{};
   qf.P = o.P; qf.S = o.S; qf.nrows_pad = o.nrows_pad; qf.heads = heads; qf.n_heads = n_heads; qf.H = a->H;
-  qf.dh = a->dh; qf.cap = kv->cap; qf.B = B; qf.hpos = o.hpos; qf.hcount = o.hcnt;
+  qf.dh = a->dh; qf.cap = kv->cap; qf.B = B; qf.hlist = o.Uh; qf.hcount = o.hcnt;
   qf.bq = a->bq; qf.bk = a->bk; qf.bv = a->bv; qf.q = o.q; qf.K = kv->K; qf.V = kv->V;
   int maxpos = 0;
   for (int b = 0; b < B; ++b) {

@@ -425,10 +425,10 @@ struct Fc1Args {
 hipError_t launch_fc1(int wtype, const Fc1Args& a, hipStream_t st);
 
 // ------------------------------------------------ batched (matrix-core) path
-// Union of B ascending sets (one workgroup): U ascending, *count, optional rank map
-// pos[n] (-1 outside) and membership bits mask[u] (bit b: U[u] is in set b).
-hipError_t launch_union(const int32_t* sets, int B, int k, int n, int32_t* U, int32_t* count, int32_t* pos,
-                        uint32_t* mask, hipStream_t st);
+// Union of B ascending sets (one workgroup): U ascending, *count and optional
+// membership bits mask[u] (bit b: U[u] is in set b).
+hipError_t launch_union(const int32_t* sets, int B, int k, int n, int32_t* U, int32_t* count, uint32_t* mask,
+                        hipStream_t st);
 
 // X16[NB][Kpad] = fp16(LN(x)) (g NULL: x), zero rows b >= B and columns k >= d.
 hipError_t launch_ln_cast(const float* x, int B, int NB, int d, int Kpad, const float* g, const float* be, float eps,
@@ -494,7 +494,7 @@ hipError_t launch_sum_cast(int NB, const float* P, int S, int nrows_pad, int row
 struct QkvFinishArgs {
   const float* P; int S, nrows_pad;
   const int32_t* heads; int n_heads, H, dh, cap, B;
-  const int32_t* hpos; const int32_t* hcount;
+  const int32_t* hlist; const int32_t* hcount;     // union of the head sets and its size
   const float* bq; const float* bk; const float* bv;
   float* q; void* K; void* V;
   int posb[kMaxBatch];
