@@ -16,8 +16,8 @@
 //                 each wavefront streams 16-row tiles straight into MFMA operands.
 //   k_mfma_cols   P2[s][b][n] = sum_{u in split s} C[b][u] M[row(u)][n]: gathered rows
 //                 contracted over the row index (fc2, out-projection). Row tiles are
-//                 transposed through a per-wavefront LDS tile (XOR-swizzled, no bank
-//                 conflicts) into the B operand.
+//                 written to a per-wavefront LDS tile (XOR-swizzled) and read back
+//                 column-wise with the LDS transpose read into the B operand.
 //   finishers     sum the split partials in a fixed order and apply bias, ReLU,
 //                 membership masks, cache writes and residuals.
 #include <math.h>
@@ -28,6 +28,15 @@ namespace dv {
 
 __device__ __forceinline__ f32x4 mfma16x16x32(f16x8 a, f16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
+typedef short v4s_t __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x4_t __attribute__((ext_vector_type(4)));
+
+// gfx950 LDS transpose read of four 16-bit elements (p: 8-byte aligned LDS address).
+__device__ __forceinline__ v4s_t ds_read_tr16(const _Float16* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (v4s_t __attribute__((address_space(3)))*)(const_cast<_Float16*>(p)));
 }
 
 // ------------------------------------------------------------------ union
@@ -398,8 +407,8 @@ __device__ __forceinline__ size_t cols_row(const McolsArgs& a, int u) {
 }
 
 // Wavefront tile in LDS: 32 rows x 64 columns fp16, 16-byte chunk c of row r stored at
-// chunk c ^ (2 * ((r >> 3) & 3)) so that both the row-wise 16-byte writes and the
-// column-wise 2-byte reads of the transpose are free of bank conflicts.
+// chunk c ^ (2 * ((r >> 3) & 3)) so that the row-wise 16-byte writes are free of bank
+// conflicts and the four 8-row groups of a transpose read land in distinct banks.
 //
 // Load pipeline of a wavefront: the row indices of batch k+2, the weights and
 // coefficients of batch k+1 and the MFMAs of batch k are in flight together. Indices
@@ -451,15 +460,19 @@ __device__ __forceinline__ void mc_load(ColsStep<NB, U>& st, const int (&ix)[U][
   }
 }
 
-template <int NB, int NW, int U, bool HEADS>
+// WIDE: the wavefronts of a workgroup take adjacent 64-column tiles over the same rows
+// (each row is then read in NW * 128 contiguous bytes, and the coefficients are shared
+// through L1), and each writes its own partial tile. Otherwise they split the rows of
+// one 64-column tile and are summed in LDS.
+template <int NB, int NW, int U, bool HEADS, bool WIDE>
 __global__ void __launch_bounds__(NW * 64) k_mfma_cols(McolsArgs a) {
   constexpr int NBT = NB / 16;
   extern __shared__ __attribute__((aligned(16))) _Float16 csm[];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int lr = lane & 15, lg = lane >> 4;
   _Float16* tile = csm + wave * (32 * 64);
-  float* red = reinterpret_cast<float*>(csm + NW * 32 * 64);     // [NW][NB][64]
-  const int n0 = blockIdx.x * 64;
+  float* red = reinterpret_cast<float*>(csm + NW * 32 * 64);     // [NW][NB][64] (not WIDE)
+  const int n0 = WIDE ? (blockIdx.x * NW + wave) * 64 : blockIdx.x * 64;
   const int s = blockIdx.y;
   const int n = cols_count(a);
   const int us = ((n + a.S - 1) / a.S + 31) & ~31;
@@ -474,9 +487,9 @@ __global__ void __launch_bounds__(NW * 64) k_mfma_cols(McolsArgs a) {
 #pragma unroll
     for (int t = 0; t < 4; ++t) acc[j][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int qstride = NW;
+  const int qstride = WIDE ? 1 : NW;
   const int bstep = qstride * U;                 // k-steps per batch of this wavefront
-  int q = qbeg + wave;
+  int q = WIDE ? qbeg : qbeg + wave;
   if (q < qend) {
     int ix0[U][4], ix1[U][4];
     mc_index<HEADS, U>(ix0, a, q, qstride, uend, lane);
@@ -510,13 +523,21 @@ __global__ void __launch_bounds__(NW * 64) k_mfma_cols(McolsArgs a) {
       for (int j = 0; j < NBT; ++j) hv[j] = __builtin_bit_cast(f16x8, cur.h[u][j]);
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        // column-wise read: token-major B operand, rows 8*lg .. 8*lg + 7 of column 16t + lr
-        const int nl = 16 * t + lr;
-        const int pc = (nl >> 3) ^ (2 * lg);
-        const _Float16* src = tile + (8 * lg) * 64 + pc * 8 + (nl & 7);
-        f16x8 bv;
+        // Column-wise B operand (lane (n = lr, g = lg) takes rows 8g .. 8g + 7 of column
+        // 16t + n) with two LDS transpose reads. Within a 16-lane group the transpose
+        // read hands lane i, slot j element i % 4 of the 4 elements that lane 4j + i/4
+        // addressed, so lane s addresses row 8g + s/4 (+ 4 for the second read) at
+        // columns 16t + 4 (s % 4) .. + 3.
+        const int col = 16 * t + 4 * (lr & 3);
+        v4s_t half[2];
 #pragma unroll
-        for (int jj = 0; jj < 8; ++jj) bv[jj] = src[jj * 64];
+        for (int hh = 0; hh < 2; ++hh) {
+          const int r = 8 * lg + (lr >> 2) + 4 * hh;
+          const int pc = (col >> 3) ^ (2 * ((r >> 3) & 3));
+          half[hh] = ds_read_tr16(tile + r * 64 + pc * 8 + (col & 7));
+        }
+        const f16x8 bv = __builtin_shufflevector(__builtin_bit_cast(f16x4_t, half[0]),
+                                                 __builtin_bit_cast(f16x4_t, half[1]), 0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
         for (int j = 0; j < NBT; ++j) acc[j][t] = mfma16x16x32(hv[j], bv, acc[j][t]);
       }
@@ -531,6 +552,19 @@ __global__ void __launch_bounds__(NW * 64) k_mfma_cols(McolsArgs a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) ix1[u][i] = ix0[u][i];
   }
+  }
+  if constexpr (WIDE) {
+    // lane holds tokens 16j + 4lg + i of columns n0 + 16t + lr
+#pragma unroll
+    for (int j = 0; j < NBT; ++j)
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int b = 16 * j + 4 * lg + i, c = n0 + 16 * t + lr;
+          if (b < a.B && c < a.d) a.P[((size_t)s * a.B + b) * a.d + c] = acc[j][t][i];
+        }
+    return;
   }
   // ---- reduce the wavefronts' partials in a fixed order
 #pragma unroll
@@ -551,25 +585,26 @@ __global__ void __launch_bounds__(NW * 64) k_mfma_cols(McolsArgs a) {
   }
 }
 
-static constexpr int kMcNW = 4, kMcU = 2;
+static constexpr int kMcNW = 8, kMcU = 1;
+static constexpr bool kMcWide = true;
 
 int mcols_split(int d, int nmax) {
-  const int tiles = (d + 63) / 64;
-  const int target = 2 * device_cu_count();
+  const int tiles = kMcWide ? (d + 64 * kMcNW - 1) / (64 * kMcNW) : (d + 63) / 64;
+  const int target = 4 * device_cu_count();
   int s = (target + tiles - 1) / tiles;
   const int q = (nmax + 31) / 32;                  // k-steps available
-  s = max(1, min(s, max(1, q / (2 * kMcNW))));
-  return min(s, 16);
+  s = max(1, min(s, max(1, kMcWide ? q / 2 : q / (2 * kMcNW))));
+  return min(s, 32);
 }
 
 template <int NB>
 static hipError_t launch_mcols_t(const McolsArgs& a, hipStream_t st) {
-  const size_t lds = (size_t)kMcNW * 32 * 64 * 2 + (size_t)kMcNW * NB * 64 * 4;
-  dim3 grid((a.d + 63) / 64, a.S);
+  const size_t lds = (size_t)kMcNW * 32 * 64 * 2 + (kMcWide ? 0 : (size_t)kMcNW * NB * 64 * 4);
+  dim3 grid(kMcWide ? (a.d + 64 * kMcNW - 1) / (64 * kMcNW) : (a.d + 63) / 64, a.S);
   if (a.dh > 0)
-    hipLaunchKernelGGL((k_mfma_cols<NB, kMcNW, kMcU, true>), grid, dim3(kMcNW * 64), lds, st, a);
+    hipLaunchKernelGGL((k_mfma_cols<NB, kMcNW, kMcU, true, kMcWide>), grid, dim3(kMcNW * 64), lds, st, a);
   else
-    hipLaunchKernelGGL((k_mfma_cols<NB, kMcNW, kMcU, false>), grid, dim3(kMcNW * 64), lds, st, a);
+    hipLaunchKernelGGL((k_mfma_cols<NB, kMcNW, kMcU, false, kMcWide>), grid, dim3(kMcNW * 64), lds, st, a);
   return hipGetLastError();
 }
 
