@@ -7,7 +7,7 @@
 // the per-sequence sets (the union is what turns B sparse GEMVs into one sparse
 // GEMM); each fetched row is read from HBM once per call.
 //
-//   k_union       union of B ascending index sets (LDS bitmap), its ranks, and
+//   k_union_*     union of B ascending index sets (chunked bitmaps, then ranks), and
 //                 per-row membership bits of the sequences.
 //   k_ln_cast     x-hat = LN(x) (or x) as fp16 [NB][Kpad], zero padded.
 //   k_mfma_rows   P[s][r][b] = sum_{k in split s} W[row(r)][k] x-hat[b][k]: gathered
@@ -40,87 +40,113 @@ __device__ __forceinline__ v4s_t ds_read_tr16(const _Float16* p) {
 }
 
 // ------------------------------------------------------------------ union
-// One workgroup. sets[b][0..k) ascending in [0, n). U receives the union in
-// ascending order and *count its size; mask (optional) [>= |U|] bit b set iff U[u] is
-// in set b.
-template <int NT>
-__global__ void __launch_bounds__(NT) k_union(const int32_t* __restrict__ sets, int B, int k, int n,
-                                              int32_t* __restrict__ U, int32_t* __restrict__ count,
-                                              uint32_t* __restrict__ mask) {
-  extern __shared__ uint32_t usm[];
-  const int nw = (n + 31) >> 5;
-  uint32_t* bits = usm;
-  int* off = reinterpret_cast<int*>(usm + nw);
-  int* red = off + nw;
-  const int tid = threadIdx.x;
-  for (int w = tid; w < nw; w += NT) bits[w] = 0u;
+// Union of B ascending sets sets[b][0..k) in [0, n), in two launches over chunks of
+// kUnionChunk indices (one workgroup per chunk):
+//   k_union_bits   the chunk's bitmap (LDS atomics from each set's entries inside the
+//                  chunk, found by binary search) and its member count;
+//   k_union_write  the chunk's offset (sum of the counts before it), the members in
+//                  ascending order at U[offset + rank], the total in *count, and
+//                  optionally the membership bits mask[u] (bit b: U[u] is in set b).
+constexpr int kUnionChunk = 2048;
+constexpr int kUnionNT = 256;
+
+__device__ __forceinline__ int lower_bound_i32(const int32_t* __restrict__ v, int len, int key) {
+  int lo = 0, hi = len;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (v[mid] < key) lo = mid + 1; else hi = mid;
+  }
+  return lo;
+}
+
+__global__ void __launch_bounds__(kUnionNT) k_union_bits(const int32_t* __restrict__ sets, int B, int k, int n,
+                                                         uint32_t* __restrict__ bits, int32_t* __restrict__ cnt) {
+  __shared__ uint32_t wb[kUnionChunk / 32];
+  __shared__ int red[kUnionNT / 64 + 1];
+  const int c = blockIdx.x, tid = threadIdx.x;
+  const int lo_i = c * kUnionChunk, hi_i = min(n, lo_i + kUnionChunk);
+  for (int w = tid; w < kUnionChunk / 32; w += kUnionNT) wb[w] = 0u;
   __syncthreads();
-  const int tot = B * k;
-  // 8 loads in flight per thread before their LDS atomics (one set entry each)
-  constexpr int UL = 8;
-  for (int e0 = 0; e0 < tot; e0 += NT * UL) {
-    int v[UL];
-#pragma unroll
-    for (int u = 0; u < UL; ++u) {
-      const int e = e0 + u * NT + tid;
-      v[u] = e < tot ? sets[e] : -1;
-    }
-#pragma unroll
-    for (int u = 0; u < UL; ++u) {
-      if (e0 + u * NT + tid < tot) {
-        const int i = min(max(v[u], 0), n - 1);
-        atomicOr(&bits[i >> 5], 1u << (i & 31));
-      }
+  // threads are spread over the sets: set b gets (kUnionNT / B) or more threads
+  for (int b = tid % B, r = tid / B, nr = (kUnionNT - tid % B + B - 1) / B; b < B; b += kUnionNT) {
+    const int32_t* sb = sets + (size_t)b * k;
+    const int e0 = lower_bound_i32(sb, k, lo_i), e1 = lower_bound_i32(sb, k, hi_i);
+    for (int e = e0 + r; e < e1; e += nr) {
+      const int i = sb[e] - lo_i;
+      if (i >= 0 && i < kUnionChunk) atomicOr(&wb[i >> 5], 1u << (i & 31));
     }
   }
   __syncthreads();
-  const int per = (nw + NT - 1) / NT;
-  const int w0 = min(tid * per, nw), w1 = min(w0 + per, nw);
-  int c = 0;
-  for (int w = w0; w < w1; ++w) c += __popc(bits[w]);
+  int m = 0;
+  for (int w = tid; w < kUnionChunk / 32; w += kUnionNT) {
+    bits[(size_t)c * (kUnionChunk / 32) + w] = wb[w];
+    m += __popc(wb[w]);
+  }
   int total = 0;
-  int base = block_excl_scan<NT>(c, red, &total);
-  for (int w = w0; w < w1; ++w) {
-    off[w] = base;
-    base += __popc(bits[w]);
+  (void)block_excl_scan<kUnionNT>(m, red, &total);
+  if (tid == 0) cnt[c] = total;
+}
+
+__global__ void __launch_bounds__(kUnionNT) k_union_write(const int32_t* __restrict__ sets, int B, int k, int n,
+                                                          const uint32_t* __restrict__ bits,
+                                                          const int32_t* __restrict__ cnt, int nchunks,
+                                                          int32_t* __restrict__ U, int32_t* __restrict__ count,
+                                                          uint32_t* __restrict__ mask) {
+  __shared__ uint32_t wb[kUnionChunk / 32];
+  __shared__ int off[kUnionChunk / 32];
+  __shared__ int red[kUnionNT / 64 + 1];
+  const int c = blockIdx.x, tid = threadIdx.x;
+  const int lo_i = c * kUnionChunk;
+  // offset of this chunk: the counts of the chunks before it, summed in order
+  int part = 0;
+  for (int j = tid; j < c; j += kUnionNT) part += cnt[j];
+  int before = 0;
+  (void)block_excl_scan<kUnionNT>(part, red, &before);
+  constexpr int NW = kUnionChunk / 32;
+  int pc = 0;
+  uint32_t wv = 0u;
+  if (tid < NW) {
+    wv = bits[(size_t)c * NW + tid];
+    pc = __popc(wv);
   }
-  if (tid == 0) *count = total;
+  int mine = 0;
+  const int ex = block_excl_scan<kUnionNT>(pc, red, &mine);
+  if (tid < NW) {
+    wb[tid] = wv;
+    off[tid] = before + ex;
+  }
+  if (c == nchunks - 1 && tid == 0) *count = before + mine;
   __syncthreads();
-  // member i goes to U[rank(i)]: consecutive lanes write consecutive ranks
-  for (int i = tid; i < n; i += NT) {
-    const uint32_t m = bits[i >> 5];
-    if ((m >> (i & 31)) & 1u) U[off[i >> 5] + __popc(m & ((1u << (i & 31)) - 1u))] = i;
+  for (int i = tid; i < kUnionChunk && lo_i + i < n; i += kUnionNT) {
+    const uint32_t m = wb[i >> 5];
+    if ((m >> (i & 31)) & 1u) U[off[i >> 5] + __popc(m & ((1u << (i & 31)) - 1u))] = lo_i + i;
   }
   if (mask != nullptr) {
-    for (int u = tid; u < total; u += NT) mask[u] = 0u;
+    for (int r = tid; r < mine; r += kUnionNT) mask[before + r] = 0u;
     __syncthreads();
-    for (int e0 = 0; e0 < tot; e0 += NT * UL) {
-      int v[UL];
-#pragma unroll
-      for (int u = 0; u < UL; ++u) {
-        const int e = e0 + u * NT + tid;
-        v[u] = e < tot ? sets[e] : -1;
-      }
-#pragma unroll
-      for (int u = 0; u < UL; ++u) {
-        const int e = e0 + u * NT + tid;
-        if (e < tot) {
-          const int i = min(max(v[u], 0), n - 1);
-          const uint32_t m = bits[i >> 5];
-          const int r = off[i >> 5] + __popc(m & ((1u << (i & 31)) - 1u));
-          atomicOr(&mask[r], 1u << (e / k));
+    const int hi_i = min(n, lo_i + kUnionChunk);
+    for (int b = tid % B, rr = tid / B, nr = (kUnionNT - tid % B + B - 1) / B; b < B; b += kUnionNT) {
+      const int32_t* sb = sets + (size_t)b * k;
+      const int e0 = lower_bound_i32(sb, k, lo_i), e1 = lower_bound_i32(sb, k, hi_i);
+      for (int e = e0 + rr; e < e1; e += nr) {
+        const int i = sb[e] - lo_i;
+        if (i >= 0 && i < kUnionChunk) {
+          const uint32_t m = wb[i >> 5];
+          atomicOr(&mask[off[i >> 5] + __popc(m & ((1u << (i & 31)) - 1u))], 1u << b);
         }
       }
     }
   }
 }
 
+int union_chunks(int n) { return (n + kUnionChunk - 1) / kUnionChunk; }
+
 hipError_t launch_union(const int32_t* sets, int B, int k, int n, int32_t* U, int32_t* count, uint32_t* mask,
-                        hipStream_t st) {
-  constexpr int NT = 1024;
-  const int nw = (n + 31) >> 5;
-  const size_t lds = (size_t)nw * 8 + (NT / 64 + 2) * sizeof(int);
-  hipLaunchKernelGGL(k_union<NT>, dim3(1), dim3(NT), lds, st, sets, B, k, n, U, count, mask);
+                        uint32_t* bits, int32_t* chunk_counts, hipStream_t st) {
+  const int nc = union_chunks(n);
+  hipLaunchKernelGGL(k_union_bits, dim3(nc), dim3(kUnionNT), 0, st, sets, B, k, n, bits, chunk_counts);
+  hipLaunchKernelGGL(k_union_write, dim3(nc), dim3(kUnionNT), 0, st, sets, B, k, n, bits, chunk_counts, nc, U, count,
+                     mask);
   return hipGetLastError();
 }
 
