@@ -97,7 +97,8 @@ def kernel_sources_digest(label):
 def counter_traffic(workload, label):
     """HBM bytes per launch of `label` from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
     summary, or None if there is none or the kernel's sources changed since."""
-    p = os.path.join(ROOT, "profiles", f"sparse_block_{workload}_hbm_counters.txt")
+    kind = "sparse_attn_mlp" if workload.endswith("_b32") else "sparse_block"
+    p = os.path.join(ROOT, "profiles", f"{kind}_{workload}_hbm_counters.txt")
     try:
         with open(p) as fh:
             line = next(l for l in fh if l.startswith("json: "))
