@@ -287,8 +287,7 @@ extern "C" dv_status dv_sparse_attn(const dv_attn* a, const float* x, int32_t B,
   q.d = a->d; q.H = a->H; q.dh = a->dh; q.cap = kv->cap; q.pos = kv->pos[0]; q.n_heads = n_heads;
   q.x = x; q.g = nullptr; q.be = nullptr; q.eps = 0.f;
   q.Wq = a->Wq; q.Wk = a->Wk; q.Wv = a->Wv; q.bq = a->bq; q.bk = a->bk; q.bv = a->bv;
-  q.K = kv->K; q.V = kv->V; q.q = o.q; q.heads_in = heads; q.head_scores = nullptr;
-  q.heads_ws = o.heads; q.heads_out = nullptr;
+  q.K = kv->K; q.V = kv->V; q.q = o.q; q.heads_in = heads; q.heads_ws = o.heads;
   DV_LAUNCH("qkv", hs, launch_qkv(a->wtype, kv->ktype, q, hs));
   st = enqueue_attention(a, kv, o, n_heads, scale, hs);
   if (st != DV_OK) return st;
@@ -405,14 +404,22 @@ extern "C" dv_status dv_sparse_block(const dv_attn* a, const dv_mlp* m, const dv
   sa.r0 = pa->r; sa.n0 = a->H; sa.BT0 = pa->BT; sa.hid0 = o.hid_h; sa.s0 = o.s_h;
   sa.r1 = ahead ? pm->r : 0; sa.n1 = ahead ? m->n : 0; sa.BT1 = pm->BT; sa.hid1 = o.hid_m; sa.s1 = o.s_m;
   sa.B = 1;
+  // The head set is selected by workgroup 0 of this launch when a head-predictor row
+  // is at most 128 chunks (two wavefront loads); otherwise by a launch of its own.
+  const bool host_heads = pa->r / chunk_elems(pa->wtype) <= 128;
+  if (host_heads) {
+    sa.sel_k0 = k_heads; sa.sel_set0 = o.heads; sa.sel_set0_out = heads_out;
+  }
   DV_LAUNCH("pred_scores", hs, launch_pred_scores(pa->wtype, sa, hs));
-  // 3. Head selection + gathered QKV + cache append.
+  if (!host_heads)
+    DV_LAUNCH("select_heads", hs,
+              launch_select(o.s_h, 1, a->H, DV_SELECT_TOPK, k_heads, 0.f, o.heads, k_heads, nullptr, heads_out, hs));
+  // 3. Gathered QKV of the selected heads + cache append.
   QkvArgs q{};
   q.d = a->d; q.H = a->H; q.dh = a->dh; q.cap = kv->cap; q.pos = kv->pos[0]; q.n_heads = k_heads;
   q.x = o.xhat; q.g = nullptr; q.be = nullptr; q.eps = 0.f;
   q.Wq = a->Wq; q.Wk = a->Wk; q.Wv = a->Wv; q.bq = a->bq; q.bk = a->bk; q.bv = a->bv;
-  q.K = kv->K; q.V = kv->V; q.q = o.q; q.heads_in = nullptr; q.head_scores = o.s_h;
-  q.heads_ws = o.heads; q.heads_out = heads_out;
+  q.K = kv->K; q.V = kv->V; q.q = o.q; q.heads_in = o.heads; q.heads_ws = nullptr;
   DV_LAUNCH("qkv", hs, launch_qkv(a->wtype, kv->ktype, q, hs));
   // 4. Split-KV attention.
   AttnWs ao{};

@@ -4,8 +4,7 @@
 //
 //   k_qkv   gathered row-dots: for every selected head i, the dh rows of W^Q_i, W^K_i
 //           and W^V_i (contiguous row blocks) against the staged x-hat; q goes to the
-//           workspace, k and v to cache row pos. Optionally selects the head set
-//           itself from the head predictor's scores (ranked in every workgroup).
+//           workspace, k and v to cache row pos.
 //   k_attn  split-KV decode attention: one workgroup per (sequence, selected head,
 //           position chunk) computes the chunk's max logit, sum of exponentials and
 //           unnormalised value sum; the out-projection kernel combines the chunks.
@@ -13,11 +12,10 @@
 
 #include "dv_internal.hpp"
 #include "dv_rowdot.hpp"
-#include "dv_select.hpp"   // wg_topk_small
 
 namespace dv {
 
-template <typename T, typename KT, int NW, int U>
+template <typename T, typename KT, int NW, int U, int KX>
 __global__ void __launch_bounds__(NW * 64) k_qkv(QkvArgs a) {
   extern __shared__ float smem[];
   constexpr int NT = NW * 64;
@@ -25,20 +23,11 @@ __global__ void __launch_bounds__(NW * 64) k_qkv(QkvArgs a) {
   float* xs = smem;
   float* red = smem + a.d;
   int32_t* hset = reinterpret_cast<int32_t*>(red + NW);
-  int* tmp = hset + a.n_heads;                                  // H ints
-  uint32_t* hkeys = reinterpret_cast<uint32_t*>(tmp + a.H);     // H keys
-  if (a.heads_in != nullptr) {
-    for (int i = threadIdx.x; i < a.n_heads; i += NT) hset[i] = min(max(a.heads_in[i], 0), a.H - 1);
-    __syncthreads();
-  } else {
-    wg_topk_small<NT>(a.head_scores, a.H, a.n_heads, hkeys, tmp, hset);
-  }
-  if (wg == 0) {
-    for (int i = threadIdx.x; i < a.n_heads; i += NT) {
-      a.heads_ws[i] = hset[i];
-      if (a.heads_out) a.heads_out[i] = hset[i];
-    }
-  }
+  float* part = reinterpret_cast<float*>(hset + a.n_heads);     // row-dot records
+  for (int i = threadIdx.x; i < a.n_heads; i += NT) hset[i] = min(max(a.heads_in[i], 0), a.H - 1);
+  __syncthreads();
+  if (wg == 0 && a.heads_ws != nullptr)
+    for (int i = threadIdx.x; i < a.n_heads; i += NT) a.heads_ws[i] = hset[i];
   const int per_mat = a.n_heads * a.dh;
   auto row_ptr = [&](int row) {
     const int m = row / per_mat;
@@ -62,24 +51,35 @@ __global__ void __launch_bounds__(NW * 64) k_qkv(QkvArgs a) {
       C[((size_t)head * a.cap + a.pos) * a.dh + t] = (KT)v;
     }
   };
-  rowdot_wave_loop<T, NW, U>(row_ptr, epi, 3 * per_mat, a.d, a.x, a.g, a.be, a.eps, xs, red, nullptr, wg, nwg);
+  rowdot_flat<T, NW, U, true, KX>(row_ptr, epi, 3 * per_mat, a.d, a.x, a.g, a.be, a.eps, xs, red, part, nullptr, wg, nwg);
 }
 
-template <typename T, typename KT>
+template <typename T, typename KT, int KX>
 static hipError_t launch_qkv_t(const QkvArgs& a, hipStream_t st) {
   constexpr int NW = 16, U = 8;
   const int nrows = 3 * a.n_heads * a.dh;
-  // One workgroup per CU; rows dealt round-robin (one wavefront per row).
+  // One workgroup per CU, each a contiguous range of rows (rowdot_flat).
   const int blocks = max(1, min(nrows, device_cu_count()));
-  size_t lds = (size_t)(a.d + NW) * sizeof(float) + (size_t)(a.n_heads + 2 * a.H + 4) * sizeof(int32_t);
-  hipLaunchKernelGGL((k_qkv<T, KT, NW, U>), dim3(blocks), dim3(NW * 64), lds, st, a);
+  size_t lds = (size_t)(a.d + NW) * sizeof(float) + (size_t)a.n_heads * sizeof(int32_t) +
+               (size_t)rowdot_flat_part(nrows, blocks, NW) * sizeof(float) + 16;
+  hipLaunchKernelGGL((k_qkv<T, KT, NW, U, KX>), dim3(blocks), dim3(NW * 64), lds, st, a);
   return hipGetLastError();
+}
+
+template <typename T, typename KT>
+static hipError_t launch_qkv_k(const QkvArgs& a, hipStream_t st) {
+  switch (rowdot_kx(a.d, 16)) {
+    case 1: return launch_qkv_t<T, KT, 1>(a, st);
+    case 2: return launch_qkv_t<T, KT, 2>(a, st);
+    case 3: return launch_qkv_t<T, KT, 3>(a, st);
+    default: return launch_qkv_t<T, KT, 4>(a, st);
+  }
 }
 
 hipError_t launch_qkv(int wtype, int kvtype, const QkvArgs& a, hipStream_t st) {
   if (wtype == DV_F16)
-    return kvtype == DV_F16 ? launch_qkv_t<_Float16, _Float16>(a, st) : launch_qkv_t<_Float16, float>(a, st);
-  return kvtype == DV_F16 ? launch_qkv_t<float, _Float16>(a, st) : launch_qkv_t<float, float>(a, st);
+    return kvtype == DV_F16 ? launch_qkv_k<_Float16, _Float16>(a, st) : launch_qkv_k<_Float16, float>(a, st);
+  return kvtype == DV_F16 ? launch_qkv_k<float, _Float16>(a, st) : launch_qkv_k<float, float>(a, st);
 }
 
 // ------------------------------------------------------------ attention

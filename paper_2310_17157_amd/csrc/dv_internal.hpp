@@ -146,156 +146,73 @@ __device__ __forceinline__ int block_excl_scan(int v, int* red, int* total) {
   return base + inc - v;
 }
 
-// Stage x[0..d) (fp32, 16-byte aligned, d % 4 == 0) into LDS in the layout of
-// xs_index<T>, optionally applying layer norm with gamma g (NULL: no LN) and beta b
-// (NULL: 0). Biased variance, two passes over LDS. Ends with a barrier.
+// Stage x[0..d) (fp32, 16-byte aligned, d % 4 == 0, d <= 16384) into LDS in the layout
+// of xs_index<T>, optionally applying layer norm with gamma g (NULL: no LN) and beta b
+// (NULL: 0). load() only issues the global reads of x, g and b into registers, so that a
+// caller can issue its own (HBM) loads behind them and still wait for these alone;
+// finish() takes mean and biased variance as two workgroup reductions over the
+// registers (two-pass, no cancellation), writes LDS and ends with a barrier.
+// K float4 per thread covers d <= 4 * NT * K.
+template <typename T, int NT, int K = (16384 / 4 + NT - 1) / NT>
+struct StageX {
+  f32x4 v[K], gv[K], bv[K];
+  __device__ __forceinline__ void load(const float* __restrict__ x, int d, const float* __restrict__ g,
+                                       const float* __restrict__ b) {
+    const int n4 = d >> 2;
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const int i = threadIdx.x + k * NT;
+      v[k] = i < n4 ? *reinterpret_cast<const f32x4*>(x + 4 * i) : z;
+      gv[k] = (g != nullptr && i < n4) ? *reinterpret_cast<const f32x4*>(g + 4 * i) : z;
+      bv[k] = (b != nullptr && i < n4) ? *reinterpret_cast<const f32x4*>(b + 4 * i) : z;
+    }
+  }
+  __device__ __forceinline__ void finish(int d, bool ln, float eps, float* xs, float* red) {
+    const int n4 = d >> 2;
+    if (!ln) {
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        const int i = threadIdx.x + k * NT;
+        if (i < n4) *reinterpret_cast<f32x4*>(xs + xs_index<T>(4 * i, d)) = v[k];
+      }
+      __syncthreads();
+      return;
+    }
+    float s = 0.f;
+#pragma unroll
+    for (int k = 0; k < K; ++k) s += (v[k][0] + v[k][1]) + (v[k][2] + v[k][3]);
+    const float mean = block_sum<NT>(s, red) / (float)d;
+    float q = 0.f;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      if (threadIdx.x + k * NT < n4) {
+        const float a0 = v[k][0] - mean, a1 = v[k][1] - mean, a2 = v[k][2] - mean, a3 = v[k][3] - mean;
+        q += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
+      }
+    }
+    const float rstd = 1.0f / sqrtf(block_sum<NT>(q, red) / (float)d + eps);
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const int i = threadIdx.x + k * NT;
+      if (i < n4) {
+        f32x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = (v[k][e] - mean) * rstd * gv[k][e] + bv[k][e];
+        *reinterpret_cast<f32x4*>(xs + xs_index<T>(4 * i, d)) = o;
+      }
+    }
+    __syncthreads();
+  }
+};
+
 template <typename T, int NT>
 __device__ void stage_x(const float* __restrict__ x, int d, const float* __restrict__ g,
                         const float* __restrict__ b, float eps, float* xs, float* red) {
-  const int n4 = d >> 2;
-  float s = 0.f;
-  for (int i = threadIdx.x; i < n4; i += NT) {
-    f32x4 v = *reinterpret_cast<const f32x4*>(x + 4 * i);
-    *reinterpret_cast<f32x4*>(xs + xs_index<T>(4 * i, d)) = v;
-    s += (v[0] + v[1]) + (v[2] + v[3]);
-  }
-  if (g == nullptr) {
-    __syncthreads();
-    return;
-  }
-  const float mean = block_sum<NT>(s, red) / (float)d;
-  float q = 0.f;
-  for (int i = threadIdx.x; i < n4; i += NT) {
-    f32x4 v = *reinterpret_cast<const f32x4*>(xs + xs_index<T>(4 * i, d));
-    float a0 = v[0] - mean, a1 = v[1] - mean, a2 = v[2] - mean, a3 = v[3] - mean;
-    q += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
-  }
-  const float var = block_sum<NT>(q, red) / (float)d;
-  const float rstd = 1.0f / sqrtf(var + eps);
-  for (int i = threadIdx.x; i < n4; i += NT) {
-    float* p = xs + xs_index<T>(4 * i, d);
-    f32x4 v = *reinterpret_cast<const f32x4*>(p);
-    f32x4 gg = *reinterpret_cast<const f32x4*>(g + 4 * i);
-    f32x4 bb = {0.f, 0.f, 0.f, 0.f};
-    if (b != nullptr) bb = *reinterpret_cast<const f32x4*>(b + 4 * i);
-    f32x4 o;
-    o[0] = (v[0] - mean) * rstd * gg[0] + bb[0];
-    o[1] = (v[1] - mean) * rstd * gg[1] + bb[1];
-    o[2] = (v[2] - mean) * rstd * gg[2] + bb[2];
-    o[3] = (v[3] - mean) * rstd * gg[3] + bb[3];
-    *reinterpret_cast<f32x4*>(p) = o;
-  }
-  __syncthreads();
+  StageX<T, NT> st;
+  st.load(x, d, g, b);
+  st.finish(d, g != nullptr, eps, xs, red);
 }
-
-// Dot product of one row (d elements of T, 16-byte aligned) with the staged x-hat,
-// computed by one wavefront over the chunks c = lane + 64*(seg + S*j). Returns the
-// wavefront total (in every lane) of this segment. U chunks per lane are in flight.
-template <typename T, int U, int S>
-__device__ __forceinline__ float wave_rowdot(const T* __restrict__ row, const float* xs, int d,
-                                             int lane, int seg) {
-  constexpr int E = Chunk<T>::E;
-  const int nch = d / E;
-  const char* base = reinterpret_cast<const char*>(row);
-  float acc0 = 0.f, acc1 = 0.f;
-  int c = lane + 64 * seg;
-  constexpr int step = 64 * S;
-  for (; c + step * (U - 1) < nch; c += step * U) {
-    u32x4 w[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) w[u] = ld_stream(base + (size_t)(c + step * u) * 16);
-#pragma unroll
-    for (int u = 0; u < U; u += 2) {
-      acc0 = dot_chunk<T>(w[u], xs, d, c + step * u, acc0);
-      if (u + 1 < U) acc1 = dot_chunk<T>(w[u + 1], xs, d, c + step * (u + 1), acc1);
-    }
-  }
-  for (; c < nch; c += step) {
-    u32x4 w = ld_stream(base + (size_t)c * 16);
-    acc0 = dot_chunk<T>(w, xs, d, c, acc0);
-  }
-  return wave_sum(acc0 + acc1);
-}
-
-// The first U chunks a wavefront will need for a row (same chunk order as
-// wave_rowdot), loaded early so that HBM latency overlaps a workgroup prologue.
-template <typename T, int U, int S>
-__device__ __forceinline__ void row_prefetch(const T* __restrict__ row, int d, int lane, int seg,
-                                             u32x4 (&w)[U]) {
-  constexpr int E = Chunk<T>::E;
-  const int nch = d / E;
-  const char* base = reinterpret_cast<const char*>(row);
-  const int c0 = lane + 64 * seg;
-#pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int c = c0 + 64 * S * u;
-    w[u] = c < nch ? ld_stream(base + (size_t)c * 16) : u32x4{0u, 0u, 0u, 0u};
-  }
-}
-
-// wave_rowdot whose first U chunks were loaded by row_prefetch.
-template <typename T, int U, int S>
-__device__ __forceinline__ float wave_rowdot_pf(const T* __restrict__ row, const float* xs, int d, int lane,
-                                                int seg, const u32x4 (&w0)[U]) {
-  constexpr int E = Chunk<T>::E;
-  constexpr int step = 64 * S;
-  const int nch = d / E;
-  const char* base = reinterpret_cast<const char*>(row);
-  const int c0 = lane + 64 * seg;
-  float acc0 = 0.f, acc1 = 0.f;
-#pragma unroll
-  for (int u = 0; u < U; u += 2) {
-    if (c0 + step * u < nch) acc0 = dot_chunk<T>(w0[u], xs, d, c0 + step * u, acc0);
-    if (u + 1 < U && c0 + step * (u + 1) < nch) acc1 = dot_chunk<T>(w0[u + 1], xs, d, c0 + step * (u + 1), acc1);
-  }
-  int c = c0 + step * U;
-  for (; c + step * (U - 1) < nch; c += step * U) {
-    u32x4 w[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) w[u] = ld_stream(base + (size_t)(c + step * u) * 16);
-#pragma unroll
-    for (int u = 0; u < U; u += 2) {
-      acc0 = dot_chunk<T>(w[u], xs, d, c + step * u, acc0);
-      if (u + 1 < U) acc1 = dot_chunk<T>(w[u + 1], xs, d, c + step * (u + 1), acc1);
-    }
-  }
-  for (; c < nch; c += step) {
-    u32x4 w = ld_stream(base + (size_t)c * 16);
-    acc0 = dot_chunk<T>(w, xs, d, c, acc0);
-  }
-  return wave_sum(acc0 + acc1);
-}
-
-// A whole workgroup streams one row: wavefront w of NW takes the chunks
-// c = lane + 64*(w + NW*j), j < JMAX (every chunk of a row of up to 64*NW*JMAX
-// chunks). load() issues the loads; dot() consumes them against the staged x-hat and
-// returns this wavefront's partial sum (in every lane).
-template <typename T, int NW, int JMAX>
-struct WgRow {
-  u32x4 w[JMAX];
-  __device__ __forceinline__ void load(const T* __restrict__ row, int nch, int lane, int wave) {
-    const char* base = reinterpret_cast<const char*>(row);
-#pragma unroll
-    for (int j = 0; j < JMAX; ++j) {
-      const int c = lane + 64 * (wave + NW * j);
-      w[j] = c < nch ? ld_stream(base + (size_t)c * 16) : u32x4{0u, 0u, 0u, 0u};
-    }
-  }
-  __device__ __forceinline__ float dot(const float* xs, int d, int nch, int lane, int wave) const {
-    float acc0 = 0.f, acc1 = 0.f;
-#pragma unroll
-    for (int j = 0; j < JMAX; ++j) {
-      const int c = lane + 64 * (wave + NW * j);
-      if (c < nch) {
-        if (j & 1)
-          acc1 = dot_chunk<T>(w[j], xs, d, c, acc1);
-        else
-          acc0 = dot_chunk<T>(w[j], xs, d, c, acc0);
-      }
-    }
-    return wave_sum(acc0 + acc1);
-  }
-};
 
 // Order-preserving key of a float: a > b  <=>  key(a) > key(b); -0 maps to +0.
 __device__ __forceinline__ uint32_t fkey(float f) {
@@ -363,10 +280,14 @@ struct PredScoreArgs {
   int r0, n0; const void* BT0; const float* hid0; float* s0;   // hid0 [B][r0], s0 [B][n0]
   int r1, n1; const void* BT1; const float* hid1; float* s1;   // n1 = 0: none
   int B;
+  // sel_k0 > 0 (B = 1, n0 <= workgroup size): one extra workgroup computes all n0
+  // scores of the first predictor and writes their top-sel_k0 set, ascending, to
+  // sel_set0 (and sel_set0_out if not NULL).
+  int sel_k0; int32_t* sel_set0; int32_t* sel_set0_out;
 };
 hipError_t launch_pred_scores(int wtype, const PredScoreArgs& a, hipStream_t st);
 
-// Gathered row-dot for Q/K/V of the selected heads (B = 1) plus optional fused work.
+// Gathered row-dot for Q/K/V of the selected heads (B = 1).
 struct QkvArgs {
   int d, H, dh, cap, pos, n_heads;
   const float* x; const float* g; const float* be; float eps;    // LN1 (g NULL: none)
@@ -374,10 +295,8 @@ struct QkvArgs {
   const float* bq; const float* bk; const float* bv;
   void* K; void* V;                 // [H][cap][dh] of this sequence
   float* q;                         // [n_heads][dh] out
-  const int32_t* heads_in;          // given head set, or NULL when selecting from scores
-  const float* head_scores;         // [H] (when heads_in == NULL)
-  int32_t* heads_ws;                // [n_heads] out: the set used (written by one workgroup)
-  int32_t* heads_out;               // optional caller copy
+  const int32_t* heads_in;          // [n_heads] the head set
+  int32_t* heads_ws;                // optional [n_heads] out: the set, clamped (one workgroup)
 };
 hipError_t launch_qkv(int wtype, int kvtype, const QkvArgs& a, hipStream_t st);
 

@@ -1,20 +1,21 @@
 // First half of the sparsified MLP of Eq. (1): for each selected neuron i,
 // z_i = x-hat . W^1_i + b1_i and a_i = ReLU(z_i). W^1_i is row i of W1T, so each
 // selected neuron is one contiguous row streamed once (Section 4.4 "Kernel fusion":
-// the gather is the load itself; nothing is copied). One workgroup per CU; rows are
-// dealt round-robin over the workgroups (one wavefront per row), so the ~10 rows per
-// CU at the OPT-175B shape are balanced to within one. The second half (the
-// a_i-weighted sum of rows of W2T) is the gathered row-axpy kernel.
+// the gather is the load itself; nothing is copied). One workgroup per CU takes a
+// contiguous range of the selected rows and its wavefronts split the range's loads
+// evenly (rowdot_flat), so every wavefront of the machine has the same work. The
+// second half (the a_i-weighted sum of rows of W2T) is the gathered row-axpy kernel.
 #include "dv_internal.hpp"
 #include "dv_rowdot.hpp"
 
 namespace dv {
 
-template <typename T, int NW, int U>
+template <typename T, int NW, int U, int KX>
 __global__ void __launch_bounds__(NW * 64) k_fc1(Fc1Args a) {
   extern __shared__ float smem[];
   float* xs = smem;
   float* red = smem + a.d;
+  float* part = red + NW;
   auto row_ptr = [&](int s) {
     return static_cast<const T*>(a.W1T) + (size_t)min(max(a.set[s], 0), a.n - 1) * a.d;
   };
@@ -23,19 +24,32 @@ __global__ void __launch_bounds__(NW * 64) k_fc1(Fc1Args a) {
     if (a.b1) v += a.b1[i];
     a.h[s] = v > 0.f ? v : 0.f;
   };
-  rowdot_wave_loop<T, NW, U>(row_ptr, epi, a.k, a.d, a.x, a.g, a.be, a.eps, xs, red, nullptr, blockIdx.x,
-                             gridDim.x);
+  rowdot_flat<T, NW, U, false, KX>(row_ptr, epi, a.k, a.d, a.x, a.g, a.be, a.eps, xs, red, part, nullptr, blockIdx.x,
+                        gridDim.x);
+}
+
+template <typename T, int KX>
+static hipError_t launch_fc1_t(const Fc1Args& a, hipStream_t st) {
+  // 16 loads per lane in flight, fewer with wider inputs (register budget)
+  constexpr int NW = 16, U = KX >= 4 ? 8 : (KX == 3 ? 12 : 16);
+  const int blocks = max(1, min(a.k, device_cu_count()));
+  const size_t lds = (size_t)(a.d + NW + rowdot_flat_part(a.k, blocks, NW)) * sizeof(float);
+  hipLaunchKernelGGL((k_fc1<T, NW, U, KX>), dim3(blocks), dim3(NW * 64), lds, st, a);
+  return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t launch_fc1_k(const Fc1Args& a, hipStream_t st) {
+  switch (rowdot_kx(a.d, 16)) {
+    case 1: return launch_fc1_t<T, 1>(a, st);
+    case 2: return launch_fc1_t<T, 2>(a, st);
+    case 3: return launch_fc1_t<T, 3>(a, st);
+    default: return launch_fc1_t<T, 4>(a, st);
+  }
 }
 
 hipError_t launch_fc1(int wtype, const Fc1Args& a, hipStream_t st) {
-  constexpr int NW = 16, U = 8;
-  const int blocks = max(1, min(a.k, device_cu_count()));
-  const size_t lds = (size_t)(a.d + NW) * sizeof(float);
-  if (wtype == DV_F16)
-    hipLaunchKernelGGL((k_fc1<_Float16, NW, U>), dim3(blocks), dim3(NW * 64), lds, st, a);
-  else
-    hipLaunchKernelGGL((k_fc1<float, NW, U>), dim3(blocks), dim3(NW * 64), lds, st, a);
-  return hipGetLastError();
+  return wtype == DV_F16 ? launch_fc1_k<_Float16>(a, st) : launch_fc1_k<float>(a, st);
 }
 
 }  // namespace dv

@@ -8,13 +8,14 @@
 namespace dv {
 
 // ----------------------------------------------------------- hidden layer
-// h[b][j] = x-hat[b] . AT[j] for the rows of up to two predictors; one wavefront per
-// row, rows dealt round-robin over one workgroup per CU.
-template <typename T, int NW, int U>
+// h[b][j] = x-hat[b] . AT[j] for the rows of up to two predictors; one workgroup per
+// CU takes a contiguous range of rows whose loads its wavefronts split evenly.
+template <typename T, int NW, int U, int KX>
 __global__ void __launch_bounds__(NW * 64) k_pred_hidden(PredHidArgs a) {
   extern __shared__ float smem[];
   float* xs = smem;
   float* red = smem + a.d;
+  float* part = red + NW;
   const int b = blockIdx.y;
   auto row_ptr = [&](int row) {
     return row < a.r0 ? static_cast<const T*>(a.AT0) + (size_t)row * a.d
@@ -26,24 +27,93 @@ __global__ void __launch_bounds__(NW * 64) k_pred_hidden(PredHidArgs a) {
     else
       a.hid1[(size_t)b * a.r1 + row - a.r0] = v;
   };
-  rowdot_wave_loop<T, NW, U>(row_ptr, epi, a.r0 + a.r1, a.d, a.x + (size_t)b * a.d, a.g, a.be, a.eps, xs, red,
-                             a.xhat_out ? a.xhat_out + (size_t)b * a.d : nullptr, blockIdx.x, gridDim.x);
+  rowdot_flat<T, NW, U, false, KX>(row_ptr, epi, a.r0 + a.r1, a.d, a.x + (size_t)b * a.d, a.g, a.be, a.eps, xs, red, part,
+                        a.xhat_out ? a.xhat_out + (size_t)b * a.d : nullptr, blockIdx.x, gridDim.x);
+}
+
+template <typename T, int KX>
+static hipError_t launch_pred_hidden_t(const PredHidArgs& a, hipStream_t st) {
+  // 16 loads per lane in flight, fewer with wider inputs (register budget)
+  constexpr int NW = 16, U = KX >= 4 ? 8 : (KX == 3 ? 12 : 16);
+  const int nrows = a.r0 + a.r1;
+  const dim3 grid(max(1, min(nrows, device_cu_count())), a.B);
+  const size_t lds = (size_t)(a.d + NW + rowdot_flat_part(nrows, grid.x, NW)) * sizeof(float);
+  hipLaunchKernelGGL((k_pred_hidden<T, NW, U, KX>), grid, dim3(NW * 64), lds, st, a);
+  return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t launch_pred_hidden_k(const PredHidArgs& a, hipStream_t st) {
+  switch (rowdot_kx(a.d, 16)) {
+    case 1: return launch_pred_hidden_t<T, 1>(a, st);
+    case 2: return launch_pred_hidden_t<T, 2>(a, st);
+    case 3: return launch_pred_hidden_t<T, 3>(a, st);
+    default: return launch_pred_hidden_t<T, 4>(a, st);
+  }
 }
 
 hipError_t launch_pred_hidden(int wtype, const PredHidArgs& a, hipStream_t st) {
-  constexpr int NW = 16, U = 8;
-  const int nrows = a.r0 + a.r1;
-  const dim3 grid(max(1, min(nrows, device_cu_count())), a.B);
-  const size_t lds = (size_t)(a.d + NW) * sizeof(float);
-  if (wtype == DV_F16)
-    hipLaunchKernelGGL((k_pred_hidden<_Float16, NW, U>), grid, dim3(NW * 64), lds, st, a);
-  else
-    hipLaunchKernelGGL((k_pred_hidden<float, NW, U>), grid, dim3(NW * 64), lds, st, a);
-  return hipGetLastError();
+  return wtype == DV_F16 ? launch_pred_hidden_k<_Float16>(a, st) : launch_pred_hidden_k<float>(a, st);
 }
 
 // ----------------------------------------------------------------- scores
 // G lanes per row (a row is r elements, short); RU rows per lane group in flight.
+// With a.sel_k0 > 0 workgroup 0 takes all rows of the first predictor (the head
+// predictor, n0 <= NT) and selects its top-k set right away, so that the next kernel
+// finds the head set ready; the other workgroups take the remaining rows.
+// Head workgroup of a hosted selection: the n0 rows of the first predictor, RB rows
+// per wavefront per round with every load of a round in flight before the input is
+// staged (one round trip at H <= RB * NW; the workgroup runs beside a kernel that
+// saturates HBM, where each round trip is slow), then the top-k set.
+template <typename T, int NW, int RB>
+__device__ __forceinline__ void head_scores_select(const PredScoreArgs& a, float* xs0, float* hsc) {
+  constexpr int NT = NW * 64;
+  constexpr int E = Chunk<T>::E;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int nch = a.r0 / E;                      // r0 <= 1536 for a hosted selection
+  const char* base = static_cast<const char*>(a.BT0);
+  const size_t rowb = (size_t)a.r0 * sizeof(T);
+  bool staged = false;
+  for (int r0 = wave; r0 - wave < a.n0; r0 += NW * RB) {
+    u32x4 w[RB][2];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int row = min(r0 + rb * NW, a.n0 - 1);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) w[rb][h] = ld_stream(base + row * rowb + (size_t)min(h * 64 + lane, nch - 1) * 16);
+    }
+    if (!staged) {
+      stage_x<T, NT>(a.hid0, a.r0, nullptr, nullptr, 0.f, xs0, nullptr);
+      staged = true;
+    }
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int row = r0 + rb * NW;
+      float acc = 0.f;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int c = h * 64 + lane;
+        if (c < nch) acc = dot_chunk<T>(w[rb][h], xs0, a.r0, c, acc);
+      }
+      acc = wave_sum(acc);
+      if (lane == 0 && row < a.n0) {
+        hsc[row] = acc;
+        a.s0[row] = acc;
+      }
+    }
+  }
+  if (!staged) stage_x<T, NT>(a.hid0, a.r0, nullptr, nullptr, 0.f, xs0, nullptr);   // (no rows: keep barriers)
+  uint32_t* keys = reinterpret_cast<uint32_t*>(hsc + a.n0);
+  int* tmp = reinterpret_cast<int*>(keys + a.n0);
+  int32_t* set = tmp + a.n0;
+  __syncthreads();
+  wg_topk_small<NT>(hsc, a.n0, a.sel_k0, keys, tmp, set);
+  for (int i = threadIdx.x; i < a.sel_k0; i += NT) {
+    a.sel_set0[i] = set[i];
+    if (a.sel_set0_out) a.sel_set0_out[i] = set[i];
+  }
+}
+
 template <typename T, int NW, int G, int RU>
 __global__ void __launch_bounds__(NW * 64) k_pred_scores(PredScoreArgs a) {
   extern __shared__ float smem[];
@@ -53,6 +123,11 @@ __global__ void __launch_bounds__(NW * 64) k_pred_scores(PredScoreArgs a) {
   const int r0a = (a.r0 + 3) & ~3;
   float* xs0 = smem;
   float* xs1 = smem + r0a;
+  const bool hosted = a.sel_k0 > 0;
+  if (hosted && blockIdx.x == 0) {
+    head_scores_select<T, NW, 6>(a, xs0, xs1 + ((a.r1 + 3) & ~3));
+    return;
+  }
   stage_x<T, NT>(a.hid0 + (size_t)b * a.r0, a.r0, nullptr, nullptr, 0.f, xs0, nullptr);
   if (a.n1 > 0) stage_x<T, NT>(a.hid1 + (size_t)b * a.r1, a.r1, nullptr, nullptr, 0.f, xs1, nullptr);
   const int nrows = a.n0 + a.n1;
@@ -60,7 +135,11 @@ __global__ void __launch_bounds__(NW * 64) k_pred_scores(PredScoreArgs a) {
   const int grp = lane / G, gl = lane % G;
   constexpr int GPW = 64 / G;          // row groups per wavefront
   constexpr int RPW = GPW * RU;        // rows per wavefront iteration
-  for (int base = (blockIdx.x * NW + wave) * RPW; base < nrows; base += gridDim.x * NW * RPW) {
+  const int row_end = nrows;
+  const int bx = (int)blockIdx.x - (hosted ? 1 : 0);
+  const int first = (hosted ? a.n0 : 0) + (bx * NW + wave) * RPW;
+  const int stride = ((int)gridDim.x - (hosted ? 1 : 0)) * NW * RPW;
+  for (int base = first; base < row_end; base += stride) {
     const char* rp[RU];
     const float* xsu[RU];
     int ru[RU], nch[RU];
@@ -70,7 +149,9 @@ __global__ void __launch_bounds__(NW * 64) k_pred_scores(PredScoreArgs a) {
     for (int u = 0; u < RU; ++u) {
       const int row = base + u * GPW + grp;
       acc[u] = 0.f;
-      if (row < a.n0) {
+      if (row >= row_end) {
+        rp[u] = nullptr; xsu[u] = xs0; ru[u] = a.r0; nch[u] = 0;
+      } else if (row < a.n0) {
         rp[u] = reinterpret_cast<const char*>(static_cast<const T*>(a.BT0) + (size_t)row * a.r0);
         xsu[u] = xs0; ru[u] = a.r0; nch[u] = a.r0 / E;
       } else if (row < nrows) {
@@ -95,7 +176,7 @@ __global__ void __launch_bounds__(NW * 64) k_pred_scores(PredScoreArgs a) {
 #pragma unroll
       for (int o = G / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
       const int row = base + u * GPW + grp;
-      if (gl == 0 && row < nrows) {
+      if (gl == 0 && row < row_end) {
         if (row < a.n0)
           a.s0[(size_t)b * a.n0 + row] = v;
         else
@@ -111,18 +192,19 @@ static hipError_t launch_scores_t(const PredScoreArgs& a, hipStream_t st) {
   constexpr int E = Chunk<T>::E;
   const int nch = max(a.r0, a.r1) / E;
   const int nrows = a.n0 + a.n1;
-  const size_t lds = (size_t)(((a.r0 + 3) & ~3) + a.r1 + 4) * sizeof(float);
+  const int hosted = a.sel_k0 > 0 ? 1 : 0;
+  const size_t lds = (size_t)(((a.r0 + 3) & ~3) + ((a.r1 + 3) & ~3) + 4 * a.n0 * hosted + 4) * sizeof(float);
   if (nch > 32) {
     constexpr int G = 64, RU = 8, RPB = NW * (64 / G) * RU;
-    dim3 grid(min((nrows + RPB - 1) / RPB, 4096), a.B);
+    dim3 grid(min((nrows + RPB - 1) / RPB, 4096) + hosted, a.B);
     hipLaunchKernelGGL((k_pred_scores<T, NW, G, RU>), grid, dim3(NW * 64), lds, st, a);
   } else if (nch > 16) {
     constexpr int G = 32, RU = 4, RPB = NW * (64 / G) * RU;
-    dim3 grid(min((nrows + RPB - 1) / RPB, 4096), a.B);
+    dim3 grid(min((nrows + RPB - 1) / RPB, 4096) + hosted, a.B);
     hipLaunchKernelGGL((k_pred_scores<T, NW, G, RU>), grid, dim3(NW * 64), lds, st, a);
   } else {
     constexpr int G = 16, RU = 4, RPB = NW * (64 / G) * RU;
-    dim3 grid(min((nrows + RPB - 1) / RPB, 4096), a.B);
+    dim3 grid(min((nrows + RPB - 1) / RPB, 4096) + hosted, a.B);
     hipLaunchKernelGGL((k_pred_scores<T, NW, G, RU>), grid, dim3(NW * 64), lds, st, a);
   }
   return hipGetLastError();

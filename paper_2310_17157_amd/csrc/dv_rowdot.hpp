@@ -1,84 +1,140 @@
 // Row-dot loops shared by the predictor's first layer, fc1 and the gathered QKV:
 // every selected row (d weights, 16-byte chunks) is dotted with an input vector
 // staged once per workgroup in LDS (optionally layer-normalised there).
-//
-// rowdot_wg_loop: a persistent grid strides over the rows; for each row the NW
-// wavefronts of a workgroup split its 16-byte chunks (WgRow), the next row's loads
-// are issued before the current row is reduced, and the first row's loads are issued
-// before the layer-norm prologue so that HBM latency overlaps it. One barrier per
-// row; the per-wavefront partial sums use two alternating LDS slots.
 #pragma once
 
 #include "dv_internal.hpp"
 
 namespace dv {
 
-// xs: d floats of LDS; red: NW + 2*NW floats of LDS. row_ptr(row) -> const T*;
-// epi(row, value) runs on thread 0. xhat_out (optional) receives the normalised
-// input from workgroup 0.
-template <typename T, int NW, int JMAX, class RowPtr, class Epi>
-__device__ __forceinline__ void rowdot_wg_loop(RowPtr row_ptr, Epi epi, int nrows, int d, const float* x,
-                                               const float* g, const float* be, float eps, float* xs,
-                                               float* red, float* xhat_out) {
+// rowdot_flat: workgroup wg of G takes the contiguous rows [wg*R/G, (wg+1)*R/G), and
+// its NW wavefronts split that range's load slots evenly across row boundaries (a
+// slot is one wavefront load of 64 lanes x 16 bytes; a row of nch chunks is
+// ipr = ceil(nch / 64) slots). Every wavefront thus has the same number of loads
+// whatever the row count, all of them issued early: the first U right behind the
+// prologue's input reads and, with PIPE, each next U before the current U are consumed (from two alternating
+// register sets, so that no wait is ever needed just to move data; surplus loads past
+// the end are clamped to the last slot and discarded). A wavefront reduces its partial sum of a
+// row when it leaves the row and records it in LDS (part[wave * mr + k] for its k-th
+// row, mr = ceil(R/G) + 1); after a barrier one thread per row adds the records of the
+// wavefronts that covered it, in wavefront order (bitwise reproducible), and calls
+// epi(row, value). xhat_out (optional) receives the staged input from workgroup 0.
+// KX: float4 of the input per thread (d <= 4 * 64 * NW * KX).
+template <typename T, int NW, int U, bool PIPE, int KX, class RowPtr, class Epi>
+__device__ __forceinline__ void rowdot_flat(RowPtr row_ptr, Epi epi, int nrows, int d, const float* x,
+                                            const float* g, const float* be, float eps, float* xs, float* red,
+                                            float* part, float* xhat_out, int wg, int G) {
   constexpr int NT = NW * 64;
   constexpr int E = Chunk<T>::E;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int nch = d / E;
-  int row = blockIdx.x;
-  WgRow<T, NW, JMAX> cur, nxt;
-  if (row < nrows) cur.load(row_ptr(row), nch, lane, wave);
-  stage_x<T, NT>(x, d, g, be, eps, xs, red);
-  if (xhat_out != nullptr && blockIdx.x == 0)
-    for (int e = threadIdx.x; e < d; e += NT) xhat_out[e] = xs[xs_index<T>(e, d)];
-  float* slots = red + NW;
-  int it = 0;
-  for (; row < nrows; row += gridDim.x, ++it) {
-    const int next = row + gridDim.x;
-    if (next < nrows) nxt.load(row_ptr(next), nch, lane, wave);
-    const float p = cur.dot(xs, d, nch, lane, wave);
-    float* slot = slots + (it & 1) * NW;
-    if (lane == 0) slot[wave] = p;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      float v = 0.f;
-#pragma unroll
-      for (int w = 0; w < NW; ++w) v += slot[w];
-      epi(row, v);
-    }
-    cur = nxt;
-  }
-}
+  const int r0 = (int)((long)wg * nrows / G), r1 = (int)((long)(wg + 1) * nrows / G);
+  const int nch = d / E, ipr = (nch + 63) >> 6;
+  const int slots = (r1 - r0) * ipr;
+  const int tw = (slots + NW - 1) / NW;
+  const int s0 = min(wave * tw, slots), s1 = min(s0 + tw, slots);
+  const int mr = (nrows + G - 1) / G + 1;
+  const bool active = s0 < s1;
 
-// Wavefront-per-row variant: G workgroups (this is number wg) of NW wavefronts; row r
-// goes to workgroup r % G, wavefront (r / G) % NW, so consecutive rows land on different CUs
-// and any row count spreads over the machine to within one row per CU. Each
-// wavefront streams a whole row with U chunks per lane in flight; its first row's
-// loads are issued before the prologue. epi(row, value) runs on lane 0.
-template <typename T, int NW, int U, class RowPtr, class Epi>
-__device__ __forceinline__ void rowdot_wave_loop(RowPtr row_ptr, Epi epi, int nrows, int d, const float* x,
-                                                 const float* g, const float* be, float eps, float* xs,
-                                                 float* red, float* xhat_out, int wg, int G) {
-  constexpr int NT = NW * 64;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  int row = wg + G * wave;
-  u32x4 pf[U];
-  if (row < nrows) row_prefetch<T, U, 1>(row_ptr(row), d, lane, 0, pf);
-  stage_x<T, NT>(x, d, g, be, eps, xs, red);
+  // The row pointer (a list lookup for gathered rows) is formed only when the load
+  // stream enters a new row, not per load.
+  int lrow = -1;
+  const char* lptr = nullptr;
+  auto load = [&](u32x4 (&w)[U], int sb) {
+    const int sc0 = min(sb, s1 - 1);
+    int rr = sc0 / ipr, j = sc0 - rr * ipr;
+    if (rr != lrow) {
+      lrow = rr;
+      lptr = reinterpret_cast<const char*>(row_ptr(r0 + rr));
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (u > 0 && sb + u < s1) {
+        if (++j == ipr) {
+          j = 0;
+          ++rr;
+          lrow = rr;
+          lptr = reinterpret_cast<const char*>(row_ptr(r0 + rr));
+        }
+      }
+      const int c = min(j * 64 + lane, nch - 1);
+      w[u] = ld_stream(lptr + (size_t)c * 16);
+    }
+  };
+  int cur = active ? s0 / ipr : 0;        // relative row being accumulated
+  const int first = cur;
+  float acc0 = 0.f, acc1 = 0.f;
+  auto flush = [&]() {
+    const float v = wave_sum(acc0 + acc1);
+    if (lane == 0) part[wave * mr + (cur - first)] = v;
+    acc0 = 0.f;
+    acc1 = 0.f;
+  };
+  auto consume = [&](const u32x4 (&w)[U], int sb) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int s = sb + u;
+      if (s >= s1) break;
+      const int rr = s / ipr;
+      if (rr != cur) {
+        flush();
+        cur = rr;
+      }
+      const int c = (s - rr * ipr) * 64 + lane;
+      if (c < nch) {
+        if (u & 1)
+          acc1 = dot_chunk<T>(w[u], xs, d, c, acc1);
+        else
+          acc0 = dot_chunk<T>(w[u], xs, d, c, acc0);
+      }
+    }
+  };
+
+  // input reads first, weight reads behind them: the prologue waits for the input only
+  StageX<T, NT, KX> st;
+  st.load(x, d, g, be);
+  u32x4 wa[U];
+  if (active) load(wa, s0);
+  st.finish(d, g != nullptr, eps, xs, red);
   if (xhat_out != nullptr && wg == 0)
     for (int e = threadIdx.x; e < d; e += NT) xhat_out[e] = xs[xs_index<T>(e, d)];
-  bool first = true;
-  for (; row < nrows; row += G * NW) {
-    const T* rp = row_ptr(row);
-    const float v = first ? wave_rowdot_pf<T, U, 1>(rp, xs, d, lane, 0, pf) : wave_rowdot<T, U, 1>(rp, xs, d, lane, 0);
-    first = false;
-    if (lane == 0) epi(row, v);
+  if (active) {
+    if constexpr (PIPE) {
+      u32x4 wb[U];
+      for (int sb = s0;;) {
+        load(wb, sb + U);
+        consume(wa, sb);
+        sb += U;
+        if (sb >= s1) break;
+        load(wa, sb + U);
+        consume(wb, sb);
+        sb += U;
+        if (sb >= s1) break;
+      }
+    } else {
+      // one register set: when a wavefront has at most U loads (the usual case for
+      // a few thousand rows) all of them are in flight before the prologue
+      for (int sb = s0;;) {
+        consume(wa, sb);
+        sb += U;
+        if (sb >= s1) break;
+        load(wa, sb);
+      }
+    }
+    flush();
+  }
+  __syncthreads();
+  for (int rr = threadIdx.x; rr < r1 - r0; rr += NT) {
+    const int wa0 = (rr * ipr) / tw, wb0 = min(((rr + 1) * ipr - 1) / tw, NW - 1);
+    float v = 0.f;
+    for (int w = wa0; w <= wb0; ++w) v += part[w * mr + (rr - (w * tw) / ipr)];
+    epi(r0 + rr, v);
   }
 }
 
-// Chunks per lane needed for a row of nch chunks with NW wavefronts.
-inline int rowdot_jmax(int nch, int nw) {
-  const int j = (nch + 64 * nw - 1) / (64 * nw);
-  return j <= 1 ? 1 : (j <= 2 ? 2 : (j <= 4 ? 4 : 8));
-}
+// Smallest KX for a row of d floats with NW wavefronts (at most 4).
+inline int rowdot_kx(int d, int nw) { return (d + 256 * nw - 1) / (256 * nw); }
+
+// LDS floats rowdot_flat needs for its per-wavefront records.
+inline int rowdot_flat_part(int nrows, int G, int nw) { return nw * ((nrows + G - 1) / G + 1); }
 
 }  // namespace dv
