@@ -420,21 +420,21 @@ extern "C" dv_status dv_sparse_block(const dv_attn* a, const dv_mlp* m, const dv
   q.x = o.xhat; q.g = nullptr; q.be = nullptr; q.eps = 0.f;
   q.Wq = a->Wq; q.Wk = a->Wk; q.Wv = a->Wv; q.bq = a->bq; q.bk = a->bk; q.bv = a->bv;
   q.K = kv->K; q.V = kv->V; q.q = o.q; q.heads_in = o.heads; q.heads_ws = nullptr;
+  if (ahead) {
+    // the neuron selection (from the LN1(y) scores) runs in one extra workgroup of
+    // the QKV launch, beside its weight stream, off the critical path (Section 4.3)
+    q.sel_n = m->n; q.sel_scores = o.s_m; q.sel_k = k_mlp; q.sel_idx = o.idx; q.sel_idx_out = idx_out;
+  }
   DV_LAUNCH("qkv", hs, launch_qkv(a->wtype, kv->ktype, q, hs));
   // 4. Split-KV attention.
   AttnWs ao{};
   ao.heads = o.heads; ao.q = o.q; ao.part = o.part;
   if ((st = enqueue_attention(a, kv, ao, k_heads, scale, hs)) != DV_OK) return st;
-  // 5. Out-projection + residual: y~ = y + MHA(LN1(y)). Look-ahead: the neuron
-  //    selection (from the LN1(y) scores) runs in one extra workgroup of this launch,
-  //    beside the out-projection's weight stream, off the critical path (Section 4.3).
+  // 5. Out-projection + residual: y~ = y + MHA(LN1(y)).
   AxpyArgs ax{};
   ax.d = a->d; ax.nrows = k_heads * a->dh; ax.M = a->WoT; ax.m_rows = a->H * a->dh; ax.set = o.heads;
   ax.dh = a->dh; ax.coef = nullptr; ax.part = o.part; ax.n_split = attn_nsplit(a, kv, k_heads);
   ax.resid = x_in; ax.bias = a->bo; ax.out = o.ytilde; ax.out2 = nullptr;
-  if (ahead) {
-    ax.sel_n = m->n; ax.sel_scores = o.s_m; ax.sel_k = k_mlp; ax.sel_idx = o.idx; ax.sel_idx_out = idx_out;
-  }
   if ((st = enqueue_axpy("oproj", a->wtype, ax, hs)) != DV_OK) return st;
   // 5b. Sequential mode: the neuron predictor reads LN2(y~).
   if (!ahead) {

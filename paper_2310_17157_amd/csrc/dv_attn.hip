@@ -4,7 +4,8 @@
 //
 //   k_qkv   gathered row-dots: for every selected head i, the dh rows of W^Q_i, W^K_i
 //           and W^V_i (contiguous row blocks) against the staged x-hat; q goes to the
-//           workspace, k and v to cache row pos.
+//           workspace, k and v to cache row pos. An extra workgroup may host the
+//           neuron top-k of the look-ahead layer.
 //   k_attn  split-KV decode attention: one workgroup per (sequence, selected head,
 //           position chunk) computes the chunk's max logit, sum of exponentials and
 //           unnormalised value sum; the out-projection kernel combines the chunks.
@@ -12,6 +13,7 @@
 
 #include "dv_internal.hpp"
 #include "dv_rowdot.hpp"
+#include "dv_select.hpp"
 
 namespace dv {
 
@@ -19,7 +21,11 @@ template <typename T, typename KT, int NW, int U, int KX>
 __global__ void __launch_bounds__(NW * 64) k_qkv(QkvArgs a) {
   extern __shared__ float smem[];
   constexpr int NT = NW * 64;
-  const int wg = blockIdx.x, nwg = gridDim.x;
+  const int wg = blockIdx.x, nwg = gridDim.x - (a.sel_n > 0 ? 1 : 0);
+  if (a.sel_n > 0 && wg == nwg) {
+    hosted_select<NT>(a.sel_scores, a.sel_n, a.sel_k, a.sel_idx, a.sel_idx_out, smem);
+    return;
+  }
   float* xs = smem;
   float* red = smem + a.d;
   int32_t* hset = reinterpret_cast<int32_t*>(red + NW);
@@ -54,15 +60,22 @@ __global__ void __launch_bounds__(NW * 64) k_qkv(QkvArgs a) {
   rowdot_flat<T, NW, U, true, KX>(row_ptr, epi, 3 * per_mat, a.d, a.x, a.g, a.be, a.eps, xs, red, part, nullptr, wg, nwg);
 }
 
+// CUs left without a QKV workgroup when a selection is hosted in the launch.
+constexpr int kQkvSelFreeCUs = 4;
+
 template <typename T, typename KT, int KX>
 static hipError_t launch_qkv_t(const QkvArgs& a, hipStream_t st) {
   constexpr int NW = 16, U = 8;
+  constexpr int NT = NW * 64;
   const int nrows = 3 * a.n_heads * a.dh;
-  // One workgroup per CU, each a contiguous range of rows (rowdot_flat).
-  const int blocks = max(1, min(nrows, device_cu_count()));
+  // One workgroup per CU, each a contiguous range of rows (rowdot_flat). A hosted
+  // selection gets one more workgroup, and a few CUs are left free for it to start at once.
+  const int cus = device_cu_count();
+  const int blocks = max(1, min(nrows, a.sel_n > 0 ? max(1, cus - kQkvSelFreeCUs) : cus));
   size_t lds = (size_t)(a.d + NW) * sizeof(float) + (size_t)a.n_heads * sizeof(int32_t) +
                (size_t)rowdot_flat_part(nrows, blocks, NW) * sizeof(float) + 16;
-  hipLaunchKernelGGL((k_qkv<T, KT, NW, U, KX>), dim3(blocks), dim3(NW * 64), lds, st, a);
+  if (a.sel_n > 0) lds = max(lds, (size_t)kSelBins * 4 + kSelSm(NT) * sizeof(int));
+  hipLaunchKernelGGL((k_qkv<T, KT, NW, U, KX>), dim3(blocks + (a.sel_n > 0 ? 1 : 0)), dim3(NW * 64), lds, st, a);
   return hipGetLastError();
 }
 

@@ -20,7 +20,6 @@
 #include <math.h>
 
 #include "dv_internal.hpp"
-#include "dv_select.hpp"
 
 namespace dv {
 
@@ -54,36 +53,13 @@ __device__ __forceinline__ void ax_consume(const u32x4 (&w)[U], const float* cf,
   }
 }
 
-// Top-k selection hosted by one extra workgroup of an axpy launch. The axpy grid (one
-// workgroup per 128-byte column tile: 192 at d = 12288 in fp16) leaves CUs free, so
-// the selection (about 20-30 us on one CU) runs beside the weight stream instead of
-// on the critical path; it is kept out of line so that its register allocation does
-// not constrain the axpy path. Up to kSelIPT * NT scores are selected from registers,
-// larger score vectors stream from memory.
-constexpr int kSelIPT = 48;
-
-template <int NT>
-__device__ __noinline__ void axpy_hosted_select(const float* scores, int n, int k, int32_t* idx,
-                                                int32_t* idx_out, float* smem) {
-  uint32_t* hist = reinterpret_cast<uint32_t*>(smem);
-  int* sm = reinterpret_cast<int*>(smem + kSelBins);
-  if (n <= NT * kSelIPT)
-    wg_select_reg<NT, kSelIPT>(scores, n, DV_SELECT_TOPK, k, 0.f, idx, k, nullptr, idx_out, hist, sm);
-  else
-    wg_select<NT>(scores, n, DV_SELECT_TOPK, k, 0.f, idx, k, nullptr, idx_out, hist, sm);
-}
-
 // HEADS selects the attention form (rows are dh-row blocks of selected heads, the
-// coefficients are combined from split-KV partials, and a selection may be hosted);
-// otherwise rows are single neurons with coefficients given per row.
+// coefficients are combined from split-KV partials); otherwise rows are single
+// neurons with coefficients given per row.
 template <typename T, int NW, int TL, int U, bool HEADS>
 __global__ void __launch_bounds__(NW * 64) k_axpy(AxpyArgs a) {
   constexpr int NT = NW * 64;
   extern __shared__ float smem[];
-  if (HEADS && a.sel_n > 0 && blockIdx.x == gridDim.x - 1) {
-    axpy_hosted_select<NT>(a.sel_scores, a.sel_n, a.sel_k, a.sel_idx, a.sel_idx_out, smem);
-    return;
-  }
   constexpr int E = Chunk<T>::E;
   constexpr int RPI = 64 / TL;                  // rows per load instruction
   constexpr int step = NW * RPI;                // rows per wavefront-group step
@@ -229,8 +205,7 @@ static hipError_t launch_axpy_t(AxpyArgs a, hipStream_t st) {
   }
   a.rows_per_batch = max(1, min(rpb, max(a.nrows, 1)));
   size_t lds = (size_t)a.rows_per_batch * 8 + (size_t)kAxNW * kAxTL * E * 4 + fac + 16;
-  if (a.sel_n > 0) lds = max(lds, (size_t)kSelBins * 4 + kSelSm(kAxNW * 64) * sizeof(int));
-  const int blocks = tiles + (a.sel_n > 0 ? 1 : 0);
+  const int blocks = tiles;
   hipLaunchKernelGGL((k_axpy<T, kAxNW, kAxTL, kAxU, HEADS>), dim3(blocks), dim3(kAxNW * 64), lds, st, a);
   return hipGetLastError();
 }
@@ -238,7 +213,6 @@ static hipError_t launch_axpy_t(AxpyArgs a, hipStream_t st) {
 hipError_t launch_axpy(int wtype, const AxpyArgs& a, hipStream_t st) {
   if (a.dh > 0)
     return wtype == DV_F16 ? launch_axpy_t<_Float16, true>(a, st) : launch_axpy_t<float, true>(a, st);
-  if (a.sel_n > 0) return hipErrorInvalidValue;
   return wtype == DV_F16 ? launch_axpy_t<_Float16, false>(a, st) : launch_axpy_t<float, false>(a, st);
 }
 

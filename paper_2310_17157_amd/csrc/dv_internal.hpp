@@ -297,6 +297,8 @@ struct QkvArgs {
   float* q;                         // [n_heads][dh] out
   const int32_t* heads_in;          // [n_heads] the head set
   int32_t* heads_ws;                // optional [n_heads] out: the set, clamped (one workgroup)
+  // Top-k selection run by one extra workgroup of the launch (sel_n == 0: none).
+  const float* sel_scores; int sel_n; int sel_k; int32_t* sel_idx; int32_t* sel_idx_out;
 };
 hipError_t launch_qkv(int wtype, int kvtype, const QkvArgs& a, hipStream_t st);
 
@@ -329,8 +331,6 @@ struct AxpyArgs {
   float* out;                        // [d]
   float* out2;                       // optional second copy of out
   int rows_per_batch;                // set by the launcher
-  // Top-k selection run by one extra workgroup of the launch (sel_n == 0: none).
-  const float* sel_scores; int sel_n; int sel_k; int32_t* sel_idx; int32_t* sel_idx_out;
 };
 hipError_t launch_axpy(int wtype, const AxpyArgs& a, hipStream_t st);
 

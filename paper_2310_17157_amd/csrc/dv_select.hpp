@@ -353,6 +353,25 @@ __device__ void wg_select_reg(const float* __restrict__ s, int n, int mode, int 
   __syncthreads();
 }
 
+// Top-k selection run by one extra workgroup of another kernel's launch (which leaves
+// CUs free for it), so that the selection runs beside that kernel's weight stream
+// instead of on the critical path. Kept out of line so that its register allocation
+// does not constrain the host kernel's main path. Up to 48 * NT scores are selected
+// from registers, larger score vectors stream from memory. smem: kSelBins u32 plus
+// kSelSm(NT) ints of LDS.
+constexpr int kSelIPT = 48;
+
+template <int NT>
+__device__ __noinline__ void hosted_select(const float* scores, int n, int k, int32_t* idx, int32_t* idx_out,
+                                           float* smem) {
+  uint32_t* hist = reinterpret_cast<uint32_t*>(smem);
+  int* sm = reinterpret_cast<int*>(smem + kSelBins);
+  if (n <= NT * kSelIPT)
+    wg_select_reg<NT, kSelIPT>(scores, n, DV_SELECT_TOPK, k, 0.f, idx, k, nullptr, idx_out, hist, sm);
+  else
+    wg_select<NT>(scores, n, DV_SELECT_TOPK, k, 0.f, idx, k, nullptr, idx_out, hist, sm);
+}
+
 // Top-k of a short score vector (n <= NT) by rank counting; writes the ascending set
 // to lds_set[0..k). The keys are staged in LDS first (one coalesced load each), then
 // every thread ranks its key against all of them: O(n^2) LDS compares, used for the
