@@ -32,6 +32,7 @@ METRIC = "µs/layer/token sparse block at OPT-175B shape, batch 1; achieved HBM 
 METRIC_B32 = ("µs/layer/token sparse attention + union MLP at OPT-175B shape, batch 32 (sets given); "
               "achieved HBM GB/s vs peak")
 PEAK_HBM_GBPS = 8000.0
+ROOFLINE_EVERY = 8   # timed steps per event-bracketed launch of the dominant kernel
 
 
 def kernel_bytes(cfg, pos):
@@ -141,12 +142,14 @@ def cpu_baseline(cfg, t_host, pos, seconds=10.0):
                       f"{len(os.sched_getaffinity(0))}"}
 
 
-def _measure(stream, step, n, calls_per_step, only=None):
-    """Run n steps; per-call LaunchTimers (all launches, or only label `only`).
-    Returns (ms per step from events on `stream`, wall seconds, {label: [ms, ...]})."""
+def _measure(stream, step, n, calls_per_step, only=None, every=1):
+    """Run n steps; per-call LaunchTimers (all launches, or only label `only`) on the
+    steps i with i % every == 0. Returns (ms per step from events on `stream`, wall
+    seconds, {label: [ms, ...]})."""
     import torch
     from paper_2310_17157_amd import binding as Bd
-    timers = [[Bd.LaunchTimer(16, only=only) for _ in range(calls_per_step)] for _ in range(n)]
+    timers = [[Bd.LaunchTimer(16, only=only) for _ in range(calls_per_step)] if i % every == 0 else None
+              for i in range(n)]
     torch.cuda.synchronize()
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
@@ -159,7 +162,7 @@ def _measure(stream, step, n, calls_per_step, only=None):
     wall = time.perf_counter() - w0
     per = {}
     for ts in timers:
-        for tm in ts:
+        for tm in ts or ():
             for lab, ms in tm.times_ms():
                 per.setdefault(lab, []).append(ms)
             tm.close()
@@ -238,8 +241,9 @@ def bench_b1(args, cfg):
     ms_all_events, _, per_kernel = _measure(stream, step, args.steps, 1)
     kb = kernel_bytes(cfg, pos)
     dom = max((l for l in per_kernel if l in kb), key=lambda l: statistics.mean(per_kernel[l]))
-    # Timed region: events only around the dominant kernel's launch.
-    ms_per_step, wall, per_dom = _measure(stream, step, args.steps, 1, only=dom)
+    # Timed region: events around the dominant kernel's launch on every
+    # ROOFLINE_EVERY-th step (each event record idles the GPU for a few microseconds).
+    ms_per_step, wall, per_dom = _measure(stream, step, args.steps, 1, only=dom, every=ROOFLINE_EVERY)
     kernels = _kernel_table(per_kernel, kb.get)
     dom_avg_s = statistics.mean(per_dom[dom]) * 1e-3
     achieved = kb[dom] / dom_avg_s / 1e9
@@ -348,7 +352,7 @@ def bench_batch(args, cfg):
     # bytes per launch averaged over the replicas the steps cycled through
     kb = {lab: statistics.mean(L["kb"][lab] for L in layers) for lab in layers[0]["kb"]}
     dom = max((l for l in per_kernel if l in kb), key=lambda l: statistics.mean(per_kernel[l]))
-    ms_per_step, wall, per_dom = _measure(stream, step, args.steps, 2, only=dom)
+    ms_per_step, wall, per_dom = _measure(stream, step, args.steps, 2, only=dom, every=ROOFLINE_EVERY)
     kernels = _kernel_table(per_kernel, lambda l: round(kb[l]) if l in kb else None)
     dom_avg_s = statistics.mean(per_dom[dom]) * 1e-3
     achieved = kb[dom] / dom_avg_s / 1e9

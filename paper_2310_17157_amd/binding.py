@@ -320,6 +320,9 @@ def predict_workspace_bytes(pred, B) -> int:
 
 
 # --------------------------------------------------------- per-launch timing
+_HIP_EVENT_DISABLE_SYSTEM_FENCE = 0x20000000   # hipEventDisableSystemFence
+
+
 class LaunchTimer:
     """HIP events around each kernel launch of the library's entry points.
 
@@ -331,7 +334,7 @@ class LaunchTimer:
 
     def __init__(self, n_pairs: int = 16, only: Optional[str] = None):
         self._hip = ctypes.CDLL("libamdhip64.so")
-        self._hip.hipEventCreate.argtypes = [POINTER(c_void_p)]
+        self._hip.hipEventCreateWithFlags.argtypes = [POINTER(c_void_p), ctypes.c_uint]
         self._hip.hipEventElapsedTime.argtypes = [POINTER(c_float), c_void_p, c_void_p]
         self._hip.hipEventSynchronize.argtypes = [c_void_p]
         self._hip.hipEventDestroy.argtypes = [c_void_p]
@@ -339,8 +342,10 @@ class LaunchTimer:
         self.events = (c_void_p * (2 * n_pairs))()
         for i in range(2 * n_pairs):
             ev = c_void_p()
-            if self._hip.hipEventCreate(ctypes.byref(ev)) != 0:
-                raise RuntimeError("hipEventCreate failed")
+            # timing-only events: no system-scope fence (cache write-back and
+            # invalidation) when recorded, which would stall the next launch
+            if self._hip.hipEventCreateWithFlags(ctypes.byref(ev), _HIP_EVENT_DISABLE_SYSTEM_FENCE) != 0:
+                raise RuntimeError("hipEventCreateWithFlags failed")
             self.events[i] = ev
         self.n_launched = c_int32(0)
         self.only = only.encode() if only else None

@@ -153,11 +153,15 @@ static dv_status enqueue_axpy(const char* label, int wtype, const AxpyArgs& ax, 
 
 // ---------------------------------------------------------------- sparse MLP
 struct MlpWs {
-  float* h; int32_t* flag;
+  float* h; float* axp; int32_t* flag;
 };
+
+// Row-split partial sums of a gathered row-axpy of width d.
+static size_t axpy_partial_bytes(int d) { return (size_t)kAxpyMaxRowSplit * d * sizeof(float); }
 
 static size_t mlp_ws_layout(const dv_mlp* m, int B, int n_idx, Workspace& w, MlpWs* o) {
   o->h = w.take<float>((size_t)B * n_idx * sizeof(float));
+  o->axp = w.take<float>(axpy_partial_bytes(m->d));
   o->flag = w.take<int32_t>(sizeof(int32_t));
   return w.off;
 }
@@ -201,14 +205,14 @@ extern "C" dv_status dv_sparse_mlp(const dv_mlp* m, const float* x, int32_t B, c
   DV_LAUNCH("fc1", hs, launch_fc1(m->wtype, f, hs));
   AxpyArgs ax{};
   ax.d = m->d; ax.nrows = n_idx; ax.M = m->W2T; ax.m_rows = m->n; ax.set = idx; ax.dh = 0;
-  ax.coef = o.h; ax.resid = nullptr; ax.bias = m->b2; ax.out = out; ax.out2 = nullptr;
+  ax.coef = o.h; ax.resid = nullptr; ax.bias = m->b2; ax.out = out; ax.out2 = nullptr; ax.partial = o.axp;
   if ((st = enqueue_axpy("fc2", m->wtype, ax, hs)) != DV_OK) return st;
   return DV_OK;
 }
 
 // ---------------------------------------------------------- sparse attention
 struct AttnWs {
-  int32_t* heads; float* q; float* part; int32_t* flag;
+  int32_t* heads; float* q; float* part; float* axp; int32_t* flag;
 };
 
 // Upper bound of split-KV chunks per head.
@@ -218,6 +222,7 @@ static size_t attn_ws_layout(const dv_attn* a, int cap, int B, int n_heads, Work
   o->heads = w.take<int32_t>((size_t)B * n_heads * sizeof(int32_t));
   o->q = w.take<float>((size_t)B * n_heads * a->dh * sizeof(float));
   o->part = w.take<float>((size_t)B * n_heads * max_split(cap) * (a->dh + 2) * sizeof(float));
+  o->axp = w.take<float>(axpy_partial_bytes(a->d));
   o->flag = w.take<int32_t>(sizeof(int32_t));
   return w.off;
 }
@@ -294,14 +299,14 @@ extern "C" dv_status dv_sparse_attn(const dv_attn* a, const float* x, int32_t B,
   AxpyArgs ax{};
   ax.d = a->d; ax.nrows = n_heads * a->dh; ax.M = a->WoT; ax.m_rows = a->H * a->dh; ax.set = o.heads;
   ax.dh = a->dh; ax.coef = nullptr; ax.part = o.part; ax.n_split = attn_nsplit(a, kv, n_heads);
-  ax.resid = nullptr; ax.bias = a->bo; ax.out = out; ax.out2 = nullptr;
+  ax.resid = nullptr; ax.bias = a->bo; ax.out = out; ax.out2 = nullptr; ax.partial = o.axp;
   return enqueue_axpy("oproj", a->wtype, ax, hs);
 }
 
 // ------------------------------------------------------------- decoder layer
 struct BlockWs {
   float* hid_h; float* hid_m; float* s_h; float* s_m; int32_t* heads; int32_t* idx;
-  float* q; float* part; float* ytilde; float* xhat; float* h; int32_t* flag;
+  float* q; float* part; float* ytilde; float* xhat; float* h; float* axp; int32_t* flag;
 };
 
 static size_t block_ws_layout(const dv_attn* a, const dv_mlp* m, const dv_predictor* pa,
@@ -318,6 +323,7 @@ static size_t block_ws_layout(const dv_attn* a, const dv_mlp* m, const dv_predic
   o->ytilde = w.take<float>((size_t)B * a->d * sizeof(float));
   o->xhat = w.take<float>((size_t)B * a->d * sizeof(float));
   o->h = w.take<float>((size_t)B * km * sizeof(float));
+  o->axp = w.take<float>(axpy_partial_bytes(a->d));
   o->flag = w.take<int32_t>(sizeof(int32_t));
   return w.off;
 }
@@ -434,7 +440,7 @@ extern "C" dv_status dv_sparse_block(const dv_attn* a, const dv_mlp* m, const dv
   AxpyArgs ax{};
   ax.d = a->d; ax.nrows = k_heads * a->dh; ax.M = a->WoT; ax.m_rows = a->H * a->dh; ax.set = o.heads;
   ax.dh = a->dh; ax.coef = nullptr; ax.part = o.part; ax.n_split = attn_nsplit(a, kv, k_heads);
-  ax.resid = x_in; ax.bias = a->bo; ax.out = o.ytilde; ax.out2 = nullptr;
+  ax.resid = x_in; ax.bias = a->bo; ax.out = o.ytilde; ax.out2 = nullptr; ax.partial = o.axp;
   if ((st = enqueue_axpy("oproj", a->wtype, ax, hs)) != DV_OK) return st;
   // 5b. Sequential mode: the neuron predictor reads LN2(y~).
   if (!ahead) {
@@ -456,7 +462,7 @@ extern "C" dv_status dv_sparse_block(const dv_attn* a, const dv_mlp* m, const dv
   // 7. fc2 + residual: y^ = y~ + MLP(LN2(y~)).
   AxpyArgs ay{};
   ay.d = m->d; ay.nrows = k_mlp; ay.M = m->W2T; ay.m_rows = m->n; ay.set = o.idx; ay.dh = 0;
-  ay.coef = o.h; ay.resid = o.ytilde; ay.bias = m->b2; ay.out = x_out; ay.out2 = nullptr;
+  ay.coef = o.h; ay.resid = o.ytilde; ay.bias = m->b2; ay.out = x_out; ay.out2 = nullptr; ay.partial = o.axp;
   if ((st = enqueue_axpy("fc2", m->wtype, ay, hs)) != DV_OK) return st;
   return DV_OK;
 }

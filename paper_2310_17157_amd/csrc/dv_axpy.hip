@@ -6,86 +6,60 @@
 // Both weights are stored transposed so that a selected neuron or head is a set of
 // whole contiguous rows (Section 4.4 "Memory coalescing").
 //
-// Tiling: a workgroup owns a 128-byte column tile (8 lanes x one 16-byte chunk) of
-// every selected row, so each wavefront load instruction covers 8 rows and each
-// wavefront keeps U such instructions in flight. The workgroup sums all selected rows
-// of its tile, so no cross-workgroup reduction, atomics or device-scope fences are
-// needed (on a multi-XCD part a device-scope release writes back the whole L2 of the
-// XCD). Lane partials are combined across row groups with shuffles and across
-// wavefronts in LDS, in a fixed order: the result is bitwise reproducible.
+// Tiling: the grid is (column spans) x (row splits). A span is 64 lanes x 16 bytes,
+// so every wavefront load instruction reads 1 KB of one row, contiguous in memory;
+// workgroup (c, s) sums span c of the rows in split s, wavefront w taking the rows
+// w, w + NW, ... of the split with U loads in flight and the next U issued before the
+// current are consumed. Wavefront partials are added in LDS in wavefront order; with
+// one split the workgroup writes out directly, otherwise it writes its partial row
+// to partial[s] and a second small launch adds the splits in split order, so the
+// result is bitwise reproducible and no cross-workgroup synchronisation (device-scope
+// fences, which write back and invalidate a whole L2) is needed.
 //
 // For the attention the coefficients H_i(y)[t] are combined first, in the prologue,
 // from the split-KV partials (max logit, sum of exponentials and unnormalised value
-// sums per position chunk) of every selected head.
+// sums per position chunk) of the heads of the workgroup's rows, while the first
+// weight loads are in flight.
 #include <math.h>
 
 #include "dv_internal.hpp"
 
 namespace dv {
 
-constexpr int kAxNW = 16;   // wavefronts per workgroup
-constexpr int kAxTL = 8;    // lanes (16-byte chunks) per row segment: 128-byte tiles
-constexpr int kAxU = 8;     // row instructions per batch (two batches in flight)
+constexpr int kAxNW = 8;    // wavefronts per workgroup
+constexpr int kAxU = 8;     // row loads per batch (two batches in flight)
+constexpr int kAxRowsLds = 3072;   // (coefficient, row index) pairs per LDS batch
 
 constexpr int kAxMaxSplit = kAttnMaxSplit;   // split-KV chunks, combined with all loads in flight
-
-template <typename T, int TL, int U>
-__device__ __forceinline__ void ax_load(u32x4 (&w)[U], const char* Mb, size_t rowb, const int* ri, int r,
-                                        int step, int nb) {
-#pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int row = r + step * u;
-    w[u] = row < nb ? ld_stream(Mb + (size_t)ri[row] * rowb) : u32x4{0u, 0u, 0u, 0u};
-  }
-}
-
-template <typename T, int E, int U>
-__device__ __forceinline__ void ax_consume(const u32x4 (&w)[U], const float* cf, int r, int step, int nb,
-                                           float (&acc)[E]) {
-#pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int row = r + step * u;
-    float v[E];
-    unpack<T>(w[u], v);
-    const float f = row < nb ? cf[row] : 0.f;
-#pragma unroll
-    for (int e = 0; e < E; ++e) acc[e] = fmaf(f, v[e], acc[e]);
-  }
-}
 
 // HEADS selects the attention form (rows are dh-row blocks of selected heads, the
 // coefficients are combined from split-KV partials); otherwise rows are single
 // neurons with coefficients given per row.
-template <typename T, int NW, int TL, int U, bool HEADS>
+template <typename T, int NW, int U, bool HEADS>
 __global__ void __launch_bounds__(NW * 64) k_axpy(AxpyArgs a) {
   constexpr int NT = NW * 64;
-  extern __shared__ float smem[];
   constexpr int E = Chunk<T>::E;
-  constexpr int RPI = 64 / TL;                  // rows per load instruction
-  constexpr int step = NW * RPI;                // rows per wavefront-group step
-  float* cf = smem;                                              // [rows_per_batch] coefficients
-  int* ri = reinterpret_cast<int*>(cf + a.rows_per_batch);       // [rows_per_batch] row indices
-  float* red = reinterpret_cast<float*>(ri + a.rows_per_batch);  // [NW][TL*E] wavefront sums
-  float* fac = red + NW * TL * E;                                // [heads of a batch][n_split]
+  constexpr int SW = 64 * E;                                     // columns per span
+  extern __shared__ float smem[];
+  const int rpb = a.rows_per_batch;
+  float* cf = smem;                                              // [rpb] coefficients
+  int* ri = reinterpret_cast<int*>(cf + rpb);                    // [rpb] row indices
+  float* red = reinterpret_cast<float*>(ri + rpb);               // [NW][SW] wavefront sums
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int S = gridDim.y, sp = blockIdx.y;
+  const int r0 = (int)((long)sp * a.nrows / S), r1 = (int)((long)(sp + 1) * a.nrows / S);
   const int nch = a.d / E;
-  const int c = blockIdx.x * TL + (lane % TL);
-  const int grp = lane / TL;
-  const bool on = c < nch;
-
-  float acc[E];
-#pragma unroll
-  for (int e = 0; e < E; ++e) acc[e] = 0.f;
-  const char* Mb = static_cast<const char*>(a.M) + (size_t)(on ? c : 0) * 16;
+  const char* Mb = static_cast<const char*>(a.M) + (size_t)min((int)blockIdx.x * 64 + lane, nch - 1) * 16;
   const size_t rowb = (size_t)a.d * sizeof(T);
   const int ns = a.n_split;
   const int stride = a.dh + 2;
 
-  // Rows are processed in batches of at most rows_per_batch so that their
-  // coefficients and row indices fit in LDS.
-  for (int rb = 0; rb < a.nrows; rb += a.rows_per_batch) {
-    const int nb = min(a.rows_per_batch, a.nrows - rb);
-    const int h0 = HEADS ? rb / a.dh : 0;
+  float acc[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) acc[e] = 0.f;
+
+  for (int rb = r0; rb < r1; rb += rpb) {
+    const int nb = min(rpb, r1 - rb);
     // ---- row indices (they need only the set), then this wavefront's first loads
     for (int i = tid; i < nb; i += NT) {
       const int row = rb + i;
@@ -97,116 +71,138 @@ __global__ void __launch_bounds__(NW * 64) k_axpy(AxpyArgs a) {
       }
     }
     __syncthreads();
-    const int rfirst = wave * RPI + grp;
-    u32x4 wa[U];
-    if (on) ax_load<T, TL, U>(wa, Mb, rowb, ri, rfirst, step, nb);
+    // this wavefront's rows: wave + NW * i, i < nwr; loads past the end are clamped
+    // to the last row (and weighted by zero), so every batch issues U loads
+    const int nwr = nb > wave ? (nb - wave + NW - 1) / NW : 0;
+    auto load = [&](u32x4 (&w)[U], int i0) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int i = min(wave + NW * (i0 + u), nb - 1);
+        w[u] = ld_stream(Mb + (size_t)ri[i] * rowb);
+      }
+    };
+    auto consume = [&](const u32x4 (&w)[U], int i0) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int i = i0 + u;
+        const float f = i < nwr ? cf[wave + NW * i] : 0.f;
+        float v[E];
+        unpack<T>(w[u], v);
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[e] = fmaf(f, v[e], acc[e]);
+      }
+    };
+    u32x4 wa[U], wb[U];
+    if (nwr > 0) load(wa, 0);
     // ---- coefficients, while those loads are in flight
     if (!HEADS) {
       for (int i = tid; i < nb; i += NT) cf[i] = a.coef[rb + i];
     } else {
-      // fac[h][s] = exp(m_s - M_h) / L_h for the heads of this batch (ns <= kAxMaxSplit)
-      const int h1 = (rb + nb - 1) / a.dh;
-      for (int hh = tid; hh <= h1 - h0; hh += NT) {
-        const float* P = a.part + (size_t)(h0 + hh) * ns * stride;
-        float m[kAxMaxSplit], l[kAxMaxSplit];
-        float M = -INFINITY;
-#pragma unroll
-        for (int sp = 0; sp < kAxMaxSplit; ++sp) {
-          m[sp] = sp < ns ? P[(size_t)sp * stride] : -INFINITY;
-          l[sp] = sp < ns ? P[(size_t)sp * stride + 1] : 0.f;
-          M = fmaxf(M, m[sp]);
-        }
-        float L = 0.f;
-#pragma unroll
-        for (int sp = 0; sp < kAxMaxSplit; ++sp) {
-          m[sp] = m[sp] == -INFINITY ? 0.f : __expf(m[sp] - M);
-          L += l[sp] * m[sp];
-        }
-        const float inv = 1.f / L;
-#pragma unroll
-        for (int sp = 0; sp < kAxMaxSplit; ++sp)
-          if (sp < ns) fac[hh * ns + sp] = m[sp] * inv;
-      }
-      __syncthreads();
+      // one thread per row reads its head's (m_s, l_s) and its own o_s[t] of every
+      // chunk s in one round: H(y)[t] = sum_s e^{m_s - M} o_s[t] / sum_s e^{m_s - M} l_s
       for (int i = tid; i < nb; i += NT) {
         const int row = rb + i;
         const int h = row / a.dh, t = row - h * a.dh;
-        const float* P = a.part + (size_t)h * ns * stride + 2 + t;
-        const float* F = fac + (h - h0) * ns;
-        float o[kAxMaxSplit];
+        const float* P = a.part + (size_t)h * ns * stride;
+        float m[kAxMaxSplit], l[kAxMaxSplit], o[kAxMaxSplit];
 #pragma unroll
-        for (int sp = 0; sp < kAxMaxSplit; ++sp) o[sp] = sp < ns ? P[(size_t)sp * stride] : 0.f;
-        float s0 = 0.f, s1 = 0.f;
-#pragma unroll
-        for (int sp = 0; sp < kAxMaxSplit; sp += 2) {
-          if (sp < ns) s0 = fmaf(o[sp], F[sp], s0);
-          if (sp + 1 < ns) s1 = fmaf(o[sp + 1], F[sp + 1], s1);
+        for (int s = 0; s < kAxMaxSplit; ++s) {
+          m[s] = s < ns ? P[(size_t)s * stride] : -INFINITY;
+          l[s] = s < ns ? P[(size_t)s * stride + 1] : 0.f;
+          o[s] = s < ns ? P[(size_t)s * stride + 2 + t] : 0.f;
         }
-        cf[i] = s0 + s1;
+        float M = -INFINITY;
+#pragma unroll
+        for (int s = 0; s < kAxMaxSplit; ++s) M = fmaxf(M, m[s]);
+        float L = 0.f, num = 0.f;
+#pragma unroll
+        for (int s = 0; s < kAxMaxSplit; ++s) {
+          const float f = m[s] == -INFINITY ? 0.f : __expf(m[s] - M);
+          L = fmaf(l[s], f, L);
+          num = fmaf(o[s], f, num);
+        }
+        cf[i] = num / L;
       }
     }
     __syncthreads();
 
-    // ---- stream: wavefront w, row group g takes rows w*RPI + g + k*step, U load
-    // instructions per batch, the next batch issued before the current is consumed.
-    if (on) {
-      for (int r = rfirst; r - grp < nb; r += step * U) {
-        u32x4 wb[U];
-        const bool more = r - grp + step * U < nb;
-        if (more) ax_load<T, TL, U>(wb, Mb, rowb, ri, r + step * U, step, nb);
-        ax_consume<T, E, U>(wa, cf, r, step, nb, acc);
-        if (more) {
-#pragma unroll
-          for (int u = 0; u < U; ++u) wa[u] = wb[u];
-        }
+    // ---- stream, alternating two register sets
+    if (nwr > 0) {
+      for (int i0 = 0;;) {
+        if (i0 + U < nwr) load(wb, i0 + U);
+        consume(wa, i0);
+        i0 += U;
+        if (i0 >= nwr) break;
+        if (i0 + U < nwr) load(wa, i0 + U);
+        consume(wb, i0);
+        i0 += U;
+        if (i0 >= nwr) break;
       }
     }
-    __syncthreads();
+    __syncthreads();   // ri / cf are rewritten by the next batch
   }
-  // ---- combine row groups (lanes with equal lane % TL), then wavefronts, in order
+  // ---- combine wavefronts in order, then write out (one split) or partial[sp]
 #pragma unroll
-  for (int o = TL; o < 64; o <<= 1)
-#pragma unroll
-    for (int e = 0; e < E; ++e) acc[e] += __shfl_xor(acc[e], o, kWave);
-  if (grp == 0) {
-#pragma unroll
-    for (int e = 0; e < E; ++e) red[wave * TL * E + lane * E + e] = acc[e];
-  }
+  for (int e = 0; e < E; ++e) red[wave * SW + lane * E + e] = acc[e];
   __syncthreads();
-  if (tid < TL * E) {
-    const int col = blockIdx.x * TL * E + tid;
+  for (int t = tid; t < SW; t += NT) {
+    const int col = blockIdx.x * SW + t;
     if (col < a.d) {
       float s = 0.f;
 #pragma unroll
-      for (int w = 0; w < NW; ++w) s += red[w * TL * E + tid];
-      if (a.resid) s += a.resid[col];
-      if (a.bias) s += a.bias[col];
-      a.out[col] = s;
-      if (a.out2) a.out2[col] = s;
+      for (int w = 0; w < NW; ++w) s += red[w * SW + t];
+      if (S == 1) {
+        if (a.resid) s += a.resid[col];
+        if (a.bias) s += a.bias[col];
+        a.out[col] = s;
+        if (a.out2) a.out2[col] = s;
+      } else {
+        a.partial[(size_t)sp * a.d + col] = s;
+      }
     }
   }
+}
+
+// out = sum_s partial[s] (in split order) + resid + bias; four columns per thread,
+// every split's load issued before the first add.
+__global__ void __launch_bounds__(256) k_axpy_sum(AxpyArgs a, int S) {
+  const int i = (blockIdx.x * 256 + threadIdx.x) * 4;
+  if (i >= a.d) return;
+  f32x4 p[kAxpyMaxRowSplit];
+#pragma unroll
+  for (int s = 0; s < kAxpyMaxRowSplit; ++s)
+    if (s < S) p[s] = *reinterpret_cast<const f32x4*>(a.partial + (size_t)s * a.d + i);
+  f32x4 v = p[0];
+#pragma unroll
+  for (int s = 1; s < kAxpyMaxRowSplit; ++s)
+    if (s < S) v += p[s];
+  if (a.resid) v += *reinterpret_cast<const f32x4*>(a.resid + i);
+  if (a.bias) v += *reinterpret_cast<const f32x4*>(a.bias + i);
+  *reinterpret_cast<f32x4*>(a.out + i) = v;
+  if (a.out2) *reinterpret_cast<f32x4*>(a.out2 + i) = v;
+}
+
+// Row splits: enough workgroups to give every CU one, each split at least two rows
+// per wavefront; one split when there is no partial buffer.
+static int axpy_row_splits(int d, int E, int nrows) {
+  const int spans = (d / E + 63) / 64;
+  int S = device_cu_count() / spans;
+  S = min(S, nrows / (2 * kAxNW));
+  return max(1, min(S, kAxpyMaxRowSplit));
 }
 
 template <typename T, bool HEADS>
 static hipError_t launch_axpy_t(AxpyArgs a, hipStream_t st) {
   constexpr int E = Chunk<T>::E;
-  const int nch = a.d / E;
-  const int tiles = (nch + kAxTL - 1) / kAxTL;
-  // LDS budget: 40 KB of (coefficient, row index) pairs plus the combine factors of
-  // the heads a batch touches.
-  int rpb = 5120;
-  size_t fac = 0;
-  if (HEADS) {
-    for (;;) {
-      fac = (size_t)(rpb / a.dh + 2) * a.n_split * 4;
-      if (fac <= 16384 || rpb <= 256) break;
-      rpb /= 2;
-    }
-  }
-  a.rows_per_batch = max(1, min(rpb, max(a.nrows, 1)));
-  size_t lds = (size_t)a.rows_per_batch * 8 + (size_t)kAxNW * kAxTL * E * 4 + fac + 16;
-  const int blocks = tiles;
-  hipLaunchKernelGGL((k_axpy<T, kAxNW, kAxTL, kAxU, HEADS>), dim3(blocks), dim3(kAxNW * 64), lds, st, a);
+  const int spans = (a.d / E + 63) / 64;
+  const int S = a.partial != nullptr ? axpy_row_splits(a.d, E, a.nrows) : 1;
+  // LDS: (coefficient, row index) pairs of a batch of the split's rows and the
+  // wavefront sums.
+  const int rpb = min(kAxRowsLds, max(1, (a.nrows + S - 1) / S));
+  a.rows_per_batch = rpb;
+  const size_t lds = (size_t)rpb * 8 + (size_t)kAxNW * 64 * E * 4;
+  hipLaunchKernelGGL((k_axpy<T, kAxNW, kAxU, HEADS>), dim3(spans, S), dim3(kAxNW * 64), lds, st, a);
+  if (S > 1) hipLaunchKernelGGL(k_axpy_sum, dim3((a.d / 4 + 255) / 256), dim3(256), 0, st, a, S);
   return hipGetLastError();
 }
 

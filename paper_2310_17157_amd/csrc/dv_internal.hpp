@@ -330,8 +330,11 @@ struct AxpyArgs {
   const float* resid; const float* bias;   // optional, [d]
   float* out;                        // [d]
   float* out2;                       // optional second copy of out
+  // Row-split partial sums [kAxpyMaxRowSplit][d] (workspace); NULL: one split.
+  float* partial;
   int rows_per_batch;                // set by the launcher
 };
+constexpr int kAxpyMaxRowSplit = 32;
 hipError_t launch_axpy(int wtype, const AxpyArgs& a, hipStream_t st);
 
 // fc1 + ReLU over the selected neurons (B = 1): h[s] = max(x-hat . W1T[set[s]] + b1, 0).
