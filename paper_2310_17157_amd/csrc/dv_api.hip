@@ -290,7 +290,7 @@ extern "C" dv_status dv_sparse_attn(const dv_attn* a, const float* x, int32_t B,
   }
   QkvArgs q{};
   q.d = a->d; q.H = a->H; q.dh = a->dh; q.cap = kv->cap; q.pos = kv->pos[0]; q.n_heads = n_heads;
-  q.x = x; q.g = nullptr; q.be = nullptr; q.eps = 0.f;
+  q.x = x;
   q.Wq = a->Wq; q.Wk = a->Wk; q.Wv = a->Wv; q.bq = a->bq; q.bk = a->bk; q.bv = a->bv;
   q.K = kv->K; q.V = kv->V; q.q = o.q; q.heads_in = heads; q.heads_ws = o.heads;
   DV_LAUNCH("qkv", hs, launch_qkv(a->wtype, kv->ktype, q, hs));
@@ -423,7 +423,7 @@ extern "C" dv_status dv_sparse_block(const dv_attn* a, const dv_mlp* m, const dv
   // 3. Gathered QKV of the selected heads + cache append.
   QkvArgs q{};
   q.d = a->d; q.H = a->H; q.dh = a->dh; q.cap = kv->cap; q.pos = kv->pos[0]; q.n_heads = k_heads;
-  q.x = o.xhat; q.g = nullptr; q.be = nullptr; q.eps = 0.f;
+  q.x = o.xhat;
   q.Wq = a->Wq; q.Wk = a->Wk; q.Wv = a->Wv; q.bq = a->bq; q.bk = a->bk; q.bv = a->bv;
   q.K = kv->K; q.V = kv->V; q.q = o.q; q.heads_in = o.heads; q.heads_ws = nullptr;
   if (ahead) {

@@ -57,7 +57,8 @@ __global__ void __launch_bounds__(NW * 64) k_qkv(QkvArgs a) {
       C[((size_t)head * a.cap + a.pos) * a.dh + t] = (KT)v;
     }
   };
-  rowdot_flat<T, NW, U, true, KX>(row_ptr, epi, 3 * per_mat, a.d, a.x, a.g, a.be, a.eps, xs, red, part, nullptr, wg, nwg);
+  rowdot_flat<T, NW, U, true, KX, false>(row_ptr, epi, 3 * per_mat, a.d, a.x, nullptr, nullptr, 0.f, xs, red, part,
+                                         nullptr, wg, nwg);
 }
 
 // CUs left without a QKV workgroup when a selection is hosted in the launch.
@@ -65,7 +66,9 @@ constexpr int kQkvSelFreeCUs = 4;
 
 template <typename T, typename KT, int KX>
 static hipError_t launch_qkv_t(const QkvArgs& a, hipStream_t st) {
-  constexpr int NW = 16, U = 8;
+  // 4 loads per batch, two batches in flight per wavefront: deeper queues only let
+  // the XCDs that win the fabric arbitration race ahead of the others
+  constexpr int NW = 16, U = 4;
   constexpr int NT = NW * 64;
   const int nrows = 3 * a.n_heads * a.dh;
   // One workgroup per CU, each a contiguous range of rows (rowdot_flat). A hosted

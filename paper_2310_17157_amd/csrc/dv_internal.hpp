@@ -146,72 +146,81 @@ __device__ __forceinline__ int block_excl_scan(int v, int* red, int* total) {
   return base + inc - v;
 }
 
-// Stage x[0..d) (fp32, 16-byte aligned, d % 4 == 0, d <= 16384) into LDS in the layout
-// of xs_index<T>, optionally applying layer norm with gamma g (NULL: no LN) and beta b
-// (NULL: 0). load() only issues the global reads of x, g and b into registers, so that a
-// caller can issue its own (HBM) loads behind them and still wait for these alone;
+// Staging of an fp32 input vector x[d] (16-byte aligned, d % 4 == 0) into LDS (xs,
+// fp32, in the layout of xs_index<T>); with LN (compile time) layer norm with gamma g and beta b (NULL: 0) is
+// applied. load() only issues the global reads of x (then g and b) into registers, so
+// that a caller can issue its own (HBM) loads behind them and still wait for these
+// alone: the reads are not predicated per lane (index clamped, surplus lanes masked
+// where used) and form straight-line code, which keeps the wait counts exact.
 // finish() takes mean and biased variance as two workgroup reductions over the
 // registers (two-pass, no cancellation), writes LDS and ends with a barrier.
 // K float4 per thread covers d <= 4 * NT * K.
-template <typename T, int NT, int K = (16384 / 4 + NT - 1) / NT>
+template <typename T, int NT, int K = (16384 / 4 + NT - 1) / NT, bool LN = false>
 struct StageX {
-  f32x4 v[K], gv[K], bv[K];
+  f32x4 v[K], gv[LN ? K : 1], bv[LN ? K : 1];
   __device__ __forceinline__ void load(const float* __restrict__ x, int d, const float* __restrict__ g,
                                        const float* __restrict__ b) {
     const int n4 = d >> 2;
-    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int k = 0; k < K; ++k) {
-      const int i = threadIdx.x + k * NT;
-      v[k] = i < n4 ? *reinterpret_cast<const f32x4*>(x + 4 * i) : z;
-      gv[k] = (g != nullptr && i < n4) ? *reinterpret_cast<const f32x4*>(g + 4 * i) : z;
-      bv[k] = (b != nullptr && i < n4) ? *reinterpret_cast<const f32x4*>(b + 4 * i) : z;
+    for (int k = 0; k < K; ++k)
+      v[k] = *reinterpret_cast<const f32x4*>(x + 4 * min((int)threadIdx.x + k * NT, n4 - 1));
+    if constexpr (LN) {
+      const float* bp = b != nullptr ? b : g;   // a missing beta reads gamma, unused
+#pragma unroll
+      for (int k = 0; k < K; ++k)
+        gv[k] = *reinterpret_cast<const f32x4*>(g + 4 * min((int)threadIdx.x + k * NT, n4 - 1));
+#pragma unroll
+      for (int k = 0; k < K; ++k)
+        bv[k] = *reinterpret_cast<const f32x4*>(bp + 4 * min((int)threadIdx.x + k * NT, n4 - 1));
     }
   }
-  __device__ __forceinline__ void finish(int d, bool ln, float eps, float* xs, float* red) {
+  __device__ __forceinline__ void finish(int d, bool has_b, float eps, float* xs, float* red) {
     const int n4 = d >> 2;
-    if (!ln) {
+    // Surplus lanes (index clamped to n4 - 1) hold the last chunk's values and store
+    // them to the same place as its own lane, so the stores need no predicate either.
+    if constexpr (!LN) {
 #pragma unroll
       for (int k = 0; k < K; ++k) {
-        const int i = threadIdx.x + k * NT;
-        if (i < n4) *reinterpret_cast<f32x4*>(xs + xs_index<T>(4 * i, d)) = v[k];
+        const int i = min((int)threadIdx.x + k * NT, n4 - 1);
+        *reinterpret_cast<f32x4*>(xs + xs_index<T>(4 * i, d)) = v[k];
       }
       __syncthreads();
-      return;
-    }
-    float s = 0.f;
+    } else {
+      float s = 0.f;
 #pragma unroll
-    for (int k = 0; k < K; ++k) s += (v[k][0] + v[k][1]) + (v[k][2] + v[k][3]);
-    const float mean = block_sum<NT>(s, red) / (float)d;
-    float q = 0.f;
+      for (int k = 0; k < K; ++k)
+        if (threadIdx.x + k * NT < n4) s += (v[k][0] + v[k][1]) + (v[k][2] + v[k][3]);
+      const float mean = block_sum<NT>(s, red) / (float)d;
+      float q = 0.f;
 #pragma unroll
-    for (int k = 0; k < K; ++k) {
-      if (threadIdx.x + k * NT < n4) {
-        const float a0 = v[k][0] - mean, a1 = v[k][1] - mean, a2 = v[k][2] - mean, a3 = v[k][3] - mean;
-        q += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
+      for (int k = 0; k < K; ++k) {
+        if (threadIdx.x + k * NT < n4) {
+          const float a0 = v[k][0] - mean, a1 = v[k][1] - mean, a2 = v[k][2] - mean, a3 = v[k][3] - mean;
+          q += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
+        }
       }
-    }
-    const float rstd = 1.0f / sqrtf(block_sum<NT>(q, red) / (float)d + eps);
+      const float rstd = 1.0f / sqrtf(block_sum<NT>(q, red) / (float)d + eps);
+      const float bm = has_b ? 1.f : 0.f;
 #pragma unroll
-    for (int k = 0; k < K; ++k) {
-      const int i = threadIdx.x + k * NT;
-      if (i < n4) {
+      for (int k = 0; k < K; ++k) {
+        const int i = min((int)threadIdx.x + k * NT, n4 - 1);
         f32x4 o;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = (v[k][e] - mean) * rstd * gv[k][e] + bv[k][e];
+        for (int e = 0; e < 4; ++e) o[e] = (v[k][e] - mean) * rstd * gv[k][e] + bm * bv[k][e];
         *reinterpret_cast<f32x4*>(xs + xs_index<T>(4 * i, d)) = o;
       }
+      __syncthreads();
     }
-    __syncthreads();
   }
 };
 
+// Stage a short vector x[d] (16-byte aligned, d % 4 == 0) into LDS as is, one
+// predicated float4 per thread and step, then a barrier.
 template <typename T, int NT>
-__device__ void stage_x(const float* __restrict__ x, int d, const float* __restrict__ g,
-                        const float* __restrict__ b, float eps, float* xs, float* red) {
-  StageX<T, NT> st;
-  st.load(x, d, g, b);
-  st.finish(d, g != nullptr, eps, xs, red);
+__device__ void stage_x(const float* __restrict__ x, int d, float* xs) {
+  for (int i = threadIdx.x; i < (d >> 2); i += NT)
+    *reinterpret_cast<f32x4*>(xs + xs_index<T>(4 * i, d)) = *reinterpret_cast<const f32x4*>(x + 4 * i);
+  __syncthreads();
 }
 
 // Order-preserving key of a float: a > b  <=>  key(a) > key(b); -0 maps to +0.
@@ -290,7 +299,7 @@ hipError_t launch_pred_scores(int wtype, const PredScoreArgs& a, hipStream_t st)
 // Gathered row-dot for Q/K/V of the selected heads (B = 1).
 struct QkvArgs {
   int d, H, dh, cap, pos, n_heads;
-  const float* x; const float* g; const float* be; float eps;    // LN1 (g NULL: none)
+  const float* x;                   // input, already layer-normalised where the block asks for it
   const void* Wq; const void* Wk; const void* Wv;
   const float* bq; const float* bk; const float* bv;
   void* K; void* V;                 // [H][cap][dh] of this sequence

@@ -10,7 +10,7 @@
 
 namespace dv {
 
-template <typename T, int NW, int U, int KX>
+template <typename T, int NW, int U, int KX, bool LN>
 __global__ void __launch_bounds__(NW * 64) k_fc1(Fc1Args a) {
   extern __shared__ float smem[];
   float* xs = smem;
@@ -19,13 +19,27 @@ __global__ void __launch_bounds__(NW * 64) k_fc1(Fc1Args a) {
   auto row_ptr = [&](int s) {
     return static_cast<const T*>(a.W1T) + (size_t)min(max(a.set[s], 0), a.n - 1) * a.d;
   };
+  // The epilogue's bias reads: the neuron index of row r0 + tid is read first of all
+  // loads (it is not waited for until the end), its bias once the stream is done.
+  const int r0 = (int)((long)blockIdx.x * a.k / gridDim.x), r1 = (int)((long)(blockIdx.x + 1) * a.k / gridDim.x);
+  const bool mine = (int)threadIdx.x < r1 - r0;
+  // (with no rows the set may be NULL: a valid word of the input is read instead)
+  const int32_t* sp = a.k > 0 ? a.set + min(r0 + (int)threadIdx.x, a.k - 1) : reinterpret_cast<const int32_t*>(a.x);
+  const int sraw = *sp;   // clamped at use
+  float bias = 0.f;
+  auto tail = [&]() {
+    if (mine && a.b1) bias = a.b1[min(max(sraw, 0), a.n - 1)];
+  };
   auto epi = [&](int s, float v) {
-    const int i = min(max(a.set[s], 0), a.n - 1);
-    if (a.b1) v += a.b1[i];
+    if (s - r0 == (int)threadIdx.x) {
+      v += bias;
+    } else if (a.b1) {
+      v += a.b1[min(max(a.set[s], 0), a.n - 1)];
+    }
     a.h[s] = v > 0.f ? v : 0.f;
   };
-  rowdot_flat<T, NW, U, false, KX>(row_ptr, epi, a.k, a.d, a.x, a.g, a.be, a.eps, xs, red, part, nullptr, blockIdx.x,
-                        gridDim.x);
+  rowdot_flat<T, NW, U, false, KX, LN>(row_ptr, epi, a.k, a.d, a.x, a.g, a.be, a.eps, xs, red, part, nullptr, blockIdx.x,
+                                   gridDim.x, tail);
 }
 
 template <typename T, int KX>
@@ -34,7 +48,10 @@ static hipError_t launch_fc1_t(const Fc1Args& a, hipStream_t st) {
   constexpr int NW = 16, U = KX >= 4 ? 8 : (KX == 3 ? 12 : 16);
   const int blocks = max(1, min(a.k, device_cu_count()));
   const size_t lds = (size_t)(a.d + NW + rowdot_flat_part(a.k, blocks, NW)) * sizeof(float);
-  hipLaunchKernelGGL((k_fc1<T, NW, U, KX>), dim3(blocks), dim3(NW * 64), lds, st, a);
+  if (a.g != nullptr)
+    hipLaunchKernelGGL((k_fc1<T, NW, U, KX, true>), dim3(blocks), dim3(NW * 64), lds, st, a);
+  else
+    hipLaunchKernelGGL((k_fc1<T, NW, U, KX, false>), dim3(blocks), dim3(NW * 64), lds, st, a);
   return hipGetLastError();
 }
 

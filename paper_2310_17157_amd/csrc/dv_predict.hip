@@ -10,7 +10,7 @@ namespace dv {
 // ----------------------------------------------------------- hidden layer
 // h[b][j] = x-hat[b] . AT[j] for the rows of up to two predictors; one workgroup per
 // CU takes a contiguous range of rows whose loads its wavefronts split evenly.
-template <typename T, int NW, int U, int KX>
+template <typename T, int NW, int U, int KX, bool LN>
 __global__ void __launch_bounds__(NW * 64) k_pred_hidden(PredHidArgs a) {
   extern __shared__ float smem[];
   float* xs = smem;
@@ -27,7 +27,7 @@ __global__ void __launch_bounds__(NW * 64) k_pred_hidden(PredHidArgs a) {
     else
       a.hid1[(size_t)b * a.r1 + row - a.r0] = v;
   };
-  rowdot_flat<T, NW, U, false, KX>(row_ptr, epi, a.r0 + a.r1, a.d, a.x + (size_t)b * a.d, a.g, a.be, a.eps, xs, red, part,
+  rowdot_flat<T, NW, U, false, KX, LN>(row_ptr, epi, a.r0 + a.r1, a.d, a.x + (size_t)b * a.d, a.g, a.be, a.eps, xs, red, part,
                         a.xhat_out ? a.xhat_out + (size_t)b * a.d : nullptr, blockIdx.x, gridDim.x);
 }
 
@@ -38,7 +38,10 @@ static hipError_t launch_pred_hidden_t(const PredHidArgs& a, hipStream_t st) {
   const int nrows = a.r0 + a.r1;
   const dim3 grid(max(1, min(nrows, device_cu_count())), a.B);
   const size_t lds = (size_t)(a.d + NW + rowdot_flat_part(nrows, grid.x, NW)) * sizeof(float);
-  hipLaunchKernelGGL((k_pred_hidden<T, NW, U, KX>), grid, dim3(NW * 64), lds, st, a);
+  if (a.g != nullptr)
+    hipLaunchKernelGGL((k_pred_hidden<T, NW, U, KX, true>), grid, dim3(NW * 64), lds, st, a);
+  else
+    hipLaunchKernelGGL((k_pred_hidden<T, NW, U, KX, false>), grid, dim3(NW * 64), lds, st, a);
   return hipGetLastError();
 }
 
@@ -83,7 +86,7 @@ __device__ __forceinline__ void head_scores_select(const PredScoreArgs& a, float
       for (int h = 0; h < 2; ++h) w[rb][h] = ld_stream(base + row * rowb + (size_t)min(h * 64 + lane, nch - 1) * 16);
     }
     if (!staged) {
-      stage_x<T, NT>(a.hid0, a.r0, nullptr, nullptr, 0.f, xs0, nullptr);
+      stage_x<T, NT>(a.hid0, a.r0, xs0);
       staged = true;
     }
 #pragma unroll
@@ -102,7 +105,7 @@ __device__ __forceinline__ void head_scores_select(const PredScoreArgs& a, float
       }
     }
   }
-  if (!staged) stage_x<T, NT>(a.hid0, a.r0, nullptr, nullptr, 0.f, xs0, nullptr);   // (no rows: keep barriers)
+  if (!staged) stage_x<T, NT>(a.hid0, a.r0, xs0);   // (no rows: keep barriers)
   uint32_t* keys = reinterpret_cast<uint32_t*>(hsc + a.n0);
   int* tmp = reinterpret_cast<int*>(keys + a.n0);
   int32_t* set = tmp + a.n0;
@@ -128,8 +131,8 @@ __global__ void __launch_bounds__(NW * 64) k_pred_scores(PredScoreArgs a) {
     head_scores_select<T, NW, 6>(a, xs0, xs1 + ((a.r1 + 3) & ~3));
     return;
   }
-  stage_x<T, NT>(a.hid0 + (size_t)b * a.r0, a.r0, nullptr, nullptr, 0.f, xs0, nullptr);
-  if (a.n1 > 0) stage_x<T, NT>(a.hid1 + (size_t)b * a.r1, a.r1, nullptr, nullptr, 0.f, xs1, nullptr);
+  stage_x<T, NT>(a.hid0 + (size_t)b * a.r0, a.r0, xs0);
+  if (a.n1 > 0) stage_x<T, NT>(a.hid1 + (size_t)b * a.r1, a.r1, xs1);
   const int nrows = a.n0 + a.n1;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int grp = lane / G, gl = lane % G;

@@ -7,26 +7,38 @@
 
 namespace dv {
 
+// Weight loads per wavefront issued before the input is staged.
+constexpr int kRowdotPre = 4;
+
 // rowdot_flat: workgroup wg of G takes the contiguous rows [wg*R/G, (wg+1)*R/G), and
 // its NW wavefronts split that range's load slots evenly across row boundaries (a
 // slot is one wavefront load of 64 lanes x 16 bytes; a row of nch chunks is
 // ipr = ceil(nch / 64) slots). Every wavefront thus has the same number of loads
-// whatever the row count, all of them issued early: the first U right behind the
-// prologue's input reads and, with PIPE, each next U before the current U are consumed (from two alternating
+// whatever the row count, all of them issued early: the first batch of U around the
+// prologue (kRowdotPre behind the input reads, the rest once the input is staged) and,
+// with PIPE, each next U before the current U are consumed (from two alternating
 // register sets, so that no wait is ever needed just to move data; surplus loads past
-// the end are clamped to the last slot and discarded). A wavefront reduces its partial sum of a
-// row when it leaves the row and records it in LDS (part[wave * mr + k] for its k-th
+// the end are clamped to the last slot and discarded). A wavefront reduces its partial
+// sum of a row when it leaves the row and records it in LDS (part[wave * mr + k] for its k-th
 // row, mr = ceil(R/G) + 1); after a barrier one thread per row adds the records of the
 // wavefronts that covered it, in wavefront order (bitwise reproducible), and calls
 // epi(row, value). xhat_out (optional) receives the staged input from workgroup 0.
-// KX: float4 of the input per thread (d <= 4 * 64 * NW * KX).
-template <typename T, int NW, int U, bool PIPE, int KX, class RowPtr, class Epi>
+// KX: float4 of the input per thread (d <= 4 * 64 * NW * KX); LN: layer norm of the
+// input with gamma g (non-NULL) and beta be (NULL: 0). tail() is called by
+// every thread once its wavefront has streamed all its loads, before the barrier that
+// precedes epi (a place to issue the epilogue's own reads).
+struct NoTail {
+  __device__ void operator()() const {}
+};
+template <typename T, int NW, int U, bool PIPE, int KX, bool LN, class RowPtr, class Epi, class Tail = NoTail>
 __device__ __forceinline__ void rowdot_flat(RowPtr row_ptr, Epi epi, int nrows, int d, const float* x,
                                             const float* g, const float* be, float eps, float* xs, float* red,
-                                            float* part, float* xhat_out, int wg, int G) {
+                                            float* part, float* xhat_out, int wg, int G, Tail tail = Tail()) {
   constexpr int NT = NW * 64;
   constexpr int E = Chunk<T>::E;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  // wave-uniform: row pointers and slot bounds live in scalar registers, so that a
+  // row change costs a scalar load (its own counter), never a wait on the stream
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int r0 = (int)((long)wg * nrows / G), r1 = (int)((long)(wg + 1) * nrows / G);
   const int nch = d / E, ipr = (nch + 63) >> 6;
   const int slots = (r1 - r0) * ipr;
@@ -39,8 +51,9 @@ __device__ __forceinline__ void rowdot_flat(RowPtr row_ptr, Epi epi, int nrows, 
   // stream enters a new row, not per load.
   int lrow = -1;
   const char* lptr = nullptr;
-  auto load = [&](u32x4 (&w)[U], int sb) {
-    const int sc0 = min(sb, s1 - 1);
+  // loads u in [u0, u1) of the batch of U slots starting at sb (u0, u1 compile-time)
+  auto load_part = [&](u32x4 (&w)[U], int sb, int u0, int u1) {
+    const int sc0 = min(sb + u0, s1 - 1);
     int rr = sc0 / ipr, j = sc0 - rr * ipr;
     if (rr != lrow) {
       lrow = rr;
@@ -48,7 +61,8 @@ __device__ __forceinline__ void rowdot_flat(RowPtr row_ptr, Epi epi, int nrows, 
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      if (u > 0 && sb + u < s1) {
+      if (u < u0 || u >= u1) continue;
+      if (u > u0 && sb + u < s1) {
         if (++j == ipr) {
           j = 0;
           ++rr;
@@ -60,6 +74,7 @@ __device__ __forceinline__ void rowdot_flat(RowPtr row_ptr, Epi epi, int nrows, 
       w[u] = ld_stream(lptr + (size_t)c * 16);
     }
   };
+  auto load = [&](u32x4 (&w)[U], int sb) { load_part(w, sb, 0, U); };
   int cur = active ? s0 / ipr : 0;        // relative row being accumulated
   const int first = cur;
   float acc0 = 0.f, acc1 = 0.f;
@@ -89,12 +104,16 @@ __device__ __forceinline__ void rowdot_flat(RowPtr row_ptr, Epi epi, int nrows, 
     }
   };
 
-  // input reads first, weight reads behind them: the prologue waits for the input only
-  StageX<T, NT, KX> st;
+  // Input reads first and only PRE weight reads behind them; the rest of the first
+  // batch follows once the input is staged, so that the staging reads do not queue
+  // behind a full batch from every wavefront of the grid.
+  constexpr int PRE = kRowdotPre < U ? kRowdotPre : U;
+  StageX<T, NT, KX, LN> st;
   st.load(x, d, g, be);
   u32x4 wa[U];
-  if (active) load(wa, s0);
-  st.finish(d, g != nullptr, eps, xs, red);
+  if (PRE > 0 && active) load_part(wa, s0, 0, PRE);
+  st.finish(d, be != nullptr, eps, xs, red);
+  if (PRE < U && active) load_part(wa, s0, PRE, U);
   if (xhat_out != nullptr && wg == 0)
     for (int e = threadIdx.x; e < d; e += NT) xhat_out[e] = xs[xs_index<T>(e, d)];
   if (active) {
@@ -122,6 +141,7 @@ __device__ __forceinline__ void rowdot_flat(RowPtr row_ptr, Epi epi, int nrows, 
     }
     flush();
   }
+  tail();
   __syncthreads();
   for (int rr = threadIdx.x; rr < r1 - r0; rr += NT) {
     const int wa0 = (rr * ipr) / tw, wb0 = min(((rr + 1) * ipr - 1) / tw, NW - 1);
