@@ -117,8 +117,14 @@ __device__ __forceinline__ void head_scores_select(const PredScoreArgs& a, float
   }
 }
 
-template <typename T, int NW, int G, int RU>
-__global__ void __launch_bounds__(NW * 64) k_pred_scores(PredScoreArgs a) {
+// The grid is sized to stay resident (two workgroups per CU); workgroup wg of G takes
+// an even contiguous share of the rows and its wavefronts split that share evenly.
+// A wavefront works in groups of RU rows per lane group (GPW = 64 / G groups of G
+// lanes), RU large enough that one group is usually all of its rows; every load of a
+// group (NR rounds of G chunks per row, row and chunk clamped, surplus masked where
+// summed) is issued before the group is used.
+template <typename T, int NW, int G, int RU, int NR>
+__global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2 * NW / 4))) k_pred_scores(PredScoreArgs a) {
   extern __shared__ float smem[];
   constexpr int NT = NW * 64;
   constexpr int E = Chunk<T>::E;
@@ -134,57 +140,57 @@ __global__ void __launch_bounds__(NW * 64) k_pred_scores(PredScoreArgs a) {
   stage_x<T, NT>(a.hid0 + (size_t)b * a.r0, a.r0, xs0);
   if (a.n1 > 0) stage_x<T, NT>(a.hid1 + (size_t)b * a.r1, a.r1, xs1);
   const int nrows = a.n0 + a.n1;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int grp = lane / G, gl = lane % G;
   constexpr int GPW = 64 / G;          // row groups per wavefront
-  constexpr int RPW = GPW * RU;        // rows per wavefront iteration
-  const int row_end = nrows;
-  const int bx = (int)blockIdx.x - (hosted ? 1 : 0);
-  const int first = (hosted ? a.n0 : 0) + (bx * NW + wave) * RPW;
-  const int stride = ((int)gridDim.x - (hosted ? 1 : 0)) * NW * RPW;
-  for (int base = first; base < row_end; base += stride) {
-    const char* rp[RU];
-    const float* xsu[RU];
-    int ru[RU], nch[RU];
-    float acc[RU];
-    int cmax = 0;
+  constexpr int RPG = GPW * RU;        // rows per wavefront group
+  const int Gw = (int)gridDim.x - (hosted ? 1 : 0), wg = (int)blockIdx.x - (hosted ? 1 : 0);
+  const int rb = hosted ? a.n0 : 0, R = nrows - rb;
+  const int w0 = rb + (int)((long)wg * R / Gw), w1 = rb + (int)((long)(wg + 1) * R / Gw);
+  const int v0 = w0 + (w1 - w0) * wave / NW, v1 = w0 + (w1 - w0) * (wave + 1) / NW;   // this wavefront's rows
+  const int ng = (v1 - v0 + RPG - 1) / RPG;
+  if (ng == 0) return;
+  const int nch0 = a.r0 / E, nch1 = a.r1 / E;
+  const int cmax = max(nch0, a.n1 > 0 ? nch1 : 0);
+
+  auto row_of = [&](int k, int u) { return v0 + k * RPG + u * GPW + grp; };
+  for (int c0 = 0; c0 < cmax; c0 += NR * G) {
+    auto load = [&](u32x4 (&w)[RU][NR], int k) {
 #pragma unroll
-    for (int u = 0; u < RU; ++u) {
-      const int row = base + u * GPW + grp;
-      acc[u] = 0.f;
-      if (row >= row_end) {
-        rp[u] = nullptr; xsu[u] = xs0; ru[u] = a.r0; nch[u] = 0;
-      } else if (row < a.n0) {
-        rp[u] = reinterpret_cast<const char*>(static_cast<const T*>(a.BT0) + (size_t)row * a.r0);
-        xsu[u] = xs0; ru[u] = a.r0; nch[u] = a.r0 / E;
-      } else if (row < nrows) {
-        rp[u] = reinterpret_cast<const char*>(static_cast<const T*>(a.BT1) + (size_t)(row - a.n0) * a.r1);
-        xsu[u] = xs1; ru[u] = a.r1; nch[u] = a.r1 / E;
-      } else {
-        rp[u] = nullptr; xsu[u] = xs0; ru[u] = a.r0; nch[u] = 0;
+      for (int u = 0; u < RU; ++u) {
+        const int row = min(row_of(k, u), v1 - 1);
+        const bool sec = row >= a.n0;
+        const char* rp = sec ? reinterpret_cast<const char*>(static_cast<const T*>(a.BT1) + (size_t)(row - a.n0) * a.r1)
+                             : reinterpret_cast<const char*>(static_cast<const T*>(a.BT0) + (size_t)row * a.r0);
+        const int nch = sec ? nch1 : nch0;
+#pragma unroll
+        for (int h = 0; h < NR; ++h) w[u][h] = ld_stream(rp + (size_t)min(c0 + h * G + gl, nch - 1) * 16);
       }
-      cmax = max(cmax, nch[u]);
-    }
-    for (int c = gl; c < cmax; c += G) {
-      u32x4 w[RU];
+    };
+    auto consume = [&](const u32x4 (&w)[RU][NR], int k) {
 #pragma unroll
-      for (int u = 0; u < RU; ++u) w[u] = c < nch[u] ? ld_stream(rp[u] + (size_t)c * 16) : u32x4{0u, 0u, 0u, 0u};
+      for (int u = 0; u < RU; ++u) {
+        const int row = row_of(k, u);
+        const bool sec = row >= a.n0;
+        const int nch = sec ? nch1 : nch0;
+        float acc = 0.f;
 #pragma unroll
-      for (int u = 0; u < RU; ++u)
-        if (c < nch[u]) acc[u] = dot_chunk<T>(w[u], xsu[u], ru[u], c, acc[u]);
-    }
+        for (int h = 0; h < NR; ++h) {
+          const int c = c0 + h * G + gl;
+          if (c < nch) acc = sec ? dot_chunk<T>(w[u][h], xs1, a.r1, c, acc) : dot_chunk<T>(w[u][h], xs0, a.r0, c, acc);
+        }
 #pragma unroll
-    for (int u = 0; u < RU; ++u) {
-      float v = acc[u];
-#pragma unroll
-      for (int o = G / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-      const int row = base + u * GPW + grp;
-      if (gl == 0 && row < row_end) {
-        if (row < a.n0)
-          a.s0[(size_t)b * a.n0 + row] = v;
-        else
-          a.s1[(size_t)b * a.n1 + row - a.n0] = v;
+        for (int o = G / 2; o > 0; o >>= 1) acc += __shfl_xor(acc, o, kWave);
+        if (gl == 0 && row < v1) {
+          float* out = sec ? a.s1 + (size_t)b * a.n1 + row - a.n0 : a.s0 + (size_t)b * a.n0 + row;
+          *out = c0 == 0 ? acc : *out + acc;   // rows longer than NR * G chunks: one round per c0
+        }
       }
+    };
+    for (int k = 0; k < ng; ++k) {
+      u32x4 w[RU][NR];
+      load(w, k);
+      consume(w, k);
     }
   }
 }
@@ -197,18 +203,16 @@ static hipError_t launch_scores_t(const PredScoreArgs& a, hipStream_t st) {
   const int nrows = a.n0 + a.n1;
   const int hosted = a.sel_k0 > 0 ? 1 : 0;
   const size_t lds = (size_t)(((a.r0 + 3) & ~3) + ((a.r1 + 3) & ~3) + 4 * a.n0 * hosted + 4) * sizeof(float);
+  // two workgroups per CU (the head-selection workgroup included): all resident at once
+  const int blocks = max(1, min(2 * device_cu_count() - hosted, nrows));
+  const dim3 grid(blocks + hosted, a.B);
   if (nch > 32) {
-    constexpr int G = 64, RU = 8, RPB = NW * (64 / G) * RU;
-    dim3 grid(min((nrows + RPB - 1) / RPB, 4096) + hosted, a.B);
-    hipLaunchKernelGGL((k_pred_scores<T, NW, G, RU>), grid, dim3(NW * 64), lds, st, a);
+    // 64 lanes per row, all chunks of a row up to 128 (r <= 1024 fp16) in one round
+    hipLaunchKernelGGL((k_pred_scores<T, NW, 64, 13, 2>), grid, dim3(NW * 64), lds, st, a);
   } else if (nch > 16) {
-    constexpr int G = 32, RU = 4, RPB = NW * (64 / G) * RU;
-    dim3 grid(min((nrows + RPB - 1) / RPB, 4096) + hosted, a.B);
-    hipLaunchKernelGGL((k_pred_scores<T, NW, G, RU>), grid, dim3(NW * 64), lds, st, a);
+    hipLaunchKernelGGL((k_pred_scores<T, NW, 32, 13, 1>), grid, dim3(NW * 64), lds, st, a);
   } else {
-    constexpr int G = 16, RU = 4, RPB = NW * (64 / G) * RU;
-    dim3 grid(min((nrows + RPB - 1) / RPB, 4096) + hosted, a.B);
-    hipLaunchKernelGGL((k_pred_scores<T, NW, G, RU>), grid, dim3(NW * 64), lds, st, a);
+    hipLaunchKernelGGL((k_pred_scores<T, NW, 16, 13, 1>), grid, dim3(NW * 64), lds, st, a);
   }
   return hipGetLastError();
 }
