@@ -615,9 +615,11 @@ static constexpr int kMcNW = 8, kMcU = 1;
 static constexpr bool kMcWide = true;
 
 int mcols_split(int d, int nmax) {
+  // one workgroup per CU: more splits only add partial-sum traffic (each split writes a
+  // full B x d partial) and, past the CU count, a second round of workgroups (measured at
+  // d = 12288: 10 splits 57 + 5 us out-proj, 32 splits 71 + 9 us)
   const int tiles = kMcWide ? (d + 64 * kMcNW - 1) / (64 * kMcNW) : (d + 63) / 64;
-  const int target = 4 * device_cu_count();
-  int s = (target + tiles - 1) / tiles;
+  int s = max(1, device_cu_count() / tiles);
   const int q = (nmax + 31) / 32;                  // k-steps available
   s = max(1, min(s, max(1, kMcWide ? q / 2 : q / (2 * kMcNW))));
   return min(s, 32);
@@ -640,6 +642,22 @@ hipError_t launch_mcols(int NB, const McolsArgs& a, hipStream_t st) {
 
 // --------------------------------------------------------------- finishers
 // sum_{s < S} P[s * stride + e] in split order, with up to 8 loads in flight.
+// Four consecutive elements summed over the splits in split order (the same order, so
+// the same bits, as sum_splits per element); every split's load is issued before the
+// first add, unpredicated (split index clamped, surplus not added).
+__device__ __forceinline__ f32x4 sum_splits4(const float* __restrict__ P, int S, size_t stride, size_t e) {
+  f32x4 v = {0.f, 0.f, 0.f, 0.f};
+  for (int s0 = 0; s0 < S; s0 += 8) {
+    f32x4 t[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) t[u] = *reinterpret_cast<const f32x4*>(P + (size_t)min(s0 + u, S - 1) * stride + e);
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (s0 + u < S) v += t[u];
+  }
+  return v;
+}
+
 __device__ __forceinline__ float sum_splits(const float* __restrict__ P, int S, size_t stride, size_t e) {
   float v = 0.f;
   for (int s0 = 0; s0 < S; s0 += 8) {
@@ -656,25 +674,33 @@ __device__ __forceinline__ float sum_splits(const float* __restrict__ P, int S, 
 // with a mask, only where bit b of mask[u] is set); zero elsewhere up to a multiple
 // of 64 rows. One workgroup per 64 rows.
 template <int NB>
-__global__ void __launch_bounds__(256) k_fc1_finish(Fc1FinishArgs a) {
+__global__ void __launch_bounds__(16 * NB) k_fc1_finish(Fc1FinishArgs a) {
+  // one thread per four tokens of one of the workgroup's 64 rows: a single round trip
   __shared__ float t[64][NB + 1];
   const int n = a.list_count ? min(*a.list_count, a.list_max) : a.list_max;
   const int u0 = blockIdx.x * 64;
   if (u0 >= ((n + 63) & ~63)) return;
-  for (int e = threadIdx.x; e < 64 * NB; e += 256) {
-    const int ul = e / NB, b = e - ul * NB;
+  {
+    const int ul = threadIdx.x / (NB / 4), b0 = (threadIdx.x - ul * (NB / 4)) * 4;
     const int u = u0 + ul;
-    float v = 0.f;
-    if (u < n && b < a.B) {
-      v = sum_splits(a.P, a.S, (size_t)a.nrows_pad * NB, (size_t)u * NB + b);
-      if (a.b1) v += a.b1[min(max(a.list[u], 0), a.list_range - 1)];
-      v = v > 0.f ? v : 0.f;
-      if (a.mask && !((a.mask[u] >> b) & 1u)) v = 0.f;
+    f32x4 v = {0.f, 0.f, 0.f, 0.f};
+    if (u < n) {
+      v = sum_splits4(a.P, a.S, (size_t)a.nrows_pad * NB, (size_t)u * NB + b0);
+      const float bias = a.b1 ? a.b1[min(max(a.list[u], 0), a.list_range - 1)] : 0.f;
+      const uint32_t mk = a.mask ? a.mask[u] : 0xffffffffu;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float x = v[i] + bias;
+        x = x > 0.f ? x : 0.f;
+        if (b0 + i >= a.B || !((mk >> (b0 + i)) & 1u)) x = 0.f;
+        v[i] = x;
+      }
     }
-    t[ul][b] = v;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) t[ul][b0 + i] = v[i];
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < 64 * NB; e += 256) {
+  for (int e = threadIdx.x; e < 64 * NB; e += 16 * NB) {
     const int b = e >> 6, ul = e & 63;
     a.C[(size_t)b * a.ldc + u0 + ul] = (_Float16)t[ul][b];
   }
@@ -683,29 +709,28 @@ __global__ void __launch_bounds__(256) k_fc1_finish(Fc1FinishArgs a) {
 hipError_t launch_fc1_finish(int NB, const Fc1FinishArgs& a, hipStream_t st) {
   const int blocks = max(1, (a.list_max + 63) / 64);
   if (NB <= 16)
-    hipLaunchKernelGGL(k_fc1_finish<16>, dim3(blocks), dim3(256), 0, st, a);
+    hipLaunchKernelGGL(k_fc1_finish<16>, dim3(blocks), dim3(16 * 16), 0, st, a);
   else
-    hipLaunchKernelGGL(k_fc1_finish<32>, dim3(blocks), dim3(256), 0, st, a);
+    hipLaunchKernelGGL(k_fc1_finish<32>, dim3(blocks), dim3(16 * 32), 0, st, a);
   return hipGetLastError();
 }
 
-// Sum of k_mfma_cols partials: out[b][c] = sum_s P2[s][b][c] + bias[c] + resid[b][c].
+// Sum of k_mfma_cols partials: out[b][c] = sum_s P2[s][b][c] + bias[c] + resid[b][c];
+// one thread per four columns (d % 4 == 0), every split's load in flight at once.
 __global__ void __launch_bounds__(256) k_cols_finish(ColsFinishArgs a) {
   const long total = (long)a.B * a.d;
-  for (long e = (long)blockIdx.x * 256 + threadIdx.x; e < total; e += (long)gridDim.x * 256) {
-    const int c = (int)(e % a.d);
-    float v = sum_splits(a.P, a.S, (size_t)total, (size_t)e);
-    if (a.bias) v += a.bias[c];
-    if (a.resid) v += a.resid[e];
-    a.out[e] = v;
-  }
+  const long e = ((long)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (e >= total) return;
+  const int c = (int)(e % a.d);
+  f32x4 v = sum_splits4(a.P, a.S, (size_t)total, (size_t)e);
+  if (a.bias) v += *reinterpret_cast<const f32x4*>(a.bias + c);
+  if (a.resid) v += *reinterpret_cast<const f32x4*>(a.resid + e);
+  *reinterpret_cast<f32x4*>(a.out + e) = v;
 }
 
 hipError_t launch_cols_finish(const ColsFinishArgs& a, hipStream_t st) {
-  const long total = (long)a.B * a.d;
-  const long want = (total + 255) / 256, cap = 4L * device_cu_count();
-  const int blocks = (int)(want < cap ? want : cap);
-  hipLaunchKernelGGL(k_cols_finish, dim3(max(1, blocks)), dim3(256), 0, st, a);
+  const long quads = ((long)a.B * a.d / 4 + 255) / 256;
+  hipLaunchKernelGGL(k_cols_finish, dim3((unsigned)max(1L, quads)), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
@@ -739,7 +764,7 @@ hipError_t launch_sum_cast(int NB, const float* P, int S, int nrows_pad, int row
 // query goes to q[b][j][:] (m = 0) or the key/value to cache row pos[b] of head h
 // (m = 1, 2; round to nearest even).
 template <int NB, typename KT>
-__global__ void __launch_bounds__(256) k_qkv_finish(QkvFinishArgs a) {
+__global__ void __launch_bounds__(1024) k_qkv_finish(QkvFinishArgs a) {
   extern __shared__ float qsm[];                  // [dh][NB + 1]
   __shared__ int jsel[NB];
   const int p = blockIdx.x, m = blockIdx.y;
@@ -762,14 +787,16 @@ __global__ void __launch_bounds__(256) k_qkv_finish(QkvFinishArgs a) {
   }
   const size_t r0 = ((size_t)m * nu + p) * a.dh;
   const float* bias = m == 0 ? a.bq : (m == 1 ? a.bk : a.bv);
-  for (int e = threadIdx.x; e < a.dh * NB; e += 256) {
+  // one thread per four tokens of a row: every split's load in flight at once
+  for (int e = threadIdx.x * 4; e < a.dh * NB; e += 1024 * 4) {
     const int t = e / NB, b = e - t * NB;
-    float v = sum_splits(a.P, a.S, (size_t)a.nrows_pad * NB, (r0 + t) * NB + b);
-    if (bias) v += bias[(size_t)h * a.dh + t];
-    qsm[t * (NB + 1) + b] = v;
+    f32x4 v = sum_splits4(a.P, a.S, (size_t)a.nrows_pad * NB, (r0 + t) * NB + b);
+    const float bs = bias ? bias[(size_t)h * a.dh + t] : 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) qsm[t * (NB + 1) + b + i] = v[i] + bs;
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < a.dh * NB; e += 256) {
+  for (int e = threadIdx.x; e < a.dh * NB; e += 1024) {
     const int b = e / a.dh, t = e - b * a.dh;
     const int jj = jsel[b];
     if (jj < 0) continue;
@@ -787,11 +814,11 @@ hipError_t launch_qkv_finish(int NB, int kvtype, const QkvFinishArgs& a, hipStre
   dim3 grid(a.H, 3);
   const size_t lds = (size_t)a.dh * (NB + 1) * sizeof(float);
   if (NB <= 16) {
-    if (kvtype == DV_F16) hipLaunchKernelGGL((k_qkv_finish<16, _Float16>), grid, dim3(256), lds, st, a);
-    else hipLaunchKernelGGL((k_qkv_finish<16, float>), grid, dim3(256), lds, st, a);
+    if (kvtype == DV_F16) hipLaunchKernelGGL((k_qkv_finish<16, _Float16>), grid, dim3(1024), lds, st, a);
+    else hipLaunchKernelGGL((k_qkv_finish<16, float>), grid, dim3(1024), lds, st, a);
   } else {
-    if (kvtype == DV_F16) hipLaunchKernelGGL((k_qkv_finish<32, _Float16>), grid, dim3(256), lds, st, a);
-    else hipLaunchKernelGGL((k_qkv_finish<32, float>), grid, dim3(256), lds, st, a);
+    if (kvtype == DV_F16) hipLaunchKernelGGL((k_qkv_finish<32, _Float16>), grid, dim3(1024), lds, st, a);
+    else hipLaunchKernelGGL((k_qkv_finish<32, float>), grid, dim3(1024), lds, st, a);
   }
   return hipGetLastError();
 }
