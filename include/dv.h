@@ -182,6 +182,7 @@ dv_status dv_predict_heads(const dv_predictor *p, const float *x, int32_t B, int
  *                sequences; idx_per_seq == 1: idx[B][n_idx], one set per sequence.
  *   batch_mode   with per-sequence sets and B > 1: DV_MLP_UNION or DV_MLP_MASKED.
  * Each selected row of W1T and W2T is read from HBM once per call, whatever B is.
+ * Limits: B > 1 needs B <= 32, fp16 weights and n <= 131072 (else DV_ERR_UNSUPPORTED).
  */
 size_t dv_sparse_mlp_workspace_bytes(const dv_mlp *m, int32_t B, int32_t n_idx, int32_t idx_per_seq);
 dv_status dv_sparse_mlp(const dv_mlp *m, const float *x, int32_t B, const int32_t *idx,

@@ -143,7 +143,7 @@ static dv_status validate_sets(const int32_t* set, int B, int n, int range, int3
 }
 
 // The batched path: 2..kMaxBatch sequences, fp16 weights.
-static constexpr int kMaxUnionN = 262144;   // LDS bitmap of the union builder
+static constexpr int kMaxUnionN = 131072;   // the union builder marks n bytes in LDS
 static bool batch_ok(int B, int wtype) { return B <= kMaxBatch && wtype == DV_F16; }
 
 static dv_status enqueue_axpy(const char* label, int wtype, const AxpyArgs& ax, hipStream_t hs) {

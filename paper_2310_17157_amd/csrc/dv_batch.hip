@@ -39,114 +39,128 @@ __device__ __forceinline__ v4s_t ds_read_tr16(const _Float16* p) {
       (v4s_t __attribute__((address_space(3)))*)(const_cast<_Float16*>(p)));
 }
 
-// ------------------------------------------------------------------ union
-// Union of B ascending sets sets[b][0..k) in [0, n), in two launches over chunks of
-// kUnionChunk indices (one workgroup per chunk):
-//   k_union_bits   the chunk's bitmap (LDS atomics from each set's entries inside the
-//                  chunk, found by binary search) and its member count;
-//   k_union_write  the chunk's offset (sum of the counts before it), the members in
-//                  ascending order at U[offset + rank], the total in *count, and
-//                  optionally the membership bits mask[u] (bit b: U[u] is in set b).
-constexpr int kUnionChunk = 2048;
-constexpr int kUnionNT = 256;
-
-__device__ __forceinline__ int lower_bound_i32(const int32_t* __restrict__ v, int len, int key) {
-  int lo = 0, hi = len;
-  while (lo < hi) {
-    const int mid = (lo + hi) >> 1;
-    if (v[mid] < key) lo = mid + 1; else hi = mid;
+static int lds_budget() {
+  static int cached = 0;
+  if (cached == 0) {
+    int dev = 0, v = 0;
+    (void)hipGetDevice(&dev);
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || v <= 0) v = 65536;
+    cached = v;
   }
-  return lo;
+  return cached;
 }
 
-__global__ void __launch_bounds__(kUnionNT) k_union_bits(const int32_t* __restrict__ sets, int B, int k, int n,
-                                                         uint32_t* __restrict__ bits, int32_t* __restrict__ cnt) {
-  __shared__ uint32_t wb[kUnionChunk / 32];
-  __shared__ int red[kUnionNT / 64 + 1];
-  const int c = blockIdx.x, tid = threadIdx.x;
-  const int lo_i = c * kUnionChunk, hi_i = min(n, lo_i + kUnionChunk);
-  for (int w = tid; w < kUnionChunk / 32; w += kUnionNT) wb[w] = 0u;
-  __syncthreads();
-  // threads are spread over the sets: set b gets (kUnionNT / B) or more threads
-  for (int b = tid % B, r = tid / B, nr = (kUnionNT - tid % B + B - 1) / B; b < B; b += kUnionNT) {
-    const int32_t* sb = sets + (size_t)b * k;
-    const int e0 = lower_bound_i32(sb, k, lo_i), e1 = lower_bound_i32(sb, k, hi_i);
-    for (int e = e0 + r; e < e1; e += nr) {
-      const int i = sb[e] - lo_i;
-      if (i >= 0 && i < kUnionChunk) atomicOr(&wb[i >> 5], 1u << (i & 31));
+
+// ------------------------------------------------------------------ union
+// Union of B ascending sets sets[b][0..k) in [0, n) in one launch, one workgroup per
+// chunk of kUnionChunk indices. Every workgroup reads all B * k entries (they stay
+// in L2) and marks a byte per index below its chunk's end in LDS (plain stores, so
+// entries shared by many sets do not contend); the members below the chunk give
+// its offset, the marks inside it the ranks. U[offset + rank] = the members in
+// ascending order, *count = their number (last chunk), and optionally
+// mask[offset + rank] = the member's sets as bits (bit b: set b holds it), gathered
+// by LDS atomics on one word per index of the chunk.
+constexpr int kUnionChunk = 2048;
+constexpr int kUnionNT = 1024;
+static_assert(kUnionChunk == 2 * kUnionNT, "two indices of the chunk per thread");
+
+// Calls fn(e, v) for every entry e of sets[0..total) with value v. The entries are
+// read as aligned int4 with all of a thread's loads in flight (one round trip for up
+// to PER * 4 * kUnionNT entries; rounds of loads past the end are not issued). sets need only be 4-byte aligned: the quads start
+// at its 16-byte block, and a 16-byte aligned block never crosses a page, so the
+// words before the first entry and after the last are readable; they are skipped.
+template <class Fn>
+__device__ __forceinline__ void union_scan(const int32_t* __restrict__ sets, int total, Fn fn) {
+  constexpr int PER = 16;
+  if (total <= 0) return;
+  const int shift = (int)(((uintptr_t)sets & 15u) >> 2);
+  const int4* base = reinterpret_cast<const int4*>((uintptr_t)sets & ~(uintptr_t)15u);
+  const int n4 = (total + shift + 3) >> 2;
+  for (int q0 = 0; q0 < n4; q0 += PER * kUnionNT) {
+    const int nu = min(PER, (n4 - q0 + kUnionNT - 1) / kUnionNT);   // rounds of quads left (workgroup-uniform)
+    int4 v[PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u)
+      v[u] = u < nu ? base[min(q0 + u * kUnionNT + (int)threadIdx.x, n4 - 1)] : make_int4(0, 0, 0, 0);
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {   // quads of rounds not loaded have e >= total
+      const int e = 4 * (q0 + u * kUnionNT + (int)threadIdx.x) - shift;
+      if (e + 0 >= 0 && e + 0 < total) fn(e + 0, v[u].x);
+      if (e + 1 >= 0 && e + 1 < total) fn(e + 1, v[u].y);
+      if (e + 2 >= 0 && e + 2 < total) fn(e + 2, v[u].z);
+      if (e + 3 >= 0 && e + 3 < total) fn(e + 3, v[u].w);
     }
   }
-  __syncthreads();
-  int m = 0;
-  for (int w = tid; w < kUnionChunk / 32; w += kUnionNT) {
-    bits[(size_t)c * (kUnionChunk / 32) + w] = wb[w];
-    m += __popc(wb[w]);
-  }
-  int total = 0;
-  (void)block_excl_scan<kUnionNT>(m, red, &total);
-  if (tid == 0) cnt[c] = total;
 }
 
-__global__ void __launch_bounds__(kUnionNT) k_union_write(const int32_t* __restrict__ sets, int B, int k, int n,
-                                                          const uint32_t* __restrict__ bits,
-                                                          const int32_t* __restrict__ cnt, int nchunks,
-                                                          int32_t* __restrict__ U, int32_t* __restrict__ count,
-                                                          uint32_t* __restrict__ mask) {
-  __shared__ uint32_t wb[kUnionChunk / 32];
-  __shared__ int off[kUnionChunk / 32];
+// Sum of four 0/1 bytes.
+__device__ __forceinline__ int byte_flags(uint32_t w) { return (int)((w * 0x01010101u) >> 24); }
+
+// Dynamic LDS: marks [round_up(n, 16)] bytes, then (mask only) kUnionChunk words.
+template <bool MASK>
+__global__ void __launch_bounds__(kUnionNT) k_union(const int32_t* __restrict__ sets, int B, int k, int n,
+                                                    int32_t* __restrict__ U, int32_t* __restrict__ count,
+                                                    uint32_t* __restrict__ mask) {
+  extern __shared__ __attribute__((aligned(16))) uint32_t ush[];
   __shared__ int red[kUnionNT / 64 + 1];
-  const int c = blockIdx.x, tid = threadIdx.x;
-  const int lo_i = c * kUnionChunk;
-  // offset of this chunk: the counts of the chunks before it, summed in order
+  const int tid = threadIdx.x, c = blockIdx.x;
+  const int lo = c * kUnionChunk, hi = min(n, lo + kUnionChunk);
+  const int n16 = (n + 15) & ~15;
+  uint8_t* mk = reinterpret_cast<uint8_t*>(ush);
+  uint32_t* mw = ush + n16 / 4;
+  const int nq = ((hi + 15) & ~15) / 16;   // marks read below: [0, round_up(hi, 16))
+  for (int q = tid; q < nq; q += kUnionNT) reinterpret_cast<uint4*>(mk)[q] = make_uint4(0u, 0u, 0u, 0u);
+  if (MASK)
+    for (int i = tid; i < kUnionChunk; i += kUnionNT) mw[i] = 0u;
+  __syncthreads();
+  union_scan(sets, B * k, [&](int e, int v) {
+    if ((unsigned)v < (unsigned)hi) {
+      mk[v] = 1;
+      if (MASK && v >= lo) atomicOr(&mw[v - lo], 1u << (e / k));
+    }
+  });
+  __syncthreads();
+  // members before the chunk (lo is a multiple of 16)
   int part = 0;
-  for (int j = tid; j < c; j += kUnionNT) part += cnt[j];
+  for (int q = tid; q < lo / 16; q += kUnionNT) {
+    const uint4 w = reinterpret_cast<const uint4*>(mk)[q];
+    part += byte_flags(w.x) + byte_flags(w.y) + byte_flags(w.z) + byte_flags(w.w);
+  }
   int before = 0;
   (void)block_excl_scan<kUnionNT>(part, red, &before);
-  constexpr int NW = kUnionChunk / 32;
-  int pc = 0;
-  uint32_t wv = 0u;
-  if (tid < NW) {
-    wv = bits[(size_t)c * NW + tid];
-    pc = __popc(wv);
+  // thread t ranks indices lo + 2t and lo + 2t + 1
+  const int i0 = lo + 2 * tid;
+  const int f0 = i0 < hi ? mk[i0] : 0, f1 = i0 + 1 < hi ? mk[i0 + 1] : 0;
+  int in_chunk = 0;
+  const int r = before + block_excl_scan<kUnionNT>(f0 + f1, red, &in_chunk);
+  if (f0) {
+    U[r] = i0;
+    if (MASK) mask[r] = mw[i0 - lo];
   }
-  int mine = 0;
-  const int ex = block_excl_scan<kUnionNT>(pc, red, &mine);
-  if (tid < NW) {
-    wb[tid] = wv;
-    off[tid] = before + ex;
+  if (f1) {
+    U[r + f0] = i0 + 1;
+    if (MASK) mask[r + f0] = mw[i0 + 1 - lo];
   }
-  if (c == nchunks - 1 && tid == 0) *count = before + mine;
-  __syncthreads();
-  for (int i = tid; i < kUnionChunk && lo_i + i < n; i += kUnionNT) {
-    const uint32_t m = wb[i >> 5];
-    if ((m >> (i & 31)) & 1u) U[off[i >> 5] + __popc(m & ((1u << (i & 31)) - 1u))] = lo_i + i;
-  }
-  if (mask != nullptr) {
-    for (int r = tid; r < mine; r += kUnionNT) mask[before + r] = 0u;
-    __syncthreads();
-    const int hi_i = min(n, lo_i + kUnionChunk);
-    for (int b = tid % B, rr = tid / B, nr = (kUnionNT - tid % B + B - 1) / B; b < B; b += kUnionNT) {
-      const int32_t* sb = sets + (size_t)b * k;
-      const int e0 = lower_bound_i32(sb, k, lo_i), e1 = lower_bound_i32(sb, k, hi_i);
-      for (int e = e0 + rr; e < e1; e += nr) {
-        const int i = sb[e] - lo_i;
-        if (i >= 0 && i < kUnionChunk) {
-          const uint32_t m = wb[i >> 5];
-          atomicOr(&mask[off[i >> 5] + __popc(m & ((1u << (i & 31)) - 1u))], 1u << b);
-        }
-      }
-    }
-  }
+  if (c == (int)gridDim.x - 1 && tid == 0) *count = before + in_chunk;
 }
 
-int union_chunks(int n) { return (n + kUnionChunk - 1) / kUnionChunk; }
+size_t union_lds_bytes(int n) { return (size_t)((n + 15) & ~15) + (size_t)kUnionChunk * 4; }
 
 hipError_t launch_union(const int32_t* sets, int B, int k, int n, int32_t* U, int32_t* count, uint32_t* mask,
-                        uint32_t* bits, int32_t* chunk_counts, hipStream_t st) {
-  const int nc = union_chunks(n);
-  hipLaunchKernelGGL(k_union_bits, dim3(nc), dim3(kUnionNT), 0, st, sets, B, k, n, bits, chunk_counts);
-  hipLaunchKernelGGL(k_union_write, dim3(nc), dim3(kUnionNT), 0, st, sets, B, k, n, bits, chunk_counts, nc, U, count,
-                     mask);
+                        hipStream_t st) {
+  const int nc = (n + kUnionChunk - 1) / kUnionChunk;
+  const size_t lds = union_lds_bytes(n);
+  static bool attr[2] = {false, false};
+  const void* kern = mask != nullptr ? reinterpret_cast<const void*>(k_union<true>)
+                                     : reinterpret_cast<const void*>(k_union<false>);
+  if (lds > 65536 && !attr[mask != nullptr]) {
+    (void)hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds_budget());
+    attr[mask != nullptr] = true;
+  }
+  if (mask != nullptr)
+    hipLaunchKernelGGL(k_union<true>, dim3(nc), dim3(kUnionNT), lds, st, sets, B, k, n, U, count, mask);
+  else
+    hipLaunchKernelGGL(k_union<false>, dim3(nc), dim3(kUnionNT), lds, st, sets, B, k, n, U, count, mask);
   return hipGetLastError();
 }
 
@@ -364,17 +378,6 @@ __global__ void __launch_bounds__(NW * 64) k_mfma_rows(MrowsArgs a) {
       }
     }
   }
-}
-
-static int lds_budget() {
-  static int cached = 0;
-  if (cached == 0) {
-    int dev = 0, v = 0;
-    (void)hipGetDevice(&dev);
-    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || v <= 0) v = 65536;
-    cached = v;
-  }
-  return cached;
 }
 
 // K per split for k_mfma_rows: a multiple of 32 * kMrU halves whose staged slice of

@@ -23,7 +23,7 @@ int batch_nb(int B) { return B <= 16 ? 16 : 32; }
 
 // ---------------------------------------------------------------- MLP
 struct BMlp {
-  _Float16* X16; int32_t* U; int32_t* cnt; uint32_t* mask; uint32_t* ubits; int32_t* ucnt; float* P; _Float16* C;
+  _Float16* X16; int32_t* U; int32_t* cnt; uint32_t* mask; float* P; _Float16* C;
   float* P2;
   int Kpad, S, Ks, umax, nrows_pad, ldc, S2;
 };
@@ -40,8 +40,6 @@ static size_t bmlp_layout(int d, int n, int B, int n_idx, bool per_seq, Workspac
   o->U = w.take<int32_t>(per_seq ? (size_t)o->umax * 4 : 0);
   o->cnt = w.take<int32_t>(4);
   o->mask = w.take<uint32_t>(per_seq ? (size_t)o->umax * 4 : 0);
-  o->ubits = w.take<uint32_t>((size_t)union_chunks(n) * 64 * 4);
-  o->ucnt = w.take<int32_t>((size_t)union_chunks(n) * 4);
   o->P = w.take<float>((size_t)o->S * o->nrows_pad * NB * 4);
   o->C = w.take<_Float16>((size_t)NB * o->ldc * 2);
   o->P2 = w.take<float>((size_t)o->S2 * B * d * 4);
@@ -62,7 +60,7 @@ static dv_status bmlp_run(const dv_mlp* m, const BMlp& o, int B, const int32_t* 
   const int32_t* list_count = nullptr;
   int list_max = n_idx;
   if (per_seq) {
-    DV_LAUNCH("union", hs, launch_union(idx, B, n_idx, m->n, o.U, o.cnt, masked ? o.mask : nullptr, o.ubits, o.ucnt, hs));
+    DV_LAUNCH("union", hs, launch_union(idx, B, n_idx, m->n, o.U, o.cnt, masked ? o.mask : nullptr, hs));
     list = o.U;
     list_count = o.cnt;
     list_max = o.umax;
@@ -103,7 +101,7 @@ dv_status batch_mlp(const dv_mlp* m, const float* x, int B, const int32_t* idx, 
 
 // ---------------------------------------------------------------- attention
 struct BAttn {
-  _Float16* X16; int32_t* Uh; int32_t* hcnt; uint32_t* ubits; int32_t* ucnt; float* P; float* q; float* part;
+  _Float16* X16; int32_t* Uh; int32_t* hcnt; float* P; float* q; float* part;
   _Float16* C;
   float* P2;
   int Kpad, S, Ks, nrows_pad, ldc, S2;
@@ -119,8 +117,6 @@ static size_t battn_layout(const dv_attn* a, int B, int n_heads, Workspace& w, B
   o->X16 = w.take<_Float16>((size_t)NB * o->Kpad * 2);
   o->Uh = w.take<int32_t>((size_t)a->H * 4);
   o->hcnt = w.take<int32_t>(4);
-  o->ubits = w.take<uint32_t>((size_t)union_chunks(a->H) * 64 * 4);
-  o->ucnt = w.take<int32_t>((size_t)union_chunks(a->H) * 4);
   o->P = w.take<float>((size_t)o->S * o->nrows_pad * NB * 4);
   o->q = w.take<float>((size_t)B * std::max(n_heads, 1) * a->dh * 4);
   o->part = w.take<float>((size_t)B * std::max(n_heads, 1) * kAttnMaxSplit * (a->dh + 2) * 4);
@@ -146,7 +142,7 @@ static dv_status battn_run(const dv_attn* a, const dv_kv* kv, const BAttn& o, in
     DV_LAUNCH("oproj_finish", hs, launch_cols_finish(e, hs));
     return DV_OK;
   }
-  DV_LAUNCH("union_heads", hs, launch_union(heads, B, n_heads, a->H, o.Uh, o.hcnt, nullptr, o.ubits, o.ucnt, hs));
+  DV_LAUNCH("union_heads", hs, launch_union(heads, B, n_heads, a->H, o.Uh, o.hcnt, nullptr, hs));
   MrowsArgs r{};
   r.d = a->d; r.Kpad = o.Kpad; r.Ks = o.Ks; r.S = o.S; r.X = o.X16; r.mode = kRowsHeads;
   r.W0 = a->Wq; r.W1 = a->Wk; r.W2 = a->Wv; r.list = o.Uh; r.list_count = o.hcnt; r.list_max = a->H;

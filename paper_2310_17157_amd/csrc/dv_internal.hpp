@@ -356,12 +356,12 @@ struct Fc1Args {
 hipError_t launch_fc1(int wtype, const Fc1Args& a, hipStream_t st);
 
 // ------------------------------------------------ batched (matrix-core) path
-// Union of B ascending sets: U ascending, *count and optional membership bits
-// mask[u] (bit b: U[u] is in set b). Scratch: bits [union_chunks(n) * 64] words and
-// chunk_counts [union_chunks(n)].
-int union_chunks(int n);
+// Union of B ascending sets in [0, n): U ascending, *count and optional membership
+// bits mask[u] (bit b: U[u] is in set b). Needs union_lds_bytes(n) of LDS per
+// workgroup (no scratch memory).
+size_t union_lds_bytes(int n);
 hipError_t launch_union(const int32_t* sets, int B, int k, int n, int32_t* U, int32_t* count, uint32_t* mask,
-                        uint32_t* bits, int32_t* chunk_counts, hipStream_t st);
+                        hipStream_t st);
 
 // X16[NB][Kpad] = fp16(LN(x)) (g NULL: x), zero rows b >= B and columns k >= d.
 hipError_t launch_ln_cast(const float* x, int B, int NB, int d, int Kpad, const float* g, const float* be, float eps,

@@ -54,6 +54,26 @@ def test_batch_mlp_per_sequence_sets(B, mode):
         assert rel_l2(got[b], ref[b]) < REL_TOL, (b, rel_l2(got[b], ref[b]))
 
 
+@pytest.mark.parametrize("offset", [1, 2, 3])
+@pytest.mark.parametrize("mode", ["union", "masked"])
+def test_batch_mlp_sets_at_any_word_offset(offset, mode):
+    """Index sets that start 4, 8 or 12 bytes into a 16-byte block (a view into a larger
+    buffer) give the same output, bit for bit, as the same sets at an aligned address."""
+    cfg = _cfg("small_b8", 17)
+    t = make_layer(cfg, 26, device="cuda", biases=True, with_predictors=False)
+    sets = zipf_mlp_sets(cfg, 26)
+    idx = torch.tensor(sets, dtype=torch.int32, device="cuda")
+    buf = torch.full((sets.size + 8,), -7, dtype=torch.int32, device="cuda")
+    view = buf[offset:offset + sets.size].view(sets.shape)
+    view.copy_(idx)
+    assert view.data_ptr() % 16 == 4 * offset
+    bm = Bd.DV_MLP_UNION if mode == "union" else Bd.DV_MLP_MASKED
+    a = Bd.dv_sparse_mlp(_mlp(t), t["x"], idx, idx_per_seq=1, batch_mode=bm)
+    b = Bd.dv_sparse_mlp(_mlp(t), t["x"], view, idx_per_seq=1, batch_mode=bm)
+    _sync()
+    assert torch.equal(a, b)
+
+
 def test_batch_mlp_union_differs_from_masked():
     """The two batch semantics give different outputs (the union adds other sequences' neurons)."""
     cfg = _cfg("small_b8")
