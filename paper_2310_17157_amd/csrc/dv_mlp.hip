@@ -21,7 +21,7 @@ __global__ void __launch_bounds__(NW * 64) k_fc1(Fc1Args a) {
   };
   // The epilogue's bias reads: the neuron index of row r0 + tid is read first of all
   // loads (it is not waited for until the end), its bias once the stream is done.
-  const int r0 = (int)((long)blockIdx.x * a.k / gridDim.x), r1 = (int)((long)(blockIdx.x + 1) * a.k / gridDim.x);
+  const int r0 = rowdot_split(blockIdx.x, a.k, gridDim.x), r1 = rowdot_split(blockIdx.x + 1, a.k, gridDim.x);
   const bool mine = (int)threadIdx.x < r1 - r0;
   // (with no rows the set may be NULL: a valid word of the input is read instead)
   const int32_t* sp = a.k > 0 ? a.set + min(r0 + (int)threadIdx.x, a.k - 1) : reinterpret_cast<const int32_t*>(a.x);

@@ -30,22 +30,39 @@ constexpr int kRowdotPre = 4;
 struct NoTail {
   __device__ void operator()() const {}
 };
+
+// i * n / G rounded down: the boundary of part i of n rows split G ways (in 32 bits
+// where the product fits, avoiding the long 64-bit division sequence).
+__device__ __forceinline__ int rowdot_split(int i, int n, int G) {
+  if (n < (1 << 23) && i <= 256) return (int)((unsigned)(i * n) / (unsigned)G);
+  return (int)((long)i * n / G);
+}
 template <typename T, int NW, int U, bool PIPE, int KX, bool LN, class RowPtr, class Epi, class Tail = NoTail>
 __device__ __forceinline__ void rowdot_flat(RowPtr row_ptr, Epi epi, int nrows, int d, const float* x,
                                             const float* g, const float* be, float eps, float* xs, float* red,
                                             float* part, float* xhat_out, int wg, int G, Tail tail = Tail()) {
   constexpr int NT = NW * 64;
   constexpr int E = Chunk<T>::E;
+  // the input's reads go out first of all, ahead of the partition arithmetic
+  StageX<T, NT, KX, LN> st;
+  st.load(x, d, g, be);
   // wave-uniform: row pointers and slot bounds live in scalar registers, so that a
   // row change costs a scalar load (its own counter), never a wait on the stream
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
-  const int r0 = (int)((long)wg * nrows / G), r1 = (int)((long)(wg + 1) * nrows / G);
+  const int r0 = rowdot_split(wg, nrows, G), r1 = rowdot_split(wg + 1, nrows, G);
   const int nch = d / E, ipr = (nch + 63) >> 6;
   const int slots = (r1 - r0) * ipr;
   const int tw = (slots + NW - 1) / NW;
   const int s0 = min(wave * tw, slots), s1 = min(s0 + tw, slots);
   const int mr = (nrows + G - 1) / G + 1;
   const bool active = s0 < s1;
+  // Every wavefront issues the same loads on every path (a wait after a branch that
+  // skips loads is counted for the path without them, so it would also wait for the
+  // loads in flight): a wavefront without slots re-reads its workgroup's last slot,
+  // and in a workgroup without rows the input vector (d floats, at least one row of
+  // T) stands in for a row.
+  const bool any = slots > 0;
+  const int shi = active ? s1 - 1 : slots - 1;   // last slot this wavefront reads
 
   // The row pointer (a list lookup for gathered rows) is formed only when the load
   // stream enters a new row, not per load.
@@ -53,16 +70,16 @@ __device__ __forceinline__ void rowdot_flat(RowPtr row_ptr, Epi epi, int nrows, 
   const char* lptr = nullptr;
   // loads u in [u0, u1) of the batch of U slots starting at sb (u0, u1 compile-time)
   auto load_part = [&](u32x4 (&w)[U], int sb, int u0, int u1) {
-    const int sc0 = min(sb + u0, s1 - 1);
+    const int sc0 = max(min(sb + u0, shi), 0);
     int rr = sc0 / ipr, j = sc0 - rr * ipr;
     if (rr != lrow) {
       lrow = rr;
-      lptr = reinterpret_cast<const char*>(row_ptr(r0 + rr));
+      lptr = any ? reinterpret_cast<const char*>(row_ptr(r0 + rr)) : reinterpret_cast<const char*>(x);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       if (u < u0 || u >= u1) continue;
-      if (u > u0 && sb + u < s1) {
+      if (u > u0 && sb + u <= shi) {
         if (++j == ipr) {
           j = 0;
           ++rr;
@@ -108,12 +125,10 @@ __device__ __forceinline__ void rowdot_flat(RowPtr row_ptr, Epi epi, int nrows, 
   // batch follows once the input is staged, so that the staging reads do not queue
   // behind a full batch from every wavefront of the grid.
   constexpr int PRE = kRowdotPre < U ? kRowdotPre : U;
-  StageX<T, NT, KX, LN> st;
-  st.load(x, d, g, be);
   u32x4 wa[U];
-  if (PRE > 0 && active) load_part(wa, s0, 0, PRE);
+  if (PRE > 0) load_part(wa, s0, 0, PRE);
   st.finish(d, be != nullptr, eps, xs, red);
-  if (PRE < U && active) load_part(wa, s0, PRE, U);
+  if (PRE < U) load_part(wa, s0, PRE, U);
   if (xhat_out != nullptr && wg == 0)
     for (int e = threadIdx.x; e < d; e += NT) xhat_out[e] = xs[xs_index<T>(e, d)];
   if (active) {
