@@ -153,7 +153,7 @@ static dv_status enqueue_axpy(const char* label, int wtype, const AxpyArgs& ax, 
 
 // ---------------------------------------------------------------- sparse MLP
 struct MlpWs {
-  float* h; float* axp; int32_t* flag;
+  float* h; float* axp; uint32_t* axc; int32_t* flag;
 };
 
 // Row-split partial sums of a gathered row-axpy of width d.
@@ -162,6 +162,7 @@ static size_t axpy_partial_bytes(int d) { return (size_t)kAxpyMaxRowSplit * d * 
 static size_t mlp_ws_layout(const dv_mlp* m, int B, int n_idx, Workspace& w, MlpWs* o) {
   o->h = w.take<float>((size_t)B * n_idx * sizeof(float));
   o->axp = w.take<float>(axpy_partial_bytes(m->d));
+  o->axc = w.take<uint32_t>(kAxpyMaxSpans * sizeof(uint32_t));
   o->flag = w.take<int32_t>(sizeof(int32_t));
   return w.off;
 }
@@ -201,18 +202,19 @@ extern "C" dv_status dv_sparse_mlp(const dv_mlp* m, const float* x, int32_t B, c
   }
   Fc1Args f{};
   f.d = m->d; f.k = n_idx; f.n = m->n; f.x = x; f.g = nullptr; f.be = nullptr; f.eps = 0.f;
-  f.W1T = m->W1T; f.b1 = m->b1; f.set = idx; f.h = o.h;
+  f.W1T = m->W1T; f.b1 = m->b1; f.set = idx; f.h = o.h; f.clear = o.axc; f.clear_n = kAxpyMaxSpans;
   DV_LAUNCH("fc1", hs, launch_fc1(m->wtype, f, hs));
   AxpyArgs ax{};
   ax.d = m->d; ax.nrows = n_idx; ax.M = m->W2T; ax.m_rows = m->n; ax.set = idx; ax.dh = 0;
   ax.coef = o.h; ax.resid = nullptr; ax.bias = m->b2; ax.out = out; ax.out2 = nullptr; ax.partial = o.axp;
+  ax.cnt = o.axc;
   if ((st = enqueue_axpy("fc2", m->wtype, ax, hs)) != DV_OK) return st;
   return DV_OK;
 }
 
 // ---------------------------------------------------------- sparse attention
 struct AttnWs {
-  int32_t* heads; float* q; float* part; float* axp; int32_t* flag;
+  int32_t* heads; float* q; float* part; float* axp; uint32_t* axc; int32_t* flag;
 };
 
 // Upper bound of split-KV chunks per head.
@@ -223,6 +225,7 @@ static size_t attn_ws_layout(const dv_attn* a, int cap, int B, int n_heads, Work
   o->q = w.take<float>((size_t)B * n_heads * a->dh * sizeof(float));
   o->part = w.take<float>((size_t)B * n_heads * max_split(cap) * (a->dh + 2) * sizeof(float));
   o->axp = w.take<float>(axpy_partial_bytes(a->d));
+  o->axc = w.take<uint32_t>(kAxpyMaxSpans * sizeof(uint32_t));
   o->flag = w.take<int32_t>(sizeof(int32_t));
   return w.off;
 }
@@ -293,20 +296,21 @@ extern "C" dv_status dv_sparse_attn(const dv_attn* a, const float* x, int32_t B,
   q.x = x;
   q.Wq = a->Wq; q.Wk = a->Wk; q.Wv = a->Wv; q.bq = a->bq; q.bk = a->bk; q.bv = a->bv;
   q.K = kv->K; q.V = kv->V; q.q = o.q; q.heads_in = heads; q.heads_ws = o.heads;
+  q.clear = o.axc; q.clear_n = kAxpyMaxSpans;
   DV_LAUNCH("qkv", hs, launch_qkv(a->wtype, kv->ktype, q, hs));
   st = enqueue_attention(a, kv, o, n_heads, scale, hs);
   if (st != DV_OK) return st;
   AxpyArgs ax{};
   ax.d = a->d; ax.nrows = n_heads * a->dh; ax.M = a->WoT; ax.m_rows = a->H * a->dh; ax.set = o.heads;
   ax.dh = a->dh; ax.coef = nullptr; ax.part = o.part; ax.n_split = attn_nsplit(a, kv, n_heads);
-  ax.resid = nullptr; ax.bias = a->bo; ax.out = out; ax.out2 = nullptr; ax.partial = o.axp;
+  ax.resid = nullptr; ax.bias = a->bo; ax.out = out; ax.out2 = nullptr; ax.partial = o.axp; ax.cnt = o.axc;
   return enqueue_axpy("oproj", a->wtype, ax, hs);
 }
 
 // ------------------------------------------------------------- decoder layer
 struct BlockWs {
   float* hid_h; float* hid_m; float* s_h; float* s_m; int32_t* heads; int32_t* idx;
-  float* q; float* part; float* ytilde; float* xhat; float* h; float* axp; int32_t* flag;
+  float* q; float* part; float* ytilde; float* xhat; float* h; float* axp; uint32_t* axc; int32_t* flag;
 };
 
 static size_t block_ws_layout(const dv_attn* a, const dv_mlp* m, const dv_predictor* pa,
@@ -324,6 +328,7 @@ static size_t block_ws_layout(const dv_attn* a, const dv_mlp* m, const dv_predic
   o->xhat = w.take<float>((size_t)B * a->d * sizeof(float));
   o->h = w.take<float>((size_t)B * km * sizeof(float));
   o->axp = w.take<float>(axpy_partial_bytes(a->d));
+  o->axc = w.take<uint32_t>(2 * kAxpyMaxSpans * sizeof(uint32_t));   // out-projection, fc2
   o->flag = w.take<int32_t>(sizeof(int32_t));
   return w.off;
 }
@@ -426,6 +431,7 @@ extern "C" dv_status dv_sparse_block(const dv_attn* a, const dv_mlp* m, const dv
   q.x = o.xhat;
   q.Wq = a->Wq; q.Wk = a->Wk; q.Wv = a->Wv; q.bq = a->bq; q.bk = a->bk; q.bv = a->bv;
   q.K = kv->K; q.V = kv->V; q.q = o.q; q.heads_in = o.heads; q.heads_ws = nullptr;
+  q.clear = o.axc; q.clear_n = kAxpyMaxSpans;
   if (ahead) {
     // the neuron selection (from the LN1(y) scores) runs in one extra workgroup of
     // the QKV launch, beside its weight stream, off the critical path (Section 4.3)
@@ -440,7 +446,7 @@ extern "C" dv_status dv_sparse_block(const dv_attn* a, const dv_mlp* m, const dv
   AxpyArgs ax{};
   ax.d = a->d; ax.nrows = k_heads * a->dh; ax.M = a->WoT; ax.m_rows = a->H * a->dh; ax.set = o.heads;
   ax.dh = a->dh; ax.coef = nullptr; ax.part = o.part; ax.n_split = attn_nsplit(a, kv, k_heads);
-  ax.resid = x_in; ax.bias = a->bo; ax.out = o.ytilde; ax.out2 = nullptr; ax.partial = o.axp;
+  ax.resid = x_in; ax.bias = a->bo; ax.out = o.ytilde; ax.out2 = nullptr; ax.partial = o.axp; ax.cnt = o.axc;
   if ((st = enqueue_axpy("oproj", a->wtype, ax, hs)) != DV_OK) return st;
   // 5b. Sequential mode: the neuron predictor reads LN2(y~).
   if (!ahead) {
@@ -458,11 +464,13 @@ extern "C" dv_status dv_sparse_block(const dv_attn* a, const dv_mlp* m, const dv
   Fc1Args f{};
   f.d = m->d; f.k = k_mlp; f.n = m->n; f.x = o.ytilde; f.g = g2; f.be = be2; f.eps = eps;
   f.W1T = m->W1T; f.b1 = m->b1; f.set = o.idx; f.h = o.h;
+  f.clear = o.axc + kAxpyMaxSpans; f.clear_n = kAxpyMaxSpans;
   DV_LAUNCH("fc1", hs, launch_fc1(m->wtype, f, hs));
   // 7. fc2 + residual: y^ = y~ + MLP(LN2(y~)).
   AxpyArgs ay{};
   ay.d = m->d; ay.nrows = k_mlp; ay.M = m->W2T; ay.m_rows = m->n; ay.set = o.idx; ay.dh = 0;
   ay.coef = o.h; ay.resid = o.ytilde; ay.bias = m->b2; ay.out = x_out; ay.out2 = nullptr; ay.partial = o.axp;
+  ay.cnt = o.axc + kAxpyMaxSpans;
   if ((st = enqueue_axpy("fc2", m->wtype, ay, hs)) != DV_OK) return st;
   return DV_OK;
 }

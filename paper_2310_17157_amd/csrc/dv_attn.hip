@@ -22,6 +22,7 @@ __global__ void __launch_bounds__(NW * 64) k_qkv(QkvArgs a) {
   extern __shared__ float smem[];
   constexpr int NT = NW * 64;
   const int wg = blockIdx.x, nwg = gridDim.x - (a.sel_n > 0 ? 1 : 0);
+  clear_counters(a.clear, a.clear_n);
   if (a.sel_n > 0 && wg == nwg) {
     hosted_select<NT>(a.sel_scores, a.sel_n, a.sel_k, a.sel_idx, a.sel_idx_out, smem);
     return;

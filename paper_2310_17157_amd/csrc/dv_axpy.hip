@@ -12,9 +12,13 @@
 // w, w + NW, ... of the split with U loads in flight and the next U issued before the
 // current are consumed. Wavefront partials are added in LDS in wavefront order; with
 // one split the workgroup writes out directly, otherwise it writes its partial row
-// to partial[s] and a second small launch adds the splits in split order, so the
-// result is bitwise reproducible and no cross-workgroup synchronisation (device-scope
-// fences, which write back and invalidate a whole L2) is needed.
+// to partial[s], and the splits are added in split order (bitwise reproducible) by
+// either a second small launch or, given arrival counters, the last split of each
+// span to arrive. The counter protocol needs no fence that writes back or
+// invalidates a whole L2: partials are written and read with agent-scope (coherent,
+// L2-bypassing) atomic stores and loads, each workgroup waits for its stores to be
+// acknowledged before it increments its span's counter, and the workgroup that
+// draws the last ticket reads every split after that.
 //
 // For the attention the coefficients H_i(y)[t] are combined first, in the prologue,
 // from the split-KV partials (max logit, sum of exponentials and unnormalised value
@@ -156,11 +160,40 @@ __global__ void __launch_bounds__(NW * 64) k_axpy(AxpyArgs a) {
         if (a.bias) s += a.bias[col];
         a.out[col] = s;
         if (a.out2) a.out2[col] = s;
-      } else {
+      } else if (a.cnt == nullptr) {
         a.partial[(size_t)sp * a.d + col] = s;
+      } else {
+        __hip_atomic_store(a.partial + (size_t)sp * a.d + col, s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
     }
   }
+  if (S == 1 || a.cnt == nullptr) return;
+  // ---- arrival: stores acknowledged, then one ticket per workgroup; the last adds
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  __shared__ int last;
+  if (tid == 0)
+    last = __hip_atomic_fetch_add(a.cnt + blockIdx.x, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == (uint32_t)(S - 1);
+  __syncthreads();
+  if (!last) return;
+  for (int t = tid; t < SW; t += NT) {
+    const int col = blockIdx.x * SW + t;
+    if (col < a.d) {
+      float p[kAxpyMaxRowSplit];
+#pragma unroll
+      for (int s = 0; s < kAxpyMaxRowSplit; ++s)
+        if (s < S) p[s] = __hip_atomic_load(a.partial + (size_t)s * a.d + col, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      float v = p[0];
+#pragma unroll
+      for (int s = 1; s < kAxpyMaxRowSplit; ++s)
+        if (s < S) v += p[s];
+      if (a.resid) v += a.resid[col];
+      if (a.bias) v += a.bias[col];
+      a.out[col] = v;
+      if (a.out2) a.out2[col] = v;
+    }
+  }
+  if (tid == 0) __hip_atomic_store(a.cnt + blockIdx.x, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // out = sum_s partial[s] (in split order) + resid + bias; four columns per thread,
@@ -196,13 +229,14 @@ static hipError_t launch_axpy_t(AxpyArgs a, hipStream_t st) {
   constexpr int E = Chunk<T>::E;
   const int spans = (a.d / E + 63) / 64;
   const int S = a.partial != nullptr ? axpy_row_splits(a.d, E, a.nrows) : 1;
+  if (spans > kAxpyMaxSpans) a.cnt = nullptr;   // no counter per span: the split sum is a launch
   // LDS: (coefficient, row index) pairs of a batch of the split's rows and the
   // wavefront sums.
   const int rpb = min(kAxRowsLds, max(1, (a.nrows + S - 1) / S));
   a.rows_per_batch = rpb;
   const size_t lds = (size_t)rpb * 8 + (size_t)kAxNW * 64 * E * 4;
   hipLaunchKernelGGL((k_axpy<T, kAxNW, kAxU, HEADS>), dim3(spans, S), dim3(kAxNW * 64), lds, st, a);
-  if (S > 1) hipLaunchKernelGGL(k_axpy_sum, dim3((a.d / 4 + 255) / 256), dim3(256), 0, st, a, S);
+  if (S > 1 && a.cnt == nullptr) hipLaunchKernelGGL(k_axpy_sum, dim3((a.d / 4 + 255) / 256), dim3(256), 0, st, a, S);
   return hipGetLastError();
 }
 

@@ -308,6 +308,7 @@ struct QkvArgs {
   int32_t* heads_ws;                // optional [n_heads] out: the set, clamped (one workgroup)
   // Top-k selection run by one extra workgroup of the launch (sel_n == 0: none).
   const float* sel_scores; int sel_n; int sel_k; int32_t* sel_idx; int32_t* sel_idx_out;
+  uint32_t* clear; int clear_n;     // counters of a later row-axpy to zero (optional)
 };
 hipError_t launch_qkv(int wtype, int kvtype, const QkvArgs& a, hipStream_t st);
 
@@ -341,9 +342,21 @@ struct AxpyArgs {
   float* out2;                       // optional second copy of out
   // Row-split partial sums [kAxpyMaxRowSplit][d] (workspace); NULL: one split.
   float* partial;
+  // Per column span arrival counters [kAxpyMaxSpans], zero at launch (an earlier
+  // kernel of the same call clears them): the last split of a span to arrive adds
+  // the partials. NULL: a second launch adds them.
+  uint32_t* cnt;
   int rows_per_batch;                // set by the launcher
 };
 constexpr int kAxpyMaxRowSplit = 32;
+constexpr int kAxpyMaxSpans = 64;     // column spans of 64 x 16 bytes at d <= 16000
+
+// Clears n counters for a later row-axpy of the same call (agent-scope stores: the
+// counters are read by atomics from every XCD).
+__device__ __forceinline__ void clear_counters(uint32_t* c, int n) {
+  if (c != nullptr && blockIdx.x == 0)
+    for (int i = threadIdx.x; i < n; i += blockDim.x) __hip_atomic_store(c + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 hipError_t launch_axpy(int wtype, const AxpyArgs& a, hipStream_t st);
 
 // fc1 + ReLU over the selected neurons (B = 1): h[s] = max(x-hat . W1T[set[s]] + b1, 0).
@@ -352,6 +365,7 @@ struct Fc1Args {
   const float* x; const float* g; const float* be; float eps;    // LN (g NULL: none)
   const void* W1T; const float* b1; const int32_t* set;
   float* h;
+  uint32_t* clear; int clear_n;     // counters of a later row-axpy to zero (optional)
 };
 hipError_t launch_fc1(int wtype, const Fc1Args& a, hipStream_t st);
 

@@ -16,6 +16,7 @@ __global__ void __launch_bounds__(NW * 64) k_fc1(Fc1Args a) {
   float* xs = smem;
   float* red = smem + a.d;
   float* part = red + NW;
+  clear_counters(a.clear, a.clear_n);
   auto row_ptr = [&](int s) {
     return static_cast<const T*>(a.W1T) + (size_t)min(max(a.set[s], 0), a.n - 1) * a.d;
   };
