@@ -120,10 +120,13 @@ __device__ __forceinline__ void head_scores_select(const PredScoreArgs& a, float
 // The grid is sized to stay resident (two workgroups per CU); workgroup wg of G takes
 // an even contiguous share of the rows and its wavefronts split that share evenly.
 // A wavefront works in groups of RU rows per lane group (GPW = 64 / G groups of G
-// lanes), RU large enough that one group is usually all of its rows; every load of a
-// group (NR rounds of G chunks per row, row and chunk clamped, surplus masked where
-// summed) is issued before the group is used.
-template <typename T, int NW, int G, int RU, int NR>
+// lanes); every load of a group (NR rounds of G chunks per row, row and chunk
+// clamped, surplus masked where summed) is issued before the group is used, and
+// with one round of chunks per row two groups are in flight. With EARLY (ranks up to 4 * NT) the
+// first group's loads go out before the hidden vectors are staged: their reads are
+// issued first, as straight-line code, so that the staging waits for them alone and
+// the weight stream starts at once instead of after their round trip.
+template <typename T, int NW, int G, int RU, int NR, bool EARLY>
 __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2 * NW / 4))) k_pred_scores(PredScoreArgs a) {
   extern __shared__ float smem[];
   constexpr int NT = NW * 64;
@@ -137,8 +140,17 @@ __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2 
     head_scores_select<T, NW, 6>(a, xs0, xs1 + ((a.r1 + 3) & ~3));
     return;
   }
-  stage_x<T, NT>(a.hid0 + (size_t)b * a.r0, a.r0, xs0);
-  if (a.n1 > 0) stage_x<T, NT>(a.hid1 + (size_t)b * a.r1, a.r1, xs1);
+  const bool two = a.n1 > 0;
+  StageX<T, NT, 1> hx0, hx1;
+  if constexpr (EARLY) {
+    hx0.load(a.hid0 + (size_t)b * a.r0, a.r0, nullptr, nullptr);
+    // (one predictor: a read that is unused and not the first one's, so that the
+    // compiler does not fold the two into a wait and a branch)
+    hx1.load(two ? a.hid1 + (size_t)b * a.r1 : a.hid0 + (size_t)b * a.r0, two ? a.r1 : 4, nullptr, nullptr);
+  } else {
+    stage_x<T, NT>(a.hid0 + (size_t)b * a.r0, a.r0, xs0);
+    if (two) stage_x<T, NT>(a.hid1 + (size_t)b * a.r1, a.r1, xs1);
+  }
   const int nrows = a.n0 + a.n1;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int grp = lane / G, gl = lane % G;
@@ -149,48 +161,68 @@ __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2 
   const int w0 = rb + (int)((long)wg * R / Gw), w1 = rb + (int)((long)(wg + 1) * R / Gw);
   const int v0 = w0 + (w1 - w0) * wave / NW, v1 = w0 + (w1 - w0) * (wave + 1) / NW;   // this wavefront's rows
   const int ng = (v1 - v0 + RPG - 1) / RPG;
-  if (ng == 0) return;
+  if (!EARLY && ng == 0) return;
   const int nch0 = a.r0 / E, nch1 = a.r1 / E;
   const int cmax = max(nch0, a.n1 > 0 ? nch1 : 0);
 
   auto row_of = [&](int k, int u) { return v0 + k * RPG + u * GPW + grp; };
+  auto load = [&](u32x4 (&w)[RU][NR], int k, int c0) {
+#pragma unroll
+    for (int u = 0; u < RU; ++u) {
+      const int row = max(min(row_of(k, u), v1 - 1), 0);   // (a wavefront without rows reads row 0)
+      const bool sec = row >= a.n0;
+      const char* rp = sec ? reinterpret_cast<const char*>(static_cast<const T*>(a.BT1) + (size_t)(row - a.n0) * a.r1)
+                           : reinterpret_cast<const char*>(static_cast<const T*>(a.BT0) + (size_t)row * a.r0);
+      const int nch = sec ? nch1 : nch0;
+#pragma unroll
+      for (int h = 0; h < NR; ++h) w[u][h] = ld_stream(rp + (size_t)min(c0 + h * G + gl, nch - 1) * 16);
+    }
+  };
+  auto consume = [&](const u32x4 (&w)[RU][NR], int k, int c0) {
+#pragma unroll
+    for (int u = 0; u < RU; ++u) {
+      const int row = row_of(k, u);
+      const bool sec = row >= a.n0;
+      const int nch = sec ? nch1 : nch0;
+      float acc = 0.f;
+#pragma unroll
+      for (int h = 0; h < NR; ++h) {
+        const int c = c0 + h * G + gl;
+        if (c < nch) acc = sec ? dot_chunk<T>(w[u][h], xs1, a.r1, c, acc) : dot_chunk<T>(w[u][h], xs0, a.r0, c, acc);
+      }
+#pragma unroll
+      for (int o = G / 2; o > 0; o >>= 1) acc += __shfl_xor(acc, o, kWave);
+      if (gl == 0 && row < v1) {
+        float* out = sec ? a.s1 + (size_t)b * a.n1 + row - a.n0 : a.s0 + (size_t)b * a.n0 + row;
+        *out = c0 == 0 ? acc : *out + acc;   // rows longer than NR * G chunks: one round per c0
+      }
+    }
+  };
+  u32x4 w[RU][NR];
+  if constexpr (EARLY) {
+    load(w, 0, 0);   // the first group, before the staging waits
+    hx0.finish(a.r0, false, 0.f, xs0, nullptr);
+    if (two) hx1.finish(a.r1, false, 0.f, xs1, nullptr);
+    if (ng == 0) return;
+  }
+  if (cmax <= NR * G) {
+    // one round of chunks (the usual case): groups alternate between two register
+    // sets, the next group's loads issued before the current group is used
+    u32x4 w2[RU][NR];
+    if (!EARLY) load(w, 0, 0);
+    for (int k = 0; k < ng; k += 2) {
+      if (k + 1 < ng) load(w2, k + 1, 0);
+      consume(w, k, 0);
+      if (k + 1 >= ng) break;
+      if (k + 2 < ng) load(w, k + 2, 0);
+      consume(w2, k + 1, 0);
+    }
+    return;
+  }
   for (int c0 = 0; c0 < cmax; c0 += NR * G) {
-    auto load = [&](u32x4 (&w)[RU][NR], int k) {
-#pragma unroll
-      for (int u = 0; u < RU; ++u) {
-        const int row = min(row_of(k, u), v1 - 1);
-        const bool sec = row >= a.n0;
-        const char* rp = sec ? reinterpret_cast<const char*>(static_cast<const T*>(a.BT1) + (size_t)(row - a.n0) * a.r1)
-                             : reinterpret_cast<const char*>(static_cast<const T*>(a.BT0) + (size_t)row * a.r0);
-        const int nch = sec ? nch1 : nch0;
-#pragma unroll
-        for (int h = 0; h < NR; ++h) w[u][h] = ld_stream(rp + (size_t)min(c0 + h * G + gl, nch - 1) * 16);
-      }
-    };
-    auto consume = [&](const u32x4 (&w)[RU][NR], int k) {
-#pragma unroll
-      for (int u = 0; u < RU; ++u) {
-        const int row = row_of(k, u);
-        const bool sec = row >= a.n0;
-        const int nch = sec ? nch1 : nch0;
-        float acc = 0.f;
-#pragma unroll
-        for (int h = 0; h < NR; ++h) {
-          const int c = c0 + h * G + gl;
-          if (c < nch) acc = sec ? dot_chunk<T>(w[u][h], xs1, a.r1, c, acc) : dot_chunk<T>(w[u][h], xs0, a.r0, c, acc);
-        }
-#pragma unroll
-        for (int o = G / 2; o > 0; o >>= 1) acc += __shfl_xor(acc, o, kWave);
-        if (gl == 0 && row < v1) {
-          float* out = sec ? a.s1 + (size_t)b * a.n1 + row - a.n0 : a.s0 + (size_t)b * a.n0 + row;
-          *out = c0 == 0 ? acc : *out + acc;   // rows longer than NR * G chunks: one round per c0
-        }
-      }
-    };
     for (int k = 0; k < ng; ++k) {
-      u32x4 w[RU][NR];
-      load(w, k);
-      consume(w, k);
+      if (!EARLY || c0 > 0 || k > 0) load(w, k, c0);
+      consume(w, k, c0);
     }
   }
 }
@@ -206,13 +238,19 @@ static hipError_t launch_scores_t(const PredScoreArgs& a, hipStream_t st) {
   // two workgroups per CU (the head-selection workgroup included): all resident at once
   const int blocks = max(1, min(2 * device_cu_count() - hosted, nrows));
   const dim3 grid(blocks + hosted, a.B);
+  // hidden vectors staged behind the first loads when one float4 per thread holds them
+  const bool early = max(a.r0, a.r1) <= 4 * NW * 64;
   if (nch > 32) {
-    // 64 lanes per row, all chunks of a row up to 128 (r <= 1024 fp16) in one round
-    hipLaunchKernelGGL((k_pred_scores<T, NW, 64, 13, 2>), grid, dim3(NW * 64), lds, st, a);
+    // 64 lanes per row, all chunks of a row up to 128 (r <= 1024 fp16) in one round;
+    // groups of 4 rows, two in flight (measured faster than one group of 13)
+    if (early) hipLaunchKernelGGL((k_pred_scores<T, NW, 64, 4, 2, true>), grid, dim3(NW * 64), lds, st, a);
+    else hipLaunchKernelGGL((k_pred_scores<T, NW, 64, 4, 2, false>), grid, dim3(NW * 64), lds, st, a);
   } else if (nch > 16) {
-    hipLaunchKernelGGL((k_pred_scores<T, NW, 32, 13, 1>), grid, dim3(NW * 64), lds, st, a);
+    if (early) hipLaunchKernelGGL((k_pred_scores<T, NW, 32, 8, 1, true>), grid, dim3(NW * 64), lds, st, a);
+    else hipLaunchKernelGGL((k_pred_scores<T, NW, 32, 8, 1, false>), grid, dim3(NW * 64), lds, st, a);
   } else {
-    hipLaunchKernelGGL((k_pred_scores<T, NW, 16, 13, 1>), grid, dim3(NW * 64), lds, st, a);
+    if (early) hipLaunchKernelGGL((k_pred_scores<T, NW, 16, 8, 1, true>), grid, dim3(NW * 64), lds, st, a);
+    else hipLaunchKernelGGL((k_pred_scores<T, NW, 16, 8, 1, false>), grid, dim3(NW * 64), lds, st, a);
   }
   return hipGetLastError();
 }
@@ -227,7 +265,10 @@ __global__ void __launch_bounds__(1024) k_select(const float* s, int n, int mode
   __shared__ uint32_t hist[kSelBins];
   __shared__ int sm[kSelSm(1024)];
   const int b = blockIdx.x;
-  if (n <= 1024 * 48)
+  if (n <= 1024)
+    wg_select_small<1024>(s + (size_t)b * n, n, mode, k, thresh, idx + (size_t)b * cap, cap,
+                          count ? count + b : nullptr, idx2 ? idx2 + (size_t)b * cap : nullptr, hist, sm);
+  else if (n <= 1024 * 48)
     wg_select_reg<1024, 48>(s + (size_t)b * n, n, mode, k, thresh, idx + (size_t)b * cap, cap,
                             count ? count + b : nullptr, idx2 ? idx2 + (size_t)b * cap : nullptr, hist, sm);
   else

@@ -353,6 +353,45 @@ __device__ void wg_select_reg(const float* __restrict__ s, int n, int mode, int 
   __syncthreads();
 }
 
+// Selection from a short score vector (n <= NT, one score per thread): the keys are
+// staged in LDS and each thread ranks its own against all of them (O(n^2) LDS reads,
+// no histogram passes). Same result as wg_select_reg: top-k keeps the k highest keys,
+// ties to the lower index (k >= n: every key), threshold keeps every key >= the
+// threshold's; the set is written ascending (its first cap members), *count_out gets
+// its full size. keys: n u32 of LDS; red: block_excl_scan scratch. Ends with a barrier.
+template <int NT>
+__device__ void wg_select_small(const float* __restrict__ s, int n, int mode, int k, float thresh,
+                                int32_t* __restrict__ out, int cap, int32_t* __restrict__ count_out,
+                                int32_t* __restrict__ out2, uint32_t* keys, int* red) {
+  const int i = threadIdx.x;
+  const uint32_t ki = i < n ? fkey(s[i]) : 0u;
+  if (i < n) keys[i] = ki;
+  __syncthreads();
+  bool sel = false;
+  if (i < n) {
+    if (mode == DV_SELECT_THRESHOLD) {
+      sel = ki >= fkey(thresh);
+    } else if (k >= n) {
+      sel = ki > 0u;          // every real key is > 0
+    } else if (k > 0) {
+      int rank = 0;
+      for (int j = 0; j < n; ++j) {
+        const uint32_t kj = keys[j];
+        rank += (kj > ki) || (kj == ki && j < i);
+      }
+      sel = rank < k;
+    }
+  }
+  int total = 0;
+  const int p = block_excl_scan<NT>(sel ? 1 : 0, red, &total);
+  if (sel && p < cap) {
+    out[p] = i;
+    if (out2) out2[p] = i;
+  }
+  if (i == 0 && count_out) *count_out = total;
+  __syncthreads();
+}
+
 // Top-k selection run by one extra workgroup of another kernel's launch (which leaves
 // CUs free for it), so that the selection runs beside that kernel's weight stream
 // instead of on the critical path. Kept out of line so that its register allocation

@@ -96,6 +96,33 @@ def test_topk_ties_and_edge_sizes():
     assert int(cnt[0]) == 0
 
 
+@pytest.mark.parametrize("n", [96, 1024, 1025, 3000])
+def test_select_paths_agree_with_oracle(n):
+    """Score vectors up to 1024 are ranked in LDS, longer ones by the radix select: both
+    give the oracle's set, with exact ties to the lower index, in top-k and threshold
+    mode (the threshold count may exceed the capacity; the first cap members are kept)."""
+    d, r = 64, 8
+    AT = torch.zeros((r, d), dtype=torch.float32, device="cuda")
+    AT[0, 0] = 1.0
+    BT = torch.zeros((n, r), dtype=torch.float32, device="cuda")
+    vals = torch.tensor([float((i * 13) % 11) - 5.0 for i in range(n)], device="cuda")   # ties, both signs
+    BT[:, 0] = vals
+    x = torch.zeros((1, d), dtype=torch.float32, device="cuda")
+    x[0, 0] = 1.0
+    pred = Bd.Predictor(AT, BT)
+    s = vals.cpu().double().numpy()
+    for k in (1, n // 3, n - 1, n):
+        idx, _ = Bd.dv_predict_heads(pred, x, k)
+        _sync()
+        assert host(idx)[0].tolist() == O.select_topk(s, k).tolist(), (n, k)
+    full = O.select_threshold(s, 2.0).tolist()
+    cap = max(1, len(full) // 2)
+    idx, cnt = Bd.dv_predict_heads(pred, x, mode=Bd.DV_SELECT_THRESHOLD, thresh=2.0, cap_idx=cap)
+    _sync()
+    assert int(cnt[0]) == len(full)
+    assert host(idx)[0][:cap].tolist() == full[:cap]
+
+
 # ------------------------------------------------------------------ sparse MLP
 @pytest.mark.parametrize("name", SMALL + ["opt6.7b_b1"])
 def test_sparse_mlp(name):
