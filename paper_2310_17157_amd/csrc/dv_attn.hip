@@ -104,7 +104,11 @@ hipError_t launch_qkv(int wtype, int kvtype, const QkvArgs& a, hipStream_t st) {
 // 64 / LPP positions per step and NSTEP steps per sub-chunk; NW wavefronts per
 // workgroup. A workgroup walks its chunk of positions sub-chunk by sub-chunk with a
 // running max, sum of exponentials and value sum per wavefront (online softmax), so a
-// chunk may be any multiple of the sub-chunk length.
+// chunk may be any multiple of the sub-chunk length. The keys and values of the next
+// sub-chunk are loaded (two register sets) before the current one is used; loads are
+// never predicated (positions past the chunk read its last row and score -inf, lanes
+// past the head width read the row's last 16 bytes and are not written out), so the
+// waits count exactly the loads of the sub-chunk being used.
 template <typename KT, int LPP, int NSTEP>
 __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   constexpr int NW = 4;
@@ -126,7 +130,7 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
 #pragma unroll
   for (int e = 0; e < E; ++e) qv[e] = lane_on ? a.q[(size_t)jb * a.dh + gl * E + e] : 0.f;
   const size_t rowb = (size_t)a.dh * sizeof(KT);
-  const size_t hoff = ((size_t)b * a.H + head) * a.cap * rowb + (size_t)gl * 16;
+  const size_t hoff = ((size_t)b * a.H + head) * a.cap * rowb + (size_t)min(gl, nchr - 1) * 16;
   const char* Kb = static_cast<const char*>(a.K) + hoff;
   const char* Vb = static_cast<const char*>(a.V) + hoff;
 
@@ -134,18 +138,19 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   float o[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) o[e] = 0.f;
-  for (int sb = t0; sb < tend; sb += SUB) {
-    u32x4 kw[NSTEP], vw[NSTEP];
+  auto ldkv = [&](u32x4 (&kw)[NSTEP], u32x4 (&vw)[NSTEP], int sb) {
 #pragma unroll
     for (int s = 0; s < NSTEP; ++s) {
-      const int t = sb + (s * NW + wave) * PPW + grp;
-      kw[s] = (t < tend && lane_on) ? ld_plain(Kb + (size_t)t * rowb) : u32x4{0u, 0u, 0u, 0u};
+      const int t = max(min(sb + (s * NW + wave) * PPW + grp, tend - 1), 0);
+      kw[s] = ld_plain(Kb + (size_t)t * rowb);
     }
 #pragma unroll
     for (int s = 0; s < NSTEP; ++s) {
-      const int t = sb + (s * NW + wave) * PPW + grp;
-      vw[s] = (t < tend && lane_on) ? ld_plain(Vb + (size_t)t * rowb) : u32x4{0u, 0u, 0u, 0u};
+      const int t = max(min(sb + (s * NW + wave) * PPW + grp, tend - 1), 0);
+      vw[s] = ld_plain(Vb + (size_t)t * rowb);
     }
+  };
+  auto use = [&](const u32x4 (&kw)[NSTEP], const u32x4 (&vw)[NSTEP], int sb) {
     float sc[NSTEP];
     float mb = -INFINITY;
 #pragma unroll
@@ -180,6 +185,17 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
       }
       m = mn;
     }
+  };
+  u32x4 ka[NSTEP], va[NSTEP], kb[NSTEP], vb[NSTEP];
+  ldkv(ka, va, t0);
+  for (int sb = t0; sb < tend;) {
+    ldkv(kb, vb, sb + SUB);
+    use(ka, va, sb);
+    sb += SUB;
+    if (sb >= tend) break;
+    ldkv(ka, va, sb + SUB);
+    use(kb, vb, sb);
+    sb += SUB;
   }
   // Each lane's l and o cover its own position group; sum over the groups.
 #pragma unroll
@@ -224,7 +240,7 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   }
 }
 
-constexpr int kAttnNStep = 8;
+constexpr int kAttnNStep = 4;
 
 static int attn_lpp(int dh, int kvtype) {
   const int nchr = dh * elem_bytes(kvtype) / 16;
@@ -232,7 +248,7 @@ static int attn_lpp(int dh, int kvtype) {
 }
 
 int attn_chunk(int n_heads, int attended, int dh, int kvtype) {
-  // Positions per workgroup: a multiple of the sub-chunk (8 steps x 4 wavefronts x
+  // Positions per workgroup: a multiple of the sub-chunk (kAttnNStep steps x 4 wavefronts x
   // positions per step). At most kAttnMaxSplit chunks per head (they are combined in
   // the out-projection's prologue); otherwise aim at about one workgroup per CU.
   const int sub = kAttnNStep * 4 * (64 / attn_lpp(dh, kvtype));
