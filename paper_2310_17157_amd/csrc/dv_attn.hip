@@ -58,7 +58,7 @@ __global__ void __launch_bounds__(NW * 64) k_qkv(QkvArgs a) {
       C[((size_t)head * a.cap + a.pos) * a.dh + t] = (KT)v;
     }
   };
-  rowdot_flat<T, NW, U, true, KX, false>(row_ptr, epi, 3 * per_mat, a.d, a.x, nullptr, nullptr, 0.f, xs, red, part,
+  rowdot_flat<T, NW, U, KX, false>(row_ptr, epi, 3 * per_mat, a.d, a.x, nullptr, nullptr, 0.f, xs, red, part,
                                          nullptr, wg, nwg);
 }
 

@@ -39,14 +39,16 @@ __global__ void __launch_bounds__(NW * 64) k_fc1(Fc1Args a) {
     }
     a.h[s] = v > 0.f ? v : 0.f;
   };
-  rowdot_flat<T, NW, U, false, KX, LN>(row_ptr, epi, a.k, a.d, a.x, a.g, a.be, a.eps, xs, red, part, nullptr, blockIdx.x,
+  rowdot_flat<T, NW, U, KX, LN>(row_ptr, epi, a.k, a.d, a.x, a.g, a.be, a.eps, xs, red, part, nullptr, blockIdx.x,
                                    gridDim.x, tail);
 }
 
 template <typename T, int KX>
 static hipError_t launch_fc1_t(const Fc1Args& a, hipStream_t st) {
-  // 16 loads per lane in flight, fewer with wider inputs (register budget)
-  constexpr int NW = 16, U = KX >= 4 ? 8 : (KX == 3 ? 12 : 16);
+  // two batches of 2 loads in flight per wavefront: measured faster than all of a
+  // wavefront's loads at once (12 at the OPT-175B shape) or batches of 1, 3, 4 or 6,
+  // as deeper queues let the XCDs that win the fabric arbitration run ahead
+  constexpr int NW = 16, U = 2;
   const int blocks = max(1, min(a.k, device_cu_count()));
   const size_t lds = (size_t)(a.d + NW + rowdot_flat_part(a.k, blocks, NW)) * sizeof(float);
   if (a.g != nullptr)

@@ -27,14 +27,16 @@ __global__ void __launch_bounds__(NW * 64) k_pred_hidden(PredHidArgs a) {
     else
       a.hid1[(size_t)b * a.r1 + row - a.r0] = v;
   };
-  rowdot_flat<T, NW, U, false, KX, LN>(row_ptr, epi, a.r0 + a.r1, a.d, a.x + (size_t)b * a.d, a.g, a.be, a.eps, xs, red, part,
+  rowdot_flat<T, NW, U, KX, LN>(row_ptr, epi, a.r0 + a.r1, a.d, a.x + (size_t)b * a.d, a.g, a.be, a.eps, xs, red, part,
                         a.xhat_out ? a.xhat_out + (size_t)b * a.d : nullptr, blockIdx.x, gridDim.x);
 }
 
 template <typename T, int KX>
 static hipError_t launch_pred_hidden_t(const PredHidArgs& a, hipStream_t st) {
-  // 16 loads per lane in flight, fewer with wider inputs (register budget)
-  constexpr int NW = 16, U = KX >= 4 ? 8 : (KX == 3 ? 12 : 16);
+  // two batches of 2 loads in flight per wavefront: measured faster than all of a
+  // wavefront's loads at once (12 at the OPT-175B shape) or batches of 1, 3, 4 or 6,
+  // as deeper queues let the XCDs that win the fabric arbitration run ahead
+  constexpr int NW = 16, U = 2;
   const int nrows = a.r0 + a.r1;
   const dim3 grid(max(1, min(nrows, device_cu_count())), a.B);
   const size_t lds = (size_t)(a.d + NW + rowdot_flat_part(nrows, grid.x, NW)) * sizeof(float);

@@ -14,11 +14,12 @@ constexpr int kRowdotPre = 4;
 // its NW wavefronts split that range's load slots evenly across row boundaries (a
 // slot is one wavefront load of 64 lanes x 16 bytes; a row of nch chunks is
 // ipr = ceil(nch / 64) slots). Every wavefront thus has the same number of loads
-// whatever the row count, all of them issued early: the first batch of U around the
-// prologue (kRowdotPre behind the input reads, the rest once the input is staged) and,
-// with PIPE, each next U before the current U are consumed (from two alternating
-// register sets, so that no wait is ever needed just to move data; surplus loads past
-// the end are clamped to the last slot and discarded). A wavefront reduces its partial
+// whatever the row count: the first batch of U around the prologue (kRowdotPre
+// behind the input reads, the rest once the input is staged), then each next U
+// before the current U are consumed (two alternating register sets, so that no wait
+// is ever needed just to move data; surplus loads past the end are clamped to the
+// last slot and discarded). Callers keep U small (2): deeper queues per wavefront
+// were measured slower on this part. A wavefront reduces its partial
 // sum of a row when it leaves the row and records it in LDS (part[wave * mr + k] for its k-th
 // row, mr = ceil(R/G) + 1); after a barrier one thread per row adds the records of the
 // wavefronts that covered it, in wavefront order (bitwise reproducible), and calls
@@ -37,7 +38,7 @@ __device__ __forceinline__ int rowdot_split(int i, int n, int G) {
   if (n < (1 << 23) && i <= 256) return (int)((unsigned)(i * n) / (unsigned)G);
   return (int)((long)i * n / G);
 }
-template <typename T, int NW, int U, bool PIPE, int KX, bool LN, class RowPtr, class Epi, class Tail = NoTail>
+template <typename T, int NW, int U, int KX, bool LN, class RowPtr, class Epi, class Tail = NoTail>
 __device__ __forceinline__ void rowdot_flat(RowPtr row_ptr, Epi epi, int nrows, int d, const float* x,
                                             const float* g, const float* be, float eps, float* xs, float* red,
                                             float* part, float* xhat_out, int wg, int G, Tail tail = Tail()) {
@@ -132,27 +133,16 @@ __device__ __forceinline__ void rowdot_flat(RowPtr row_ptr, Epi epi, int nrows, 
   if (xhat_out != nullptr && wg == 0)
     for (int e = threadIdx.x; e < d; e += NT) xhat_out[e] = xs[xs_index<T>(e, d)];
   if (active) {
-    if constexpr (PIPE) {
-      u32x4 wb[U];
-      for (int sb = s0;;) {
-        load(wb, sb + U);
-        consume(wa, sb);
-        sb += U;
-        if (sb >= s1) break;
-        load(wa, sb + U);
-        consume(wb, sb);
-        sb += U;
-        if (sb >= s1) break;
-      }
-    } else {
-      // one register set: when a wavefront has at most U loads (the usual case for
-      // a few thousand rows) all of them are in flight before the prologue
-      for (int sb = s0;;) {
-        consume(wa, sb);
-        sb += U;
-        if (sb >= s1) break;
-        load(wa, sb);
-      }
+    u32x4 wb[U];
+    for (int sb = s0;;) {
+      load(wb, sb + U);
+      consume(wa, sb);
+      sb += U;
+      if (sb >= s1) break;
+      load(wa, sb + U);
+      consume(wb, sb);
+      sb += U;
+      if (sb >= s1) break;
     }
     flush();
   }
