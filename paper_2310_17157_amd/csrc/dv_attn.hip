@@ -67,9 +67,9 @@ constexpr int kQkvSelFreeCUs = 4;
 
 template <typename T, typename KT, int KX>
 static hipError_t launch_qkv_t(const QkvArgs& a, hipStream_t st) {
-  // 2 loads per batch, two batches in flight per wavefront (measured: 2 < 1, 3 < 4
-  // < 6, 8, 16): deeper queues only let the XCDs that win the fabric arbitration race
-  // ahead of the others
+  // 2 loads per batch, two batches in flight per wavefront (measured fastest; 1 and 3
+  // were close, 4, 6, 8 and 16 slower): deeper queues only let the XCDs that win the
+  // fabric arbitration race ahead of the others
   constexpr int NW = 16, U = 2;
   constexpr int NT = NW * 64;
   const int nrows = 3 * a.n_heads * a.dh;
