@@ -39,6 +39,16 @@ __device__ __forceinline__ v4s_t ds_read_tr16(const _Float16* p) {
       (v4s_t __attribute__((address_space(3)))*)(const_cast<_Float16*>(p)));
 }
 
+// Raises a kernel's dynamic LDS limit to the bytes a launch needs (above the 64 KB
+// default; the limit is per kernel, kept in *cur). The limit is the request itself,
+// not the device maximum: the kernel's static LDS has to fit beside it.
+static hipError_t ensure_dyn_lds(const void* kern, size_t bytes, int* cur) {
+  if (bytes <= 65536 || (int)bytes <= *cur) return hipSuccess;
+  const hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  if (e == hipSuccess) *cur = (int)bytes;
+  return e;
+}
+
 static int lds_budget() {
   static int cached = 0;
   if (cached == 0) {
@@ -150,13 +160,11 @@ hipError_t launch_union(const int32_t* sets, int B, int k, int n, int32_t* U, in
                         hipStream_t st) {
   const int nc = (n + kUnionChunk - 1) / kUnionChunk;
   const size_t lds = union_lds_bytes(n);
-  static bool attr[2] = {false, false};
+  static int cur[2] = {0, 0};
   const void* kern = mask != nullptr ? reinterpret_cast<const void*>(k_union<true>)
                                      : reinterpret_cast<const void*>(k_union<false>);
-  if (lds > 65536 && !attr[mask != nullptr]) {
-    (void)hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds_budget());
-    attr[mask != nullptr] = true;
-  }
+  const hipError_t e = ensure_dyn_lds(kern, lds, &cur[mask != nullptr]);
+  if (e != hipSuccess) return e;
   if (mask != nullptr)
     hipLaunchKernelGGL(k_union<true>, dim3(nc), dim3(kUnionNT), lds, st, sets, B, k, n, U, count, mask);
   else
@@ -399,12 +407,9 @@ template <int NB, int MODE>
 static hipError_t launch_mrows_t(MrowsArgs a, hipStream_t st) {
   const size_t lds = (size_t)NB * (a.Ks + 8) * 2 + kMrTileBytes;
   const auto kern = k_mfma_rows<NB, kMrNW, kMrU, MODE>;
-  static bool attr = false;
-  if (!attr) {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
-                              lds_budget());
-    attr = true;
-  }
+  static int cur = 0;
+  const hipError_t e = ensure_dyn_lds(reinterpret_cast<const void*>(kern), lds, &cur);
+  if (e != hipSuccess) return e;
   const int G = max(1, device_cu_count() / a.S);
   hipLaunchKernelGGL(kern, dim3(G * a.S), dim3(kMrNW * 64), lds, st, a);
   return hipGetLastError();

@@ -136,6 +136,9 @@ def test_batched_path_limits(lib):
     assert _call_mlp(lib, _mlp(), Bn=33, per_seq=1) == B.DV_ERR_UNSUPPORTED
     assert _call_mlp(lib, _mlp(wtype=B.DV_F32), Bn=2, per_seq=1) == B.DV_ERR_UNSUPPORTED
     assert _call_mlp(lib, _mlp(), Bn=2, per_seq=1, ws=None) == B.DV_ERR_WORKSPACE
+    # the union marks one byte per neuron in LDS: up to 131072 neurons at B > 1
+    assert _call_mlp(lib, _mlp(n=131073), Bn=2, per_seq=1) == B.DV_ERR_UNSUPPORTED
+    assert _call_mlp(lib, _mlp(n=131072), Bn=2, per_seq=1, ws=None) == B.DV_ERR_WORKSPACE
     m = _mlp()
     one = lib.dv_sparse_mlp_workspace_bytes(ctypes.byref(m), 1, 8, 1)
     many = lib.dv_sparse_mlp_workspace_bytes(ctypes.byref(m), 32, 8, 1)

@@ -74,6 +74,27 @@ def test_batch_mlp_sets_at_any_word_offset(offset, mode):
     assert torch.equal(a, b)
 
 
+@pytest.mark.parametrize("mode", ["union", "masked"])
+def test_batch_mlp_largest_neuron_count(mode):
+    """n = 131072, the largest neuron count of the batched path (the union kernel's
+    per-neuron marks then take 128 KB of LDS): per-sequence outputs match the oracle."""
+    cfg = _cfg("small_b8", 4).with_(name="n131072_b4", N=131072, k_mlp=3000)
+    t = make_layer(cfg, 27, device="cuda", biases=True, with_predictors=False)
+    sets = zipf_mlp_sets(cfg, 27)
+    idx = torch.tensor(sets, dtype=torch.int32, device="cuda")
+    bm = Bd.DV_MLP_UNION if mode == "union" else Bd.DV_MLP_MASKED
+    out = Bd.dv_sparse_mlp(_mlp(t), t["x"], idx, idx_per_seq=1, batch_mode=bm, flags=Bd.DV_VALIDATE)
+    _sync()
+    U = np.unique(sets)
+    W1, W2, b1 = host(t["W1T"])[U], host(t["W2T"])[U], host(t["b1"])[U]   # the union's rows only
+    pos = {int(u): i for i, u in enumerate(U)}
+    local = [np.array([pos[int(v)] for v in s_], dtype=np.int64).tolist() for s_ in sets]
+    ref = O.mlp_batch(host(t["x"]), W1, b1, W2, host(t["b2"]), local, mode)
+    got = host(out)
+    for b in range(cfg.B):
+        assert rel_l2(got[b], ref[b]) < REL_TOL, (b, rel_l2(got[b], ref[b]))
+
+
 def test_batch_mlp_union_differs_from_masked():
     """The two batch semantics give different outputs (the union adds other sequences' neurons)."""
     cfg = _cfg("small_b8")
