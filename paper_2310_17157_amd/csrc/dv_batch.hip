@@ -39,16 +39,6 @@ __device__ __forceinline__ v4s_t ds_read_tr16(const _Float16* p) {
       (v4s_t __attribute__((address_space(3)))*)(const_cast<_Float16*>(p)));
 }
 
-// Raises a kernel's dynamic LDS limit to the bytes a launch needs (above the 64 KB
-// default; the limit is per kernel, kept in *cur). The limit is the request itself,
-// not the device maximum: the kernel's static LDS has to fit beside it.
-static hipError_t ensure_dyn_lds(const void* kern, size_t bytes, int* cur) {
-  if (bytes <= 65536 || (int)bytes <= *cur) return hipSuccess;
-  const hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-  if (e == hipSuccess) *cur = (int)bytes;
-  return e;
-}
-
 static int lds_budget() {
   static int cached = 0;
   if (cached == 0) {

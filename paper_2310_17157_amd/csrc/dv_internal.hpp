@@ -351,6 +351,16 @@ struct AxpyArgs {
 constexpr int kAxpyMaxRowSplit = 32;
 constexpr int kAxpyMaxSpans = 64;     // column spans of 64 x 16 bytes at d <= 16000
 
+// Raises a kernel's dynamic LDS limit to the bytes a launch needs (above the 64 KB
+// default; the limit is per kernel, kept in *cur). The limit is the request itself,
+// not the device maximum: the kernel's static LDS has to fit beside it.
+inline hipError_t ensure_dyn_lds(const void* kern, size_t bytes, int* cur) {
+  if (bytes <= 65536 || (int)bytes <= *cur) return hipSuccess;
+  const hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  if (e == hipSuccess) *cur = (int)bytes;
+  return e;
+}
+
 // Clears n counters for a later row-axpy of the same call (agent-scope stores: the
 // counters are read by atomics from every XCD).
 __device__ __forceinline__ void clear_counters(uint32_t* c, int n) {

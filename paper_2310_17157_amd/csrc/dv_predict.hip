@@ -40,6 +40,11 @@ static hipError_t launch_pred_hidden_t(const PredHidArgs& a, hipStream_t st) {
   const int nrows = a.r0 + a.r1;
   const dim3 grid(max(1, min(nrows, device_cu_count())), a.B);
   const size_t lds = (size_t)(a.d + NW + rowdot_flat_part(nrows, grid.x, NW)) * sizeof(float);
+  static int cur[2] = {0, 0};   // (wide inputs and many rows per workgroup pass 64 KB)
+  const void* kern = a.g != nullptr ? reinterpret_cast<const void*>(k_pred_hidden<T, NW, U, KX, true>)
+                                    : reinterpret_cast<const void*>(k_pred_hidden<T, NW, U, KX, false>);
+  const hipError_t e = ensure_dyn_lds(kern, lds, &cur[a.g != nullptr]);
+  if (e != hipSuccess) return e;
   if (a.g != nullptr)
     hipLaunchKernelGGL((k_pred_hidden<T, NW, U, KX, true>), grid, dim3(NW * 64), lds, st, a);
   else
@@ -229,6 +234,16 @@ __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2 
   }
 }
 
+// (ranks of two predictors staged together pass 64 KB: up to 2 x 16000 floats)
+template <typename T, int NW, int G, int RU, int NR, bool EARLY>
+static hipError_t launch_scores_k(const PredScoreArgs& a, dim3 grid, size_t lds, hipStream_t st) {
+  static int cur = 0;
+  const hipError_t e = ensure_dyn_lds(reinterpret_cast<const void*>(k_pred_scores<T, NW, G, RU, NR, EARLY>), lds, &cur);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((k_pred_scores<T, NW, G, RU, NR, EARLY>), grid, dim3(NW * 64), lds, st, a);
+  return hipGetLastError();
+}
+
 template <typename T>
 static hipError_t launch_scores_t(const PredScoreArgs& a, hipStream_t st) {
   constexpr int NW = 8;
@@ -245,16 +260,14 @@ static hipError_t launch_scores_t(const PredScoreArgs& a, hipStream_t st) {
   if (nch > 32) {
     // 64 lanes per row, all chunks of a row up to 128 (r <= 1024 fp16) in one round;
     // groups of 2 rows, two in flight (measured fastest; groups of 1, 4 or 13 rows were slower)
-    if (early) hipLaunchKernelGGL((k_pred_scores<T, NW, 64, 2, 2, true>), grid, dim3(NW * 64), lds, st, a);
-    else hipLaunchKernelGGL((k_pred_scores<T, NW, 64, 2, 2, false>), grid, dim3(NW * 64), lds, st, a);
+    return early ? launch_scores_k<T, NW, 64, 2, 2, true>(a, grid, lds, st)
+                 : launch_scores_k<T, NW, 64, 2, 2, false>(a, grid, lds, st);
   } else if (nch > 16) {
-    if (early) hipLaunchKernelGGL((k_pred_scores<T, NW, 32, 8, 1, true>), grid, dim3(NW * 64), lds, st, a);
-    else hipLaunchKernelGGL((k_pred_scores<T, NW, 32, 8, 1, false>), grid, dim3(NW * 64), lds, st, a);
-  } else {
-    if (early) hipLaunchKernelGGL((k_pred_scores<T, NW, 16, 8, 1, true>), grid, dim3(NW * 64), lds, st, a);
-    else hipLaunchKernelGGL((k_pred_scores<T, NW, 16, 8, 1, false>), grid, dim3(NW * 64), lds, st, a);
+    return early ? launch_scores_k<T, NW, 32, 8, 1, true>(a, grid, lds, st)
+                 : launch_scores_k<T, NW, 32, 8, 1, false>(a, grid, lds, st);
   }
-  return hipGetLastError();
+  return early ? launch_scores_k<T, NW, 16, 8, 1, true>(a, grid, lds, st)
+               : launch_scores_k<T, NW, 16, 8, 1, false>(a, grid, lds, st);
 }
 
 hipError_t launch_pred_scores(int wtype, const PredScoreArgs& a, hipStream_t st) {

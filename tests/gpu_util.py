@@ -11,7 +11,8 @@ NEAR_TIE = 1e-3        # relative band around the k-th score inside which set me
 
 
 def layer(cfg_name, seed, **kw):
-    cfg = get_config(cfg_name)
+    """A seeded layer on the GPU for a named configuration (or a Config)."""
+    cfg = get_config(cfg_name) if isinstance(cfg_name, str) else cfg_name
     return cfg, make_layer(cfg, seed, device="cuda", **kw)
 
 

@@ -11,6 +11,7 @@ import torch
 from oracle import dejavu as O
 from paper_2310_17157_amd import binding as Bd
 from paper_2310_17157_amd.workload import layer_objects
+from synth import get_config
 from tests.gpu_util import (REL_TOL, check_topk_set, host, layer, near_tie_band, oracle_attn, oracle_ln,
                             oracle_mlp, rel_l2)
 
@@ -291,6 +292,23 @@ def test_sparse_block_is_deterministic():
         _sync()
         outs.append((host(out).tobytes(), host(hs).tobytes(), host(ms).tobytes()))
     assert outs[0] == outs[1]
+
+
+def test_sparse_block_at_the_width_limit():
+    """d = 16000, the widest input the row-dot kernels stage: with many rows per
+    workgroup their LDS passes 64 KB (QKV over 16 heads x 128 rows of each projection,
+    fc1 over 6000 neurons, the predictors' hidden layer at rank 3000)."""
+    cfg = get_config("small_f16").with_(name="d16000", d=16000, N=8192, H=32, dh=128, L=64, r=3000,
+                                        k_mlp=6000, k_heads=16)
+    _block(cfg, 45, Bd.DV_LOOKAHEAD)
+
+
+def test_sparse_block_at_the_rank_limit():
+    """Predictor rank 16000 for both predictors: the score launch stages both hidden
+    vectors, 128 KB of LDS."""
+    cfg = get_config("small_f16").with_(name="r16000", d=256, N=512, H=4, dh=64, L=40, r=16000,
+                                        k_mlp=100, k_heads=2)
+    _block(cfg, 46, Bd.DV_LOOKAHEAD)
 
 
 @pytest.mark.parametrize("name", ["opt6.7b_b1", "opt66b_b1", "opt175b_b1"])
