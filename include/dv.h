@@ -164,7 +164,7 @@ const char *dv_launch_label(int32_t i);
  *   count  [B] int32 device, out (may be NULL for top-k): |S| (threshold mode: the
  *          full count, which may exceed cap_idx).
  *   scores [B][n_out] fp32 device, out, or NULL: the raw scores s.
- * Limits: n_out <= 65536 for selection. Both functions compute the same thing;
+ * Limits: n_out <= 2^26 for selection. Both functions compute the same thing;
  * they differ only in launch tuning for a large (neurons) or small (heads) n_out.
  */
 size_t dv_predict_workspace_bytes(const dv_predictor *p, int32_t B);

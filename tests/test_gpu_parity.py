@@ -124,6 +124,32 @@ def test_select_paths_agree_with_oracle(n):
     assert host(idx)[0][:cap].tolist() == full[:cap]
 
 
+def test_select_streaming_path_agrees_with_oracle():
+    """More than 49152 scores do not fit the registers of one workgroup: the radix
+    select streams them from memory in every pass. Exact ties, top-k and threshold."""
+    n = 100000
+    d, r = 64, 8
+    AT = torch.zeros((r, d), dtype=torch.float32, device="cuda")
+    AT[0, 0] = 1.0
+    BT = torch.zeros((n, r), dtype=torch.float32, device="cuda")
+    vals = torch.tensor([float((i * 37) % 1009) - 500.0 for i in range(n)], device="cuda")
+    BT[:, 0] = vals
+    x = torch.zeros((1, d), dtype=torch.float32, device="cuda")
+    x[0, 0] = 1.0
+    pred = Bd.Predictor(AT, BT)
+    s = vals.cpu().double().numpy()
+    for k in (1, 5000, n - 1, n):
+        idx, _ = Bd.dv_predict_mlp(pred, x, k)
+        _sync()
+        assert host(idx)[0].tolist() == O.select_topk(s, k).tolist(), k
+    full = O.select_threshold(s, 400.0).tolist()
+    cap = len(full) - 7
+    idx, cnt = Bd.dv_predict_mlp(pred, x, mode=Bd.DV_SELECT_THRESHOLD, thresh=400.0, cap_idx=cap)
+    _sync()
+    assert int(cnt[0]) == len(full)
+    assert host(idx)[0][:cap].tolist() == full[:cap]
+
+
 # ------------------------------------------------------------------ sparse MLP
 @pytest.mark.parametrize("name", SMALL + ["opt6.7b_b1"])
 def test_sparse_mlp(name):
@@ -309,6 +335,14 @@ def test_sparse_block_at_the_rank_limit():
     cfg = get_config("small_f16").with_(name="r16000", d=256, N=512, H=4, dh=64, L=40, r=16000,
                                         k_mlp=100, k_heads=2)
     _block(cfg, 46, Bd.DV_LOOKAHEAD)
+
+
+def test_sparse_block_neuron_selection_streams_past_49152():
+    """65536 neurons: the neuron top-k hosted in the QKV launch streams the scores
+    (more than one workgroup's registers hold)."""
+    cfg = get_config("small_f16").with_(name="n65536", d=256, N=65536, H=4, dh=64, L=40, r=64,
+                                        k_mlp=3000, k_heads=2)
+    _block(cfg, 47, Bd.DV_LOOKAHEAD)
 
 
 @pytest.mark.parametrize("name", ["opt6.7b_b1", "opt66b_b1", "opt175b_b1"])
