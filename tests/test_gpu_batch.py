@@ -178,6 +178,19 @@ def test_batch_attn(B, kv_scale):
     _check_attn(cfg, t, heads, out, K0, V0)
 
 
+@pytest.mark.parametrize("kvd", ["f16", "f32"])
+def test_batch_attn_widest_heads(kvd):
+    """Heads of 256 on the batched path, with an fp16 or an fp32 cache."""
+    cfg = _cfg("small_b8", 4).with_(name=f"dh256_b4_{kvd}", d=1024, H=6, dh=256, k_heads=3, kvdtype=kvd)
+    t = make_layer(cfg, 34, device="cuda", biases=True)
+    K0, V0 = host(t["K"]).copy(), host(t["V"]).copy()
+    heads = uniform_head_sets(cfg, 34)
+    attn, _, _, _, kv, _ = layer_objects(t, cfg.H)
+    out = Bd.dv_sparse_attn(attn, t["x"], kv, torch.tensor(heads, device="cuda"), 1.0 / np.sqrt(cfg.dh))
+    _sync()
+    _check_attn(cfg, t, heads, out, K0, V0)
+
+
 def test_batch_attn_all_heads_and_pos0():
     cfg = _cfg("small_b8").with_(k_heads=10, L_range=(1, 2))
     t = make_layer(cfg, 32, device="cuda", biases=True)

@@ -226,6 +226,20 @@ def test_sparse_attn(name):
             assert Kg[h].tobytes() == K0[h].tobytes() and Vg[h].tobytes() == V0[h].tobytes()
 
 
+@pytest.mark.parametrize("wd,kvd", [("f16", "f16"), ("f32", "f32"), ("f16", "f32")])
+def test_sparse_attn_widest_heads_and_cache_types(wd, kvd):
+    """Heads of 256, the widest head the attention kernel takes, with each pairing of
+    weight and cache types (an fp32 cache beside fp16 weights included)."""
+    cfg = get_config("small_f16").with_(name=f"dh256_{wd}_{kvd}", d=1024, H=6, dh=256, L=300, k_heads=3,
+                                        wdtype=wd, kvdtype=kvd)
+    _, t, heads, p, out, ref, K0, V0, Kn, Vn = _attn_case(cfg, 33)
+    assert rel_l2(host(out)[0], ref) < REL_TOL
+    Kg, Vg = host(t["K"])[0], host(t["V"])[0]
+    for h in heads:
+        assert rel_l2(Kg[h, p].astype(np.float64), Kn[h, p]) < REL_TOL
+        assert rel_l2(Vg[h, p].astype(np.float64), Vn[h, p]) < REL_TOL
+
+
 def test_sparse_attn_peaky_scores_and_first_position():
     # Large logits exercise the max-subtracted softmax and the split-KV combine.
     cfg, t, heads, p, out, ref, *_ = _attn_case("small_f16", 32, kv_scale=30.0)
