@@ -220,6 +220,37 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   float M = -INFINITY;
 #pragma unroll
   for (int w = 0; w < NW; ++w) M = fmaxf(M, sm_m[w]);
+  if (a.C != nullptr) {
+    // one chunk: H_h(x_b)[t] = o[t] / L, as fp16 coefficients at h's place in the union
+    __shared__ int up;
+    if (threadIdx.x == 0) {
+      int lo = 0, hi = *a.ucount - 1, pp = -1;
+      while (lo <= hi) {
+        const int mid = (lo + hi) >> 1;
+        const int v = a.ulist[mid];
+        if (v == head) { pp = mid; break; }
+        if (v < head) lo = mid + 1; else hi = mid - 1;
+      }
+      up = pp;
+    }
+    __syncthreads();
+    if (up < 0 || M == -INFINITY) return;   // (the matrix was cleared)
+    float L = 0.f, f[NW];
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      f[w] = sm_m[w] == -INFINITY ? 0.f : __expf(sm_m[w] - M);
+      L += sm_l[w] * f[w];
+    }
+    const float rl = 1.f / L;
+    _Float16* o = a.C + (size_t)b * a.ldc + (size_t)up * a.dh;
+    for (int t = threadIdx.x; t < a.dh; t += 256) {
+      float acc = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) acc += sm_o[w][t] * f[w];
+      o[t] = (_Float16)(acc * rl);
+    }
+    return;
+  }
   float* out = a.part + ((size_t)jb * a.n_split + c) * (a.dh + 2);
   if (M == -INFINITY) {
     for (int t = threadIdx.x; t < a.dh + 2; t += 256) out[t] = t == 0 ? -INFINITY : 0.f;

@@ -766,6 +766,11 @@ __global__ void __launch_bounds__(1024) k_qkv_finish(QkvFinishArgs a) {
   extern __shared__ float qsm[];                  // [dh][NB + 1]
   __shared__ int jsel[NB];
   const int p = blockIdx.x, m = blockIdx.y;
+  if (a.zero != nullptr) {   // the attention's coefficient matrix, before it writes its part
+    const int wg = blockIdx.x + gridDim.x * blockIdx.y, nwg = gridDim.x * gridDim.y;
+    for (int i = wg * 1024 + (int)threadIdx.x; i < a.zero_n / 8; i += nwg * 1024)
+      reinterpret_cast<u32x4*>(a.zero)[i] = u32x4{0u, 0u, 0u, 0u};
+  }
   const int nu = *a.hcount;
   if (p >= nu) return;
   const int h = min(max(a.hlist[p], 0), a.H - 1);

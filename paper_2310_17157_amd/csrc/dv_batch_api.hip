@@ -158,18 +158,27 @@ static dv_status battn_run(const dv_attn* a, const dv_kv* kv, const BAttn& o, in
     qf.posb[b] = kv->pos[b];
     maxpos = std::max(maxpos, kv->pos[b]);
   }
-  DV_LAUNCH("qkv_finish", hs, launch_qkv_finish(NB, kv->ktype, qf, hs));
   AttnArgs at{};
   at.H = a->H; at.dh = a->dh; at.cap = kv->cap; at.n_heads = n_heads;
   for (int b = 0; b < B; ++b) at.posb[b] = kv->pos[b];
   at.chunk = attn_chunk(B * n_heads, maxpos + 1, a->dh, kv->ktype);
   at.n_split = (maxpos + 1 + at.chunk - 1) / at.chunk;
   at.q = o.q; at.heads = heads; at.K = kv->K; at.V = kv->V; at.scale = scale; at.part = o.part;
+  // One chunk per head (many sequences): the attention writes the coefficients itself,
+  // into a matrix the QKV finisher clears; otherwise a launch combines the chunks.
+  const bool direct = at.n_split == 1;
+  if (direct) {
+    qf.zero = o.C; qf.zero_n = NB * o.ldc;
+    at.C = o.C; at.ldc = o.ldc; at.ulist = o.Uh; at.ucount = o.hcnt;
+  }
+  DV_LAUNCH("qkv_finish", hs, launch_qkv_finish(NB, kv->ktype, qf, hs));
   DV_LAUNCH("attn", hs, launch_attn(kv->ktype, at, B, hs));
-  AttnFinishArgs af{};
-  af.part = o.part; af.n_split = at.n_split; af.n_heads = n_heads; af.dh = a->dh; af.B = B; af.heads = heads;
-  af.list = o.Uh; af.hcount = o.hcnt; af.C = o.C; af.ldc = o.ldc;
-  DV_LAUNCH("attn_finish", hs, launch_attn_finish(NB, af, hs));
+  if (!direct) {
+    AttnFinishArgs af{};
+    af.part = o.part; af.n_split = at.n_split; af.n_heads = n_heads; af.dh = a->dh; af.B = B; af.heads = heads;
+    af.list = o.Uh; af.hcount = o.hcnt; af.C = o.C; af.ldc = o.ldc;
+    DV_LAUNCH("attn_finish", hs, launch_attn_finish(NB, af, hs));
+  }
   McolsArgs c{};
   c.d = a->d; c.M = a->WoT; c.list = o.Uh; c.list_count = o.hcnt; c.list_max = a->H; c.dh = a->dh;
   c.list_range = a->H;

@@ -324,6 +324,10 @@ struct AttnArgs {
   const void* K; const void* V;     // [B][H][cap][dh]
   float scale;
   float* part;                      // [B][n_heads][n_split][dh + 2]
+  // One chunk per head (n_split == 1) and C set: the output H_h(x_b) goes straight to
+  // the out-projection's fp16 coefficients C[b][p * dh + t] (p: h's place in the union
+  // list ulist[0..*ucount)) instead of a partial; the rest of C is zeroed beforehand.
+  _Float16* C; int ldc; const int32_t* ulist; const int32_t* ucount;
 };
 hipError_t launch_attn(int kvtype, const AttnArgs& a, int B, hipStream_t st);
 
@@ -455,6 +459,7 @@ struct QkvFinishArgs {
   const float* bq; const float* bk; const float* bv;
   float* q; void* K; void* V;
   int posb[kMaxBatch];
+  _Float16* zero; int zero_n;       // optional: halves to clear (multiple of 8, 16-byte aligned)
 };
 hipError_t launch_qkv_finish(int NB, int kvtype, const QkvFinishArgs& a, hipStream_t st);
 
