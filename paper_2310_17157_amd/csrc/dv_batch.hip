@@ -96,14 +96,14 @@ __device__ __forceinline__ void union_scan(const int32_t* __restrict__ sets, int
 // Sum of four 0/1 bytes.
 __device__ __forceinline__ int byte_flags(uint32_t w) { return (int)((w * 0x01010101u) >> 24); }
 
-// Dynamic LDS: marks [round_up(n, 16)] bytes, then (mask only) kUnionChunk words.
+// Chunk c of nc; ush: dynamic LDS, marks [round_up(n, 16)] bytes, then (mask only)
+// kUnionChunk words.
 template <bool MASK>
-__global__ void __launch_bounds__(kUnionNT) k_union(const int32_t* __restrict__ sets, int B, int k, int n,
-                                                    int32_t* __restrict__ U, int32_t* __restrict__ count,
-                                                    uint32_t* __restrict__ mask) {
-  extern __shared__ __attribute__((aligned(16))) uint32_t ush[];
+__device__ __forceinline__ void union_chunk(const int32_t* __restrict__ sets, int B, int k, int n,
+                                            int32_t* __restrict__ U, int32_t* __restrict__ count,
+                                            uint32_t* __restrict__ mask, int c, int nc, uint32_t* ush) {
   __shared__ int red[kUnionNT / 64 + 1];
-  const int tid = threadIdx.x, c = blockIdx.x;
+  const int tid = threadIdx.x;
   const int lo = c * kUnionChunk, hi = min(n, lo + kUnionChunk);
   const int n16 = (n + 15) & ~15;
   uint8_t* mk = reinterpret_cast<uint8_t*>(ush);
@@ -141,7 +141,15 @@ __global__ void __launch_bounds__(kUnionNT) k_union(const int32_t* __restrict__ 
     U[r + f0] = i0 + 1;
     if (MASK) mask[r + f0] = mw[i0 + 1 - lo];
   }
-  if (c == (int)gridDim.x - 1 && tid == 0) *count = before + in_chunk;
+  if (c == nc - 1 && tid == 0) *count = before + in_chunk;
+}
+
+template <bool MASK>
+__global__ void __launch_bounds__(kUnionNT) k_union(const int32_t* __restrict__ sets, int B, int k, int n,
+                                                    int32_t* __restrict__ U, int32_t* __restrict__ count,
+                                                    uint32_t* __restrict__ mask) {
+  extern __shared__ __attribute__((aligned(16))) uint32_t ush[];
+  union_chunk<MASK>(sets, B, k, n, U, count, mask, blockIdx.x, gridDim.x, ush);
 }
 
 size_t union_lds_bytes(int n) { return (size_t)((n + 15) & ~15) + (size_t)kUnionChunk * 4; }
@@ -165,11 +173,10 @@ hipError_t launch_union(const int32_t* sets, int B, int k, int n, int32_t* U, in
 // --------------------------------------------------------------- x-hat cast
 // X16[b][0..Kpad) = fp16(LN(x[b])) (g == NULL: x[b]) for b < B; zero for b >= B
 // and for k >= d. One workgroup per row b of NB; d % 4 == 0, so rows move as float4.
-__global__ void __launch_bounds__(1024) k_ln_cast(const float* __restrict__ x, int B, int d, int Kpad,
-                                                  const float* __restrict__ g, const float* __restrict__ be,
-                                                  float eps, _Float16* __restrict__ X16) {
+__device__ __forceinline__ void ln_cast_row(const float* __restrict__ x, int B, int d, int Kpad,
+                                            const float* __restrict__ g, const float* __restrict__ be, float eps,
+                                            _Float16* __restrict__ X16, int b) {
   __shared__ float red[16];
-  const int b = blockIdx.x;
   _Float16* o = X16 + (size_t)b * Kpad;
   const int n4 = d >> 2;
   if (b >= B) {
@@ -212,9 +219,51 @@ __global__ void __launch_bounds__(1024) k_ln_cast(const float* __restrict__ x, i
   }
 }
 
+__global__ void __launch_bounds__(1024) k_ln_cast(const float* __restrict__ x, int B, int d, int Kpad,
+                                                  const float* __restrict__ g, const float* __restrict__ be,
+                                                  float eps, _Float16* __restrict__ X16) {
+  ln_cast_row(x, B, d, Kpad, g, be, eps, X16, blockIdx.x);
+}
+
+// The cast and the union of the batch's sets in one launch (they are independent):
+// workgroups [0, NB) cast row b, the next nc take union chunk c.
+template <bool MASK>
+__global__ void __launch_bounds__(1024) k_cast_union(const float* __restrict__ x, int B, int d, int Kpad,
+                                                     const float* __restrict__ g, const float* __restrict__ be,
+                                                     float eps, _Float16* __restrict__ X16, int NB,
+                                                     const int32_t* __restrict__ sets, int k, int n,
+                                                     int32_t* __restrict__ U, int32_t* __restrict__ count,
+                                                     uint32_t* __restrict__ mask, int nc) {
+  extern __shared__ __attribute__((aligned(16))) uint32_t ush[];
+  if ((int)blockIdx.x < NB)
+    ln_cast_row(x, B, d, Kpad, g, be, eps, X16, blockIdx.x);
+  else
+    union_chunk<MASK>(sets, B, k, n, U, count, mask, (int)blockIdx.x - NB, nc, ush);
+}
+
 hipError_t launch_ln_cast(const float* x, int B, int NB, int d, int Kpad, const float* g, const float* be, float eps,
                           _Float16* X16, hipStream_t st) {
   hipLaunchKernelGGL(k_ln_cast, dim3(NB), dim3(1024), 0, st, x, B, d, Kpad, g, be, eps, X16);
+  return hipGetLastError();
+}
+
+hipError_t launch_cast_union(const float* x, int B, int NB, int d, int Kpad, const float* g, const float* be,
+                             float eps, _Float16* X16, const int32_t* sets, int k, int n, int32_t* U,
+                             int32_t* count, uint32_t* mask, hipStream_t st) {
+  static_assert(kUnionNT == 1024, "the cast and the union share the workgroup size");
+  const int nc = (n + kUnionChunk - 1) / kUnionChunk;
+  const size_t lds = union_lds_bytes(n);
+  static int cur[2] = {0, 0};
+  const void* kern = mask != nullptr ? reinterpret_cast<const void*>(k_cast_union<true>)
+                                     : reinterpret_cast<const void*>(k_cast_union<false>);
+  const hipError_t e = ensure_dyn_lds(kern, lds, &cur[mask != nullptr]);
+  if (e != hipSuccess) return e;
+  if (mask != nullptr)
+    hipLaunchKernelGGL(k_cast_union<true>, dim3(NB + nc), dim3(1024), lds, st, x, B, d, Kpad, g, be, eps, X16, NB,
+                       sets, k, n, U, count, mask, nc);
+  else
+    hipLaunchKernelGGL(k_cast_union<false>, dim3(NB + nc), dim3(1024), lds, st, x, B, d, Kpad, g, be, eps, X16, NB,
+                       sets, k, n, U, count, mask, nc);
   return hipGetLastError();
 }
 

@@ -53,14 +53,16 @@ size_t batch_mlp_ws(const dv_mlp* m, int B, int n_idx, int per_seq) {
 }
 
 // The MLP on x16 (already normalised, fp16 [NB][Kpad]) for the sets `idx`.
+// union_done: the union (and masks) were built by the launch that cast x.
 static dv_status bmlp_run(const dv_mlp* m, const BMlp& o, int B, const int32_t* idx, int n_idx, bool per_seq,
-                          bool masked, const float* resid, float* out, hipStream_t hs) {
+                          bool masked, const float* resid, float* out, hipStream_t hs, bool union_done = false) {
   const int NB = batch_nb(B);
   const int32_t* list = idx;
   const int32_t* list_count = nullptr;
   int list_max = n_idx;
   if (per_seq) {
-    DV_LAUNCH("union", hs, launch_union(idx, B, n_idx, m->n, o.U, o.cnt, masked ? o.mask : nullptr, hs));
+    if (!union_done)
+      DV_LAUNCH("union", hs, launch_union(idx, B, n_idx, m->n, o.U, o.cnt, masked ? o.mask : nullptr, hs));
     list = o.U;
     list_count = o.cnt;
     list_max = o.umax;
@@ -95,8 +97,14 @@ dv_status batch_mlp(const dv_mlp* m, const float* x, int B, const int32_t* idx, 
     const dv_status st = validate_sets_sync(idx, per_seq ? B : 1, n_idx, m->n, o.cnt, hs);
     if (st != DV_OK) return st;
   }
+  const bool masked = batch_mode == DV_MLP_MASKED;
+  if (per_seq) {
+    DV_LAUNCH("xcast_union", hs, launch_cast_union(x, B, batch_nb(B), m->d, o.Kpad, nullptr, nullptr, 0.f, o.X16, idx,
+                                                   n_idx, m->n, o.U, o.cnt, masked ? o.mask : nullptr, hs));
+    return bmlp_run(m, o, B, idx, n_idx, true, masked, nullptr, out, hs, true);
+  }
   DV_LAUNCH("xcast", hs, launch_ln_cast(x, B, batch_nb(B), m->d, o.Kpad, nullptr, nullptr, 0.f, o.X16, hs));
-  return bmlp_run(m, o, B, idx, n_idx, per_seq != 0, batch_mode == DV_MLP_MASKED, nullptr, out, hs);
+  return bmlp_run(m, o, B, idx, n_idx, false, masked, nullptr, out, hs);
 }
 
 // ---------------------------------------------------------------- attention
@@ -133,8 +141,10 @@ size_t batch_attn_ws(const dv_attn* a, int B, int n_heads) {
 
 // Attention of every sequence on x16 (normalised fp16 [NB][Kpad]) for head sets
 // heads[B][n_heads]; out = resid + bo + sum_{h in S_A^b} H_h W^O_h.
+// union_done: the head union was built by the launch that cast x.
 static dv_status battn_run(const dv_attn* a, const dv_kv* kv, const BAttn& o, int B, const int32_t* heads,
-                           int n_heads, float scale, const float* resid, float* out, hipStream_t hs) {
+                           int n_heads, float scale, const float* resid, float* out, hipStream_t hs,
+                           bool union_done = false) {
   const int NB = batch_nb(B);
   if (n_heads == 0) {
     ColsFinishArgs e{};
@@ -142,7 +152,7 @@ static dv_status battn_run(const dv_attn* a, const dv_kv* kv, const BAttn& o, in
     DV_LAUNCH("oproj_finish", hs, launch_cols_finish(e, hs));
     return DV_OK;
   }
-  DV_LAUNCH("union_heads", hs, launch_union(heads, B, n_heads, a->H, o.Uh, o.hcnt, nullptr, hs));
+  if (!union_done) DV_LAUNCH("union_heads", hs, launch_union(heads, B, n_heads, a->H, o.Uh, o.hcnt, nullptr, hs));
   MrowsArgs r{};
   r.d = a->d; r.Kpad = o.Kpad; r.Ks = o.Ks; r.S = o.S; r.X = o.X16; r.mode = kRowsHeads;
   r.W0 = a->Wq; r.W1 = a->Wk; r.W2 = a->Wv; r.list = o.Uh; r.list_count = o.hcnt; r.list_max = a->H;
@@ -200,8 +210,9 @@ dv_status batch_attn(const dv_attn* a, const float* x, int B, const dv_kv* kv, c
     if (st != DV_OK) return st;
   }
   if (n_heads > 0)
-    DV_LAUNCH("xcast", hs, launch_ln_cast(x, B, batch_nb(B), a->d, o.Kpad, nullptr, nullptr, 0.f, o.X16, hs));
-  return battn_run(a, kv, o, B, heads, n_heads, scale, nullptr, out, hs);
+    DV_LAUNCH("xcast_union_heads", hs, launch_cast_union(x, B, batch_nb(B), a->d, o.Kpad, nullptr, nullptr, 0.f, o.X16,
+                                                         heads, n_heads, a->H, o.Uh, o.hcnt, nullptr, hs));
+  return battn_run(a, kv, o, B, heads, n_heads, scale, nullptr, out, hs, true);
 }
 
 // ---------------------------------------------------------------- layer
@@ -306,8 +317,14 @@ dv_status batch_block(const dv_attn* a, const dv_mlp* m, const dv_predictor* pa,
   // 2. y~ = y + MHA_{S_A}(LN1(y)).
   st = battn_run(a, kv, o.at, B, o.heads, kh, scale, x_in, o.yt, hs);
   if (st != DV_OK) return st;
-  // 3. LN2(y~) as fp16 (into the MLP's x-hat buffer); sequential mode predicts S_M here.
-  DV_LAUNCH("ln2", hs, launch_ln_cast(o.yt, B, NB, m->d, o.ml.Kpad, g2, be2, eps, o.ml.X16, hs));
+  // 3. LN2(y~) as fp16 (into the MLP's x-hat buffer), with the union of the neuron sets
+  //    in the same launch in look-ahead mode; sequential mode predicts S_M here.
+  const bool masked = batch_mode == DV_MLP_MASKED;
+  if (ahead)
+    DV_LAUNCH("ln2_union", hs, launch_cast_union(o.yt, B, NB, m->d, o.ml.Kpad, g2, be2, eps, o.ml.X16, o.idx, km,
+                                                 m->n, o.ml.U, o.ml.cnt, masked ? o.ml.mask : nullptr, hs));
+  else
+    DV_LAUNCH("ln2", hs, launch_ln_cast(o.yt, B, NB, m->d, o.ml.Kpad, g2, be2, eps, o.ml.X16, hs));
   if (!ahead) {
     st = bpredict(o, o.ml.X16, m->d, B, pm, o.Hm16, o.ldr1, o.s_m, nullptr, nullptr, 0, nullptr, hs);
     if (st != DV_OK) return st;
@@ -315,7 +332,7 @@ dv_status batch_block(const dv_attn* a, const dv_mlp* m, const dv_predictor* pa,
               launch_select(o.s_m, B, m->n, DV_SELECT_TOPK, km, 0.f, o.idx, km, nullptr, idx_out, hs));
   }
   // 4. y^ = y~ + MLP_{S_M}(LN2(y~)) on the union of the sets.
-  return bmlp_run(m, o.ml, B, o.idx, km, true, batch_mode == DV_MLP_MASKED, o.yt, x_out, hs);
+  return bmlp_run(m, o.ml, B, o.idx, km, true, masked, o.yt, x_out, hs, ahead);
 }
 
 }  // namespace dv

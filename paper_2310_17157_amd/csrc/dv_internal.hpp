@@ -394,6 +394,10 @@ hipError_t launch_union(const int32_t* sets, int B, int k, int n, int32_t* U, in
 // X16[NB][Kpad] = fp16(LN(x)) (g NULL: x), zero rows b >= B and columns k >= d.
 hipError_t launch_ln_cast(const float* x, int B, int NB, int d, int Kpad, const float* g, const float* be, float eps,
                           _Float16* X16, hipStream_t st);
+// The cast above and the union of the B sets (launch_union) in one launch.
+hipError_t launch_cast_union(const float* x, int B, int NB, int d, int Kpad, const float* g, const float* be,
+                             float eps, _Float16* X16, const int32_t* sets, int k, int n, int32_t* U,
+                             int32_t* count, uint32_t* mask, hipStream_t st);
 
 enum { kRowsList = 0, kRowsHeads = 1, kRowsIdentity = 2 };
 
