@@ -363,3 +363,9 @@ def test_sparse_block_neuron_selection_streams_past_49152():
 def test_sparse_block_full_size(name):
     """The full-size layers, at the launch configuration the benchmark times."""
     _block(name, 44, Bd.DV_LOOKAHEAD)
+
+
+def test_sparse_block_full_size_sequential():
+    """OPT-175B shape in sequential mode: the neuron predictor reads LN2(y~) after the
+    out-projection and selects 2457 of 49152 neurons in a launch of its own."""
+    _block("opt175b_b1", 48, Bd.DV_SEQUENTIAL)
