@@ -206,8 +206,9 @@ __device__ void wg_select(const float* __restrict__ s, int n, int mode, int k, f
 //
 // Slots past n hold key 0, which no real score produces (every finite or infinite
 // float maps above 2^22), so they fall in the lowest histogram bin, never match a
-// selected prefix, and need no separate validity test. The selection boundary is
-// re-read from LDS before the write walk so the compiler recomputes the per-key
+// selected prefix, and need no separate validity test (k >= n, where every score
+// is taken, writes 0..n-1 directly). The selection boundary is re-read from LDS,
+// wavefront-uniform, before the write walk, so the compiler recomputes the per-key
 // predicates instead of keeping them live across the scans.
 template <int NT, int IPT>
 __device__ void wg_select_reg(const float* __restrict__ s, int n, int mode, int k, float thresh,
@@ -242,8 +243,15 @@ __device__ void wg_select_reg(const float* __restrict__ s, int n, int mode, int 
     prefix = fkey(thresh);
     pbits = 32;
   } else if (k >= n) {
-    prefix = 0u;          // every real key is > 0
-    pbits = 32;
+    // every score, in index order (the padding slots' keys must not be counted)
+    const int m = min(n, cap);
+    for (int p = tid; p < m; p += NT) {
+      out[p] = p;
+      if (out2) out2[p] = p;
+    }
+    if (tid == 0 && count_out) *count_out = n;
+    __syncthreads();
+    return;
   } else if (k <= 0) {
     if (tid == 0 && count_out) *count_out = 0;
     __syncthreads();
@@ -283,14 +291,24 @@ __device__ void wg_select_reg(const float* __restrict__ s, int n, int mode, int 
     bound[0] = (int)prefix;
     bound[1] = 32 - pbits;
   }
-  // Per-wavefront totals (ballots: no cross-lane shuffles).
+  // A key is selected when its top pbits bits (13, 26 or 32 here, so the shift is
+  // below 32) exceed the prefix; of the keys equal to it, all are taken when eq_take
+  // is unbounded (threshold mode, or the last digit's bin was consumed exactly: the
+  // usual case, which needs one predicate per key), else the eq_take lowest-indexed.
+  // Per-wavefront totals from ballots (no cross-lane shuffles).
+  const bool all_eq = eq_take == INT_MAX;
   int sh = 32 - pbits;
   int ngt = 0, neq = 0;
+  if (all_eq) {
 #pragma unroll
-  for (int j = 0; j < IPT; ++j) {
-    const uint32_t u = shr32(key[j], sh);
-    ngt += __popcll(__ballot(u > prefix));
-    neq += __popcll(__ballot(u == prefix));
+    for (int j = 0; j < IPT; ++j) ngt += __popcll(__ballot((key[j] >> sh) >= prefix));
+  } else {
+#pragma unroll
+    for (int j = 0; j < IPT; ++j) {
+      const uint32_t u = key[j] >> sh;
+      ngt += __popcll(__ballot(u > prefix));
+      neq += __popcll(__ballot(u == prefix));
+    }
   }
   if (lane == 0) {
     sm[2 * wave] = ngt;
@@ -309,44 +327,90 @@ __device__ void wg_select_reg(const float* __restrict__ s, int n, int mode, int 
   }
   const int total = tgt + min(teq, eq_take);
   DV_SELECT_MARK(18);
-  prefix = (uint32_t)bound[0];
-  sh = bound[1];
+  prefix = (uint32_t)__builtin_amdgcn_readfirstlane(bound[0]);
+  sh = __builtin_amdgcn_readfirstlane(bound[1]);
   // Write walk: group by group; inside a group, lanes in order, then elements. The
   // rank of (lane l, element e) within the group is the number of selected elements
-  // of lanes below l (popcounts of four ballots under the lane mask) plus those of
-  // lane l before e.
-  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  // of lanes below l (mbcnt over the group's ballots) plus those of lane l before e.
+  // put(p, i, take) is called for every slot and stores index i at rank p if take.
+  auto below = [](uint64_t m, int acc) {
+    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, (uint32_t)acc));
+  };
+  auto walk_all = [&](auto put) {   // all_eq: one predicate, one running rank
+    int r = rg;
 #pragma unroll
-  for (int g = 0; g < G; ++g) {
-    bool gt[4], eq[4];
-    int bgt = 0, beq = 0, tg = 0, te = 0;
+    for (int g = 0; g < G; ++g) {
+      bool sl[4];
+      int bl = 0, t = 0;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const uint32_t u = shr32(key[4 * g + e], sh);
-      gt[e] = u > prefix;
-      eq[e] = u == prefix;
-      const uint64_t mg = __ballot(gt[e]), me = __ballot(eq[e]);
-      bgt += __popcll(mg & below);
-      beq += __popcll(me & below);
-      tg += __popcll(mg);
-      te += __popcll(me);
-    }
-    int pg = rg + bgt, pe = re + beq;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      if (gt[e] || (eq[e] && pe < eq_take)) {
-        const int p = pg + min(pe, eq_take);
-        if (p < cap) {
-          const int i = wbase + 256 * g + e;
-          out[p] = i;
-          if (out2) out2[p] = i;
-        }
+      for (int e = 0; e < 4; ++e) {
+        sl[e] = (key[4 * g + e] >> sh) >= prefix;
+        const uint64_t ms = __ballot(sl[e]);
+        bl = below(ms, bl);
+        t += __popcll(ms);
       }
-      pg += gt[e];
-      pe += eq[e];
+      int p = r + bl;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        put(p, wbase + 256 * g + e, sl[e] && p < cap);
+        p += sl[e];
+      }
+      r += t;
     }
-    rg += tg;
-    re += te;
+  };
+  auto walk_ties = [&](auto put) {  // above the prefix, plus the first eq_take equal keys
+    int r_gt = rg, r_eq = re;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      bool gt[4], eq[4];
+      int bgt = 0, beq = 0, tg = 0, te = 0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t u = key[4 * g + e] >> sh;
+        gt[e] = u > prefix;
+        eq[e] = u == prefix;
+        const uint64_t mg = __ballot(gt[e]), me = __ballot(eq[e]);
+        bgt = below(mg, bgt);
+        beq = below(me, beq);
+        tg += __popcll(mg);
+        te += __popcll(me);
+      }
+      int pg = r_gt + bgt, pe = r_eq + beq;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int p = pg + min(pe, eq_take);
+        put(p, wbase + 256 * g + e, (gt[e] || (eq[e] && pe < eq_take)) && p < cap);
+        pg += gt[e];
+        pe += eq[e];
+      }
+      r_gt += tg;
+      r_eq += te;
+    }
+  };
+  // A set that fits the histogram's LDS (less 64 slots that take the unselected lanes'
+  // writes, so the walk needs no branch) is placed there first and then copied out in
+  // contiguous runs; a larger one (threshold mode) is written directly.
+  const int m = min(total, cap);
+  if (m <= kSelBins - kWave) {
+    const int dummy = kSelBins - kWave + lane;
+    auto put = [&](int p, int i, bool take) { hist[take ? p : dummy] = (uint32_t)i; };
+    if (all_eq)
+      walk_all(put);
+    else
+      walk_ties(put);
+    __syncthreads();
+    for (int p = tid; p < m; p += NT) {
+      const int32_t i = (int32_t)hist[p];
+      out[p] = i;
+      if (out2) out2[p] = i;
+    }
+  } else {
+    walk_ties([&](int p, int i, bool take) {
+      if (take) {
+        out[p] = i;
+        if (out2) out2[p] = i;
+      }
+    });
   }
   DV_SELECT_MARK(19);
   if (tid == 0 && count_out) *count_out = total;
@@ -372,7 +436,7 @@ __device__ void wg_select_small(const float* __restrict__ s, int n, int mode, in
     if (mode == DV_SELECT_THRESHOLD) {
       sel = ki >= fkey(thresh);
     } else if (k >= n) {
-      sel = ki > 0u;          // every real key is > 0
+      sel = true;             // every score
     } else if (k > 0) {
       int rank = 0;
       for (int j = 0; j < n; ++j) {
@@ -394,15 +458,17 @@ __device__ void wg_select_small(const float* __restrict__ s, int n, int mode, in
 
 // Top-k selection run by one extra workgroup of another kernel's launch (which leaves
 // CUs free for it), so that the selection runs beside that kernel's weight stream
-// instead of on the critical path. Kept out of line so that its register allocation
-// does not constrain the host kernel's main path. Up to 48 * NT scores are selected
-// from registers, larger score vectors stream from memory. smem: kSelBins u32 plus
-// kSelSm(NT) ints of LDS.
+// instead of on the critical path. Inlined: as a call it needs a stack frame for the
+// callee-saved registers besides its own spills, which raised the host kernel's
+// private segment to 336 bytes per lane and its duration by 1.5-2 us on the
+// 3 x 4096-row QKV launch (inlined: 120 bytes).
+// Up to 48 * NT scores are selected from registers, larger score vectors stream from
+// memory. smem: kSelBins u32 plus kSelSm(NT) ints of LDS.
 constexpr int kSelIPT = 48;
 
 template <int NT>
-__device__ __noinline__ void hosted_select(const float* scores, int n, int k, int32_t* idx, int32_t* idx_out,
-                                           float* smem) {
+__device__ __forceinline__ void hosted_select(const float* scores, int n, int k, int32_t* idx,
+                                              int32_t* idx_out, float* smem) {
   uint32_t* hist = reinterpret_cast<uint32_t*>(smem);
   int* sm = reinterpret_cast<int*>(smem + kSelBins);
   if (n <= NT * kSelIPT)

@@ -113,12 +113,42 @@ def test_select_paths_agree_with_oracle(n):
     pred = Bd.Predictor(AT, BT)
     s = vals.cpu().double().numpy()
     for k in (1, n // 3, n - 1, n):
-        idx, _ = Bd.dv_predict_heads(pred, x, k)
+        idx, cnt = Bd.dv_predict_heads(pred, x, k)
         _sync()
         assert host(idx)[0].tolist() == O.select_topk(s, k).tolist(), (n, k)
+        assert int(cnt[0]) == k, (n, k)
     full = O.select_threshold(s, 2.0).tolist()
     cap = max(1, len(full) // 2)
     idx, cnt = Bd.dv_predict_heads(pred, x, mode=Bd.DV_SELECT_THRESHOLD, thresh=2.0, cap_idx=cap)
+    _sync()
+    assert int(cnt[0]) == len(full)
+    assert host(idx)[0][:cap].tolist() == full[:cap]
+
+
+def test_select_register_path_large_sets():
+    """Register-resident selection (n <= 49152) of sets too large to stage in LDS
+    (more than 8128 members) is written straight to memory: top-k with and without a
+    tie at the boundary, and threshold mode with the count above the capacity."""
+    n = 40000
+    d, r = 64, 8
+    AT = torch.zeros((r, d), dtype=torch.float32, device="cuda")
+    AT[0, 0] = 1.0
+    BT = torch.zeros((n, r), dtype=torch.float32, device="cuda")
+    vals = torch.tensor([float((i * 37) % 1009) - 500.0 for i in range(n)], device="cuda")
+    BT[:, 0] = vals
+    x = torch.zeros((1, d), dtype=torch.float32, device="cuda")
+    x[0, 0] = 1.0
+    pred = Bd.Predictor(AT, BT)
+    s = vals.cpu().double().numpy()
+    for k in (8128, 8129, 9000, 20000, 39999):
+        idx, cnt = Bd.dv_predict_mlp(pred, x, k)
+        _sync()
+        assert host(idx)[0].tolist() == O.select_topk(s, k).tolist(), k
+        assert int(cnt[0]) == k, k
+    full = O.select_threshold(s, 0.0).tolist()
+    assert len(full) > 8128
+    cap = len(full) - 7
+    idx, cnt = Bd.dv_predict_mlp(pred, x, mode=Bd.DV_SELECT_THRESHOLD, thresh=0.0, cap_idx=cap)
     _sync()
     assert int(cnt[0]) == len(full)
     assert host(idx)[0][:cap].tolist() == full[:cap]
@@ -139,9 +169,10 @@ def test_select_streaming_path_agrees_with_oracle():
     pred = Bd.Predictor(AT, BT)
     s = vals.cpu().double().numpy()
     for k in (1, 5000, n - 1, n):
-        idx, _ = Bd.dv_predict_mlp(pred, x, k)
+        idx, cnt = Bd.dv_predict_mlp(pred, x, k)
         _sync()
         assert host(idx)[0].tolist() == O.select_topk(s, k).tolist(), k
+        assert int(cnt[0]) == k, k
     full = O.select_threshold(s, 400.0).tolist()
     cap = len(full) - 7
     idx, cnt = Bd.dv_predict_mlp(pred, x, mode=Bd.DV_SELECT_THRESHOLD, thresh=400.0, cap_idx=cap)
