@@ -157,8 +157,10 @@ const char *dv_launch_label(int32_t i);
 /* ---------------------------------------------------------------- predictors
  * dv_predict_mlp / dv_predict_heads: S = select(s), s = (x A) B (Sections 4.1-4.2).
  *   x      [B][d] fp32 device: the predictor input (already normalised, if any).
- *   mode   DV_SELECT_TOPK: the k highest scores, ties to the lower index;
- *          DV_SELECT_THRESHOLD: every i with s_i >= thresh (k ignored).
+ *   mode   DV_SELECT_TOPK: the k highest scores, ties to the lower index, for
+ *          0 <= k <= n_out (else DV_ERR_SHAPE; k = n_out gives 0..n_out-1);
+ *          DV_SELECT_THRESHOLD: every i with s_i >= thresh (k ignored). Scores are
+ *          ordered as floats with -0 = +0; a NaN score gives an unspecified set.
  *   idx    [B][cap_idx] int32 device, out: each sequence's set, ascending. Top-k
  *          needs cap_idx >= k. Threshold mode writes the first cap_idx members.
  *   count  [B] int32 device, out (may be NULL for top-k): |S| (threshold mode: the
