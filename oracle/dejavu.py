@@ -342,6 +342,30 @@ def mlp_batch(Y, W1T, b1, W2T, b2, sets, mode: str = "union") -> np.ndarray:
     return np.stack([mlp_sparse(Y[b], W1T, b1, W2T, b2, sets[b]) for b in range(Y.shape[0])])
 
 
+def mlp_union_rows(Y, W1T, b1, W2T, b2, U, rows_per_step: int = 2048) -> np.ndarray:
+    """Eq. (1) on the rows U for every sequence of a batch, as matrix products.
+
+    out[b] = b2 + sum_{i in U} ReLU(Y[b] . W^1_i + b1_i) W^2_i, taken over slices of U
+    (rows_per_step neurons at a time, so that a slice of fp16 rows upcast to float64
+    stays small). The same sum as mlp_sparse for each sequence, grouped by slices
+    of neurons instead of one neuron at a time. Y: [B, d]; returns [B, d].
+    """
+    Y = _f64(Y)
+    W1T = np.asarray(W1T)
+    W2T = np.asarray(W2T)
+    U = np.asarray(U, dtype=np.int64)
+    out = np.zeros((Y.shape[0], W1T.shape[1]), dtype=F64)
+    if b2 is not None:
+        out += _f64(b2)
+    for c0 in range(0, U.shape[0], rows_per_step):
+        rows = U[c0:c0 + rows_per_step]
+        z = Y @ _f64(W1T[rows]).T                 # [B, rows]
+        if b1 is not None:
+            z = z + _f64(b1)[rows]
+        out += np.maximum(z, 0.0) @ _f64(W2T[rows])
+    return out
+
+
 def mha_batch(Y, attn: Dict, K, V, pos: Sequence[int], head_sets, scale: float):
     """Batched sparse MHA: sequence b uses its own head set, cache K[b], V[b] and pos[b].
 

@@ -91,3 +91,28 @@ def test_union_and_batched_forms():
     for b, p in enumerate([3, 8, 0]):
         ref, Kr, _, _ = O.mha_sparse(Y[b], attn, Kb[b], Vb[b], p, sorted(hs[b]), 0.3)
         assert np.array_equal(out[b], ref) and np.array_equal(Kn[b], Kr)
+
+
+@pytest.mark.parametrize("step", [1, 5, 2048])
+def test_union_rows_matrix_form_equals_gather_form(step):
+    """mlp_union_rows (slices of neurons as matrix products, the form used to check the
+    batch-32 union MLP at full size) against mlp_sparse one neuron at a time, and against
+    the mask form; a dropped bias, a wrong slice bound or a transposed factor would
+    differ."""
+    rng = np.random.default_rng(34)
+    _, mlp, *_ = _layer(rng, N=48)
+    Y = rng.normal(size=(5, 24))
+    sets = [np.sort(rng.choice(48, 9, replace=False)) for _ in range(5)]
+    U = O.union_of_sets(sets)
+    got = O.mlp_union_rows(Y, mlp["W1T"], mlp["b1"], mlp["W2T"], mlp["b2"], U, rows_per_step=step)
+    for b in range(5):
+        ref = O.mlp_sparse(Y[b], mlp["W1T"], mlp["b1"], mlp["W2T"], mlp["b2"], U)
+        assert _rel(got[b], ref) < 1e-13
+        assert _rel(got[b], O.mlp_sparse_masked(Y[b], mlp["W1T"], mlp["b1"], mlp["W2T"], mlp["b2"], U)) < 1e-13
+    # no biases, fp16 storage: the rows are upcast exactly
+    W1 = mlp["W1T"].astype(np.float16)
+    W2 = mlp["W2T"].astype(np.float16)
+    got = O.mlp_union_rows(Y, W1, None, W2, None, U, rows_per_step=step)
+    assert _rel(got[2], O.mlp_sparse(Y[2], W1, None, W2, None, U)) < 1e-13
+    # the empty union leaves b2
+    assert np.array_equal(O.mlp_union_rows(Y, W1, None, W2, mlp["b2"], [])[3], mlp["b2"])
