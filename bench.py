@@ -112,34 +112,167 @@ def counter_traffic(workload, label):
         return None
 
 
-def cpu_baseline(cfg, t_host, pos, seconds=10.0):
-    """The fp64 oracle's predict + sparse block for one token of this workload."""
-    import numpy as np
-    from oracle import dejavu as O
+def _blas_threads():
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        return max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
-        threads = 1
-    h = t_host
+        return 1
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _oracle_sparse_step(O, cfg, h, pos):
+    """One token through the oracle: both predictors, top-k and the sparse layer."""
+    import numpy as np
     lno = dict(g1=h["g1"], be1=h["be1"], g2=h["g2"], be2=h["be2"], eps=1e-5)
     attn = {k: h[k] for k in ("Wq", "Wk", "Wv", "WoT", "bq", "bk", "bv", "bo")}
     mlp = {k: h[k] for k in ("W1T", "W2T", "b1", "b2")}
-    runs = []
-    t_end = time.perf_counter() + seconds
-    while True:
+    return O.sparse_block(h["x"][0], attn, mlp, h["K"][0], h["V"][0], pos, 1.0 / np.sqrt(cfg.dh),
+                          pred_h=dict(AT=h["AT_h"], BT=h["BT_h"]), pred_m=dict(AT=h["AT_m"], BT=h["BT_m"]),
+                          k_heads=cfg.k_heads, k_mlp=cfg.k_mlp, ln=lno, mode="lookahead")
+
+
+def _oracle_dense_step(O, cfg, h, pos):
+    import numpy as np
+    lno = dict(g1=h["g1"], be1=h["be1"], g2=h["g2"], be2=h["be2"], eps=1e-5)
+    attn = {k: h[k] for k in ("Wq", "Wk", "Wv", "WoT", "bq", "bk", "bv", "bo")}
+    mlp = {k: h[k] for k in ("W1T", "W2T", "b1", "b2")}
+    return O.dense_block(h["x"][0], attn, mlp, h["K"][0], h["V"][0], pos, 1.0 / np.sqrt(cfg.dh), ln=lno)
+
+
+def _timed(fn, runs):
+    ts = []
+    for _ in range(runs):
         t0 = time.perf_counter()
-        O.sparse_block(h["x"][0], attn, mlp, h["K"][0], h["V"][0], pos, 1.0 / np.sqrt(cfg.dh),
-                       pred_h=dict(AT=h["AT_h"], BT=h["BT_h"]), pred_m=dict(AT=h["AT_m"], BT=h["BT_m"]),
-                       k_heads=cfg.k_heads, k_mlp=cfg.k_mlp, ln=lno, mode="lookahead")
-        runs.append(time.perf_counter() - t0)
-        if time.perf_counter() > t_end or len(runs) >= 3:
-            break
-    med = statistics.median(runs)
-    return {"value": med * 1e6, "unit": "us/layer/token", "cores": threads, "kind": "oracle",
-            "sample": f"{len(runs)} run(s) of the full predict + sparse block for one token of "
-                      f"{cfg.name} (same seeded layer), median; host cores visible: "
-                      f"{len(os.sched_getaffinity(0))}"}
+        fn()
+        ts.append(time.perf_counter() - t0)
+    return statistics.median(ts) * 1e6
+
+
+def cpu_baseline(cfg, t_host, pos, small_configs=("opt125m_b1", "opt6.7b_b1", "opt66b_b1")):
+    """The fp64 oracle on this host: the predict + sparse layer for one token of the
+    benchmark's own workload (median of 3, all BLAS threads, and once on 1 thread), and
+    the sparse and dense layers of the smaller OPT shapes (median of 3 / 1 run)."""
+    from oracle import dejavu as O
+    from synth import get_config, make_layer
+    threads = _blas_threads()
+    value = _timed(lambda: _oracle_sparse_step(O, cfg, t_host, pos), 3)
+    one = None
+    try:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1):
+            one = round(_timed(lambda: _oracle_sparse_step(O, cfg, t_host, pos), 1), 1)
+    except Exception:  # pragma: no cover
+        pass
+    by_cfg = {}
+    for name in small_configs:
+        c = get_config(name)
+        h = _host_copy(make_layer(c, 0, device="cuda", biases=False, ln_random=False))
+        p = c.L - 1
+        by_cfg[name] = {"sparse_us": round(_timed(lambda: _oracle_sparse_step(O, c, h, p), 3), 1),
+                        "dense_us": round(_timed(lambda: _oracle_dense_step(O, c, h, p), 1 if c.d > 4096 else 3), 1)}
+        del h
+    return {"value": value, "unit": "us/layer/token", "cores": threads, "kind": "oracle",
+            "sample": f"the fp64 oracle's predict + sparse layer for one token of {cfg.name} (the same seeded "
+                      f"layer as replica 0), median of 3 runs on {threads} BLAS threads; host cores visible: "
+                      f"{len(os.sched_getaffinity(0))}",
+            "cpu_model": _cpu_model(), "one_thread_us": one, "by_config": by_cfg}
+
+
+class StepEvents:
+    """Timing-only HIP events (no system fence) recorded around whole steps on a stream."""
+
+    def __init__(self, n):
+        import ctypes
+        from ctypes import POINTER, c_float, c_void_p
+        self._ct = ctypes
+        self._hip = ctypes.CDLL("libamdhip64.so")
+        self._hip.hipEventCreateWithFlags.argtypes = [POINTER(c_void_p), ctypes.c_uint]
+        self._hip.hipEventRecord.argtypes = [c_void_p, c_void_p]
+        self._hip.hipEventElapsedTime.argtypes = [POINTER(c_float), c_void_p, c_void_p]
+        self._hip.hipEventSynchronize.argtypes = [c_void_p]
+        self._hip.hipEventDestroy.argtypes = [c_void_p]
+        self.ev = []
+        for _ in range(2 * n):
+            e = c_void_p()
+            if self._hip.hipEventCreateWithFlags(ctypes.byref(e), 0x20000000) != 0:
+                raise RuntimeError("hipEventCreateWithFlags failed")
+            self.ev.append(e)
+
+    def record(self, i, stream):
+        self._hip.hipEventRecord(self.ev[i], stream.cuda_stream)
+
+    def ms(self, i):
+        a, b = self.ev[2 * i], self.ev[2 * i + 1]
+        self._hip.hipEventSynchronize(b)
+        out = self._ct.c_float(0.0)
+        self._hip.hipEventElapsedTime(self._ct.byref(out), a, b)
+        return out.value
+
+    def close(self):
+        for e in self.ev:
+            self._hip.hipEventDestroy(e)
+
+
+def step_spread(stream, step, n):
+    """p10 / p50 / p90 of single steps, each bracketed by its own pair of timing-only
+    events (the events leave the GPU idle for a few microseconds each, so this pass is
+    reported beside the unbracketed window mean, not instead of it)."""
+    import torch
+    ev = StepEvents(n)
+    torch.cuda.synchronize()
+    for i in range(n):
+        ev.record(2 * i, stream)
+        step(i)
+        ev.record(2 * i + 1, stream)
+    torch.cuda.synchronize()
+    v = sorted(ev.ms(i) * 1e3 for i in range(n))
+    ev.close()
+    q = lambda f: round(v[min(n - 1, int(f * (n - 1) + 0.5))], 2)
+    return {"steps": n, "p10_us": q(0.1), "p50_us": q(0.5), "p90_us": q(0.9), "min_us": round(v[0], 2),
+            "max_us": round(v[-1], 2)}
+
+
+def stream_ceiling(nbytes_list, steps, replicas=4):
+    """The plain streaming read (dv_stream_read) of each byte count, rotating over
+    `replicas` buffers (beyond the 256 MB Infinity Cache); launch averages from events
+    on the stream."""
+    import torch
+    from paper_2310_17157_amd import binding as Bd
+    top = max(nbytes_list)
+    bufs = [torch.empty(top, dtype=torch.uint8, device="cuda") for _ in range(replicas)]
+    sink = torch.zeros(1, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    out = {}
+    for nb in nbytes_list:
+        nb16 = nb // 16 * 16
+
+        def step(i, timers=None):
+            if timers:
+                timers[0].arm()
+            Bd.dv_stream_read(bufs[i % replicas], sink, nb16, stream=stream)
+            if timers:
+                timers[0].disarm()
+
+        for i in range(5):
+            step(i)
+        _, _, per = _measure(stream, step, steps, 1)
+        us = statistics.mean(per["stream_read"]) * 1e3
+        out[str(nb)] = {"bytes": nb16, "avg_launch_us": round(us, 2), "GBps": round(nb16 / us / 1e3, 1),
+                        "frac": round(nb16 / us / 1e3 / PEAK_HBM_GBPS, 4)}
+    del bufs
+    torch.cuda.empty_cache()
+    return out
 
 
 def _measure(stream, step, n, calls_per_step, only=None, every=1):
@@ -195,6 +328,10 @@ def _host_copy(t, keys=None):
     return out
 
 
+BLOCK_KERNELS = ("qkv", "attn", "oproj", "fc1", "fc2")   # the sparse layer itself (not the predictors)
+TARGET_FRAC = 0.70                                        # of peak HBM bandwidth, over the block's bytes
+
+
 def bench_b1(args, cfg):
     import numpy as np
     import torch
@@ -244,36 +381,62 @@ def bench_b1(args, cfg):
     # Timed region: events around the dominant kernel's launch on every
     # ROOFLINE_EVERY-th step (each event record idles the GPU for a few microseconds).
     ms_per_step, wall, per_dom = _measure(stream, step, args.steps, 1, only=dom, every=ROOFLINE_EVERY)
+    # Each block kernel timed the same way in a pass of its own (launch averages for
+    # the block roofline).
+    per_one = {dom: per_dom[dom]}
+    for lab in BLOCK_KERNELS:
+        if lab != dom and lab in per_kernel:
+            per_one[lab] = _measure(stream, step, args.steps, 1, only=lab, every=4)[2][lab]
     kernels = _kernel_table(per_kernel, kb.get)
+    for lab, v in per_one.items():
+        kernels[lab]["avg_us_alone"] = round(statistics.mean(v) * 1e3, 2)
     dom_avg_s = statistics.mean(per_dom[dom]) * 1e-3
     achieved = kb[dom] / dom_avg_s / 1e9
     b = accounting.layer_bytes(cfg)
-    roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
-                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
+    spread = step_spread(stream, step, args.steps)
+
+    # measured ceiling: a plain contiguous read of the block's bytes and of the step's bytes
+    torch.cuda.set_stream(torch.cuda.default_stream())
+    ceil = stream_ceiling([b.block, b.total, kb[dom]], args.steps)
+    torch.cuda.set_stream(stream)
+    blk_us = sum(statistics.mean(per_one[k]) * 1e3 for k in BLOCK_KERNELS if k in per_one)
+    blk_gbps = b.block / (blk_us * 1e-6) / 1e9
+    block = {"kernels": list(BLOCK_KERNELS), "bytes": b.block, "us": round(blk_us, 2),
+             "achieved": round(blk_gbps, 1), "frac": round(blk_gbps / PEAK_HBM_GBPS, 4),
+             "target_frac": TARGET_FRAC, "met": bool(blk_gbps / PEAK_HBM_GBPS >= TARGET_FRAC),
+             "stream_same_bytes_GBps": ceil[str(b.block)]["GBps"],
+             "frac_vs_measured_stream": round(blk_gbps / ceil[str(b.block)]["GBps"], 4)}
+    roofline = {"bound": "hbm", "kernel": dom, "scope": "dominant kernel", "achieved": round(achieved, 1),
+                "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
                 "traffic": counter_traffic(cfg.name, dom),
-                "bytes_per_launch": kb[dom], "avg_launch_us": round(dom_avg_s * 1e6, 2)}
-    blk_us = round(sum(kernels[k]["avg_us"] for k in ("qkv", "attn", "oproj", "fc1", "fc2") if k in kernels), 2)
+                "bytes_per_launch": kb[dom], "avg_launch_us": round(dom_avg_s * 1e6, 2),
+                "frac_vs_measured_stream": round(achieved / ceil[str(kb[dom])]["GBps"], 4),
+                "block": block}
+    step_gbps = b.total / (ms_per_step * 1e-3) / 1e9
     hbm = {"block_bytes": b.block, "predictor_bytes": b.pred, "total_bytes": b.total,
-           "step_GBps": round(b.total / (ms_per_step * 1e-3) / 1e9, 1),
-           "step_frac": round(b.total / (ms_per_step * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
-           "sparse_block_kernels_us": blk_us,
-           "sparse_block_kernels_frac": round(b.block / (blk_us * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4) if blk_us else None}
+           "step_GBps": round(step_gbps, 1), "step_frac": round(step_gbps / PEAK_HBM_GBPS, 4),
+           "step_frac_vs_measured_stream": round(step_gbps / ceil[str(b.total)]["GBps"], 4),
+           "sparse_block_kernels_us": block["us"], "sparse_block_kernels_frac": block["frac"],
+           "stream_ceiling": ceil}
 
     cpu = None
     if not args.no_cpu_baseline:
         print("[bench] timing the fp64 oracle on the host", file=sys.stderr, flush=True)
         cpu = cpu_baseline(cfg, _host_copy(layers[0][0]), pos)
+    del layers
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
 
     return {
         "metric": METRIC, "value": round(ms_per_step * 1e3, 2), "unit": "us/layer/token", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
-        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "f16 weights, f32 accumulate",
         "data": "synthetic",
         "config": {"workload": cfg.name, "d_model": cfg.d, "ffn": cfg.N, "heads": cfg.H, "head_dim": cfg.dh,
                    "kv_len": cfg.L, "rank": cfg.r, "k_mlp": cfg.k_mlp, "k_heads": cfg.k_heads, "batch": 1,
                    "weights": cfg.wdtype, "kv": cfg.kvdtype, "mode": args.mode, "replicas": args.replicas,
                    "parallelism": "none (1 GPU)"},
-        "roofline": roofline, "cpu_baseline": cpu, "hbm": hbm, "kernels": kernels,
+        "roofline": roofline, "cpu_baseline": cpu, "hbm": hbm, "step_spread": spread, "kernels": kernels,
         "wall_s_timed": round(wall, 4), "ms_per_step_all_launch_events": round(ms_all_events, 5),
     }
 
@@ -396,6 +559,8 @@ def main():
     ap.add_argument("--replicas", type=int, default=4)
     ap.add_argument("--mode", choices=["lookahead", "sequential"], default="lookahead")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-b32", dest="b32", action="store_false",
+                    help="skip the batch-32 sub-record of the default batch-1 run")
     ap.add_argument("--copy-calib-gib", type=float, default=0.0,
                     help="only run a plain device-to-device copy of this many GiB (counter calibration)")
     args = ap.parse_args()
@@ -421,6 +586,14 @@ def main():
 
     cfg = get_config(args.workload)
     rec = bench_b1(args, cfg) if cfg.B == 1 else bench_batch(args, cfg)
+    if cfg.B == 1 and args.b32 and cfg.name == "opt175b_b1":
+        # the batch-32 workload of the same layer shape, as a sub-record of the line
+        print("[bench] batch-32 sub-record", file=sys.stderr, flush=True)
+        a32 = argparse.Namespace(**vars(args))
+        a32.no_cpu_baseline = True
+        r32 = bench_batch(a32, get_config("opt175b_b32"))
+        rec["b32"] = {k: r32[k] for k in ("metric", "value", "unit", "ms_per_step", "dtype", "config", "roofline",
+                                          "hbm", "kernels")}
     print(json.dumps(rec))
 
 

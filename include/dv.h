@@ -15,11 +15,16 @@
  *
  * Conventions shared by every entry point
  *   Memory.   Every array pointer is a DEVICE pointer owned by the caller, except
- *             dv_kv.pos, which is a HOST array. The library never allocates or
- *             frees memory on these paths and keeps no per-call state; scratch
- *             space is the caller's workspace `ws` of at least the size returned
- *             by the matching *_workspace_bytes query (256-byte aligned). Calls
- *             that share a workspace must be ordered on one stream.
+ *             dv_kv.pos, which is a HOST array (the attention grid is sized from
+ *             it on the host). The library never allocates or frees memory on
+ *             these paths and keeps no per-call state; scratch space is the
+ *             caller's workspace `ws` of at least the size returned by the
+ *             matching *_workspace_bytes query (256-byte aligned). Calls that
+ *             share a workspace must be ordered on one stream. Global state is
+ *             limited to a thread-safe per-device cache (CU count, LDS size,
+ *             which kernels had their LDS limit raised) and the per-thread
+ *             launch-event hook below; entry points may be called from several
+ *             threads and on several devices.
  *   Layout.   Row-major. A weight row is 16-byte aligned: base pointers must be
  *             16-byte aligned and d (and r for predictors) a multiple of 8 for
  *             fp16 or 4 for fp32 elements.
@@ -153,6 +158,14 @@ int32_t dv_abi_version(void);
  * disarm. Returns DV_ERR_SHAPE if n_pairs < 0. */
 dv_status dv_set_launch_events(void **events, int32_t n_pairs, int32_t *n_launched, const char *only);
 const char *dv_launch_label(int32_t i);
+
+/* Measured ceiling (measurement aid, not part of the method): reads `bytes` bytes of
+ * the device buffer `buf` once, contiguously, with the same 16-byte non-temporal loads
+ * the gathered kernels use, and nothing else. `bytes` must be a multiple of 16 and
+ * `buf` 16-byte aligned (else DV_ERR_ALIGN); `sink` is one device float that is never
+ * written in practice (it keeps the loads from being removed). The gathered kernels'
+ * bandwidth is reported against this plain stream of the same byte count. */
+dv_status dv_stream_read(const void *buf, size_t bytes, float *sink, void *stream);
 
 /* ---------------------------------------------------------------- predictors
  * dv_predict_mlp / dv_predict_heads: S = select(s), s = (x A) B (Sections 4.1-4.2).

@@ -74,6 +74,7 @@ _SIGS = {
     "dv_set_launch_events": (c_int32, [POINTER(c_void_p), c_int32, POINTER(c_int32), c_char_p]),
     "dv_launch_label": (c_char_p, [c_int32]),
     "dv_abi_version": (c_int32, []),
+    "dv_stream_read": (c_int32, [c_void_p, c_size_t, c_void_p, c_void_p]),
     "dv_predict_workspace_bytes": (c_size_t, [POINTER(CPredictor), c_int32]),
     "dv_predict_mlp": (c_int32, _PRED_ARGS),
     "dv_predict_heads": (c_int32, _PRED_ARGS),
@@ -127,6 +128,51 @@ def _wtype(t: torch.Tensor) -> int:
     raise TypeError(f"unsupported storage dtype {t.dtype}")
 
 
+_F32 = (torch.float32,)
+_I32 = (torch.int32,)
+_STORE = (torch.float16, torch.float32)
+
+
+def _tensor(name, t, dtypes, ndim=None, shape=None, optional=False, dev=True):
+    """Argument check before anything reaches the library: dtype, rank, shape,
+    contiguity and device. The kernels read raw pointers, so a wrong dtype or a strided
+    view would be read as something else (or past its end)."""
+    if t is None:
+        if optional:
+            return
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor, not {type(t).__name__}")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name} has dtype {t.dtype}; expected {' or '.join(str(d) for d in dtypes)}")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must be {ndim}-D, got shape {tuple(t.shape)}")
+    if shape is not None and any(w is not None and w != g for w, g in zip(shape, t.shape)):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}; expected {tuple(shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dev:
+        _gpu(name, t)
+
+
+def _gpu(name, *ts):
+    for t in ts:
+        if t is not None and t.device.type != "cuda":
+            raise ValueError(f"{name} must be a GPU tensor, not on {t.device}")
+
+
+def _wsarg(ws):
+    """(pointer, bytes) of a workspace: a contiguous uint8 GPU tensor."""
+    _tensor("ws", ws, (torch.uint8,), 1)
+    return ws.data_ptr(), ws.numel()
+
+
+def _same_dtype(name, *ts):
+    ds = {t.dtype for t in ts if t is not None}
+    if len(ds) > 1:
+        raise TypeError(f"{name}: all weights must share one dtype, got {sorted(str(d) for d in ds)}")
+
+
 def _stream(stream) -> Optional[int]:
     if stream is None:
         return torch.cuda.current_stream().cuda_stream
@@ -150,8 +196,17 @@ class Predictor:
     BT: torch.Tensor
 
     def c(self) -> CPredictor:
-        r, d = self.AT.shape
-        return CPredictor(d, r, self.BT.shape[0], _wtype(self.AT), _ptr(self.AT), _ptr(self.BT))
+        # checked and built once per set of tensors (calls are on the hot path)
+        key = tuple(id(t) for t in (self.AT, self.BT,))
+        if getattr(self, "_ck", None) != key:
+            _tensor("Predictor.AT", self.AT, _STORE, 2, dev=False)
+            r, d = self.AT.shape
+            _tensor("Predictor.BT", self.BT, _STORE, 2, (None, r), dev=False)
+            _same_dtype("Predictor", self.AT, self.BT)
+            _gpu(type(self).__name__, self.AT, self.BT)
+            self._cs = CPredictor(d, r, self.BT.shape[0], _wtype(self.AT), _ptr(self.AT), _ptr(self.BT))
+            self._ck = key
+        return self._cs
 
 
 @dataclass
@@ -162,8 +217,19 @@ class MLP:
     b2: Optional[torch.Tensor] = None
 
     def c(self) -> CMlp:
-        n, d = self.W1T.shape
-        return CMlp(d, n, _wtype(self.W1T), 0, _ptr(self.W1T), _ptr(self.b1), _ptr(self.W2T), _ptr(self.b2))
+        # checked and built once per set of tensors (calls are on the hot path)
+        key = tuple(id(t) for t in (self.W1T, self.W2T, self.b1, self.b2,))
+        if getattr(self, "_ck", None) != key:
+            _tensor("MLP.W1T", self.W1T, _STORE, 2, dev=False)
+            n, d = self.W1T.shape
+            _tensor("MLP.W2T", self.W2T, _STORE, 2, (n, d), dev=False)
+            _same_dtype("MLP", self.W1T, self.W2T)
+            _tensor("MLP.b1", self.b1, _F32, 1, (n,), optional=True, dev=False)
+            _tensor("MLP.b2", self.b2, _F32, 1, (d,), optional=True, dev=False)
+            _gpu(type(self).__name__, self.W1T, self.W2T, self.b1, self.b2)
+            self._cs = CMlp(d, n, _wtype(self.W1T), 0, _ptr(self.W1T), _ptr(self.b1), _ptr(self.W2T), _ptr(self.b2))
+            self._ck = key
+        return self._cs
 
 
 @dataclass
@@ -179,9 +245,24 @@ class Attn:
     bo: Optional[torch.Tensor] = None
 
     def c(self) -> CAttn:
-        hd, d = self.Wq.shape
-        return CAttn(d, self.H, hd // self.H, _wtype(self.Wq), _ptr(self.Wq), _ptr(self.Wk), _ptr(self.Wv),
-                     _ptr(self.bq), _ptr(self.bk), _ptr(self.bv), _ptr(self.WoT), _ptr(self.bo))
+        # checked and built once per set of tensors (calls are on the hot path)
+        key = tuple(id(t) for t in (self.Wq, self.Wk, self.Wv, self.WoT, self.bq, self.bk, self.bv, self.bo, self.H,))
+        if getattr(self, "_ck", None) != key:
+            _tensor("Attn.Wq", self.Wq, _STORE, 2, dev=False)
+            hd, d = self.Wq.shape
+            if self.H <= 0 or hd % self.H:
+                raise ValueError(f"Attn: {hd} projection rows do not split into H = {self.H} heads")
+            for nm in ("Wk", "Wv", "WoT"):
+                _tensor(f"Attn.{nm}", getattr(self, nm), _STORE, 2, (hd, d), dev=False)
+            _same_dtype("Attn", self.Wq, self.Wk, self.Wv, self.WoT)
+            for nm in ("bq", "bk", "bv"):
+                _tensor(f"Attn.{nm}", getattr(self, nm), _F32, 1, (hd,), optional=True, dev=False)
+            _tensor("Attn.bo", self.bo, _F32, 1, (d,), optional=True, dev=False)
+            _gpu(type(self).__name__, self.Wq, self.Wk, self.Wv, self.WoT, self.bq, self.bk, self.bv, self.bo)
+            self._cs = CAttn(d, self.H, hd // self.H, _wtype(self.Wq), _ptr(self.Wq), _ptr(self.Wk), _ptr(self.Wv),
+                         _ptr(self.bq), _ptr(self.bk), _ptr(self.bv), _ptr(self.WoT), _ptr(self.bo))
+            self._ck = key
+        return self._cs
 
 
 class KVCache:
@@ -192,9 +273,18 @@ class KVCache:
         self._pos = (c_int32 * K.shape[0])(*[int(p) for p in pos])
 
     def c(self) -> CKV:
-        B, H, cap, dh = self.K.shape
-        return CKV(B, H, dh, cap, _wtype(self.K), 0, _ptr(self.K), _ptr(self.V),
-                   ctypes.cast(self._pos, POINTER(c_int32)))
+        # checked and built once per set of tensors (calls are on the hot path)
+        key = tuple(id(t) for t in (self.K, self.V, self._pos,))
+        if getattr(self, "_ck", None) != key:
+            _tensor("KVCache.K", self.K, _STORE, 4, dev=False)
+            _tensor("KVCache.V", self.V, _STORE, 4, tuple(self.K.shape), dev=False)
+            _same_dtype("KVCache", self.K, self.V)
+            B, H, cap, dh = self.K.shape
+            _gpu(type(self).__name__, self.K, self.V)
+            self._cs = CKV(B, H, dh, cap, _wtype(self.K), 0, _ptr(self.K), _ptr(self.V),
+                       ctypes.cast(self._pos, POINTER(c_int32)))
+            self._ck = key
+        return self._cs
 
 
 @dataclass
@@ -206,7 +296,15 @@ class LN:
     eps: float = 1e-5
 
     def c(self) -> CLN:
-        return CLN(_ptr(self.g1), _ptr(self.be1), _ptr(self.g2), _ptr(self.be2), self.eps)
+        # checked and built once per set of tensors (calls are on the hot path)
+        key = tuple(id(t) for t in (self.g1, self.be1, self.g2, self.be2, self.eps,))
+        if getattr(self, "_ck", None) != key:
+            for nm in ("g1", "be1", "g2", "be2"):
+                _tensor(f"LN.{nm}", getattr(self, nm), _F32, 1, optional=True, dev=False)
+            _gpu(type(self).__name__, self.g1, self.be1, self.g2, self.be2)
+            self._cs = CLN(_ptr(self.g1), _ptr(self.be1), _ptr(self.g2), _ptr(self.be2), self.eps)
+            self._ck = key
+        return self._cs
 
 
 # ------------------------------------------------------------- entry points
@@ -214,7 +312,12 @@ def _predict(fn, pred: Predictor, x, k=0, mode=DV_SELECT_TOPK, thresh=0.0, idx=N
              scores=None, cap_idx=None, ws=None, flags=0, stream=None):
     lib = load()
     cp = pred.c()
+    _tensor("x", x, _F32, 2, (None, cp.d), dev=False)
     B = x.shape[0]
+    _tensor("idx", idx, _I32, 2, (B, None), optional=True, dev=False)
+    _tensor("count", count, _I32, 1, (B,), optional=True, dev=False)
+    _tensor("scores", scores, _F32, 2, (B, cp.n_out), optional=True, dev=False)
+    _gpu("arguments", x, idx, count, scores)
     if cap_idx is None:
         cap_idx = k if mode == DV_SELECT_TOPK else cp.n_out
     if idx is None:
@@ -224,7 +327,7 @@ def _predict(fn, pred: Predictor, x, k=0, mode=DV_SELECT_TOPK, thresh=0.0, idx=N
     if ws is None:
         ws = _workspace(lib.dv_predict_workspace_bytes(ctypes.byref(cp), B), x.device)
     st = getattr(lib, fn)(ctypes.byref(cp), _ptr(x), B, mode, k, thresh, _ptr(idx), cap_idx, _ptr(count),
-                          _ptr(scores), _ptr(ws), ws.numel(), flags, _stream(stream))
+                          _ptr(scores), *_wsarg(ws), flags, _stream(stream))
     _check(fn, st)
     return idx, count
 
@@ -244,14 +347,20 @@ def dv_sparse_mlp(mlp: MLP, x, idx, idx_per_seq=0, batch_mode=DV_MLP_UNION, out=
     """out[b] = MLP_S(x[b]) (Eq. (1)), without residual."""
     lib = load()
     cm = mlp.c()
+    _tensor("x", x, _F32, 2, (None, cm.d), dev=False)
     B = x.shape[0]
+    _tensor("idx", idx, _I32, dev=False)
     n_idx = idx.shape[-1]
+    if idx_per_seq and idx.numel() != B * n_idx:
+        raise ValueError(f"idx holds {idx.numel()} entries; per-sequence sets need B x n_idx = {B * n_idx}")
+    _tensor("out", out, _F32, 2, (B, cm.d), optional=True, dev=False)
+    _gpu("arguments", x, idx, out)
     if out is None:
         out = torch.empty((B, cm.d), dtype=torch.float32, device=x.device)
     if ws is None:
         ws = _workspace(lib.dv_sparse_mlp_workspace_bytes(ctypes.byref(cm), B, n_idx, idx_per_seq), x.device)
     st = lib.dv_sparse_mlp(ctypes.byref(cm), _ptr(x), B, _ptr(idx), n_idx, idx_per_seq, batch_mode,
-                           _ptr(out), _ptr(ws), ws.numel(), flags, _stream(stream))
+                           _ptr(out), *_wsarg(ws), flags, _stream(stream))
     _check("dv_sparse_mlp", st)
     return out
 
@@ -260,15 +369,21 @@ def dv_sparse_attn(attn: Attn, x, kv: KVCache, heads, scale, out=None, ws=None, 
     """out[b] = bo + sum_{i in S_A^b} H_i(x[b]) W^O_i (Eq. (2)); updates the cache rows at pos."""
     lib = load()
     ca, ck = attn.c(), kv.c()
+    _tensor("x", x, _F32, 2, (None, ca.d), dev=False)
     B = x.shape[0]
+    _tensor("heads", heads, _I32, dev=False)
     n_heads = heads.shape[-1]
+    if heads.numel() != B * n_heads:
+        raise ValueError(f"heads holds {heads.numel()} entries; expected B x n_heads = {B * n_heads}")
+    _tensor("out", out, _F32, 2, (B, ca.d), optional=True, dev=False)
+    _gpu("arguments", x, heads, out)
     if out is None:
         out = torch.empty((B, ca.d), dtype=torch.float32, device=x.device)
     if ws is None:
         ws = _workspace(lib.dv_sparse_attn_workspace_bytes(ctypes.byref(ca), ctypes.byref(ck), B, n_heads),
                         x.device)
     st = lib.dv_sparse_attn(ctypes.byref(ca), _ptr(x), B, ctypes.byref(ck), _ptr(heads), n_heads, scale,
-                            _ptr(out), _ptr(ws), ws.numel(), flags, _stream(stream))
+                            _ptr(out), *_wsarg(ws), flags, _stream(stream))
     _check("dv_sparse_attn", st)
     return out
 
@@ -280,7 +395,12 @@ def dv_sparse_block(attn: Attn, mlp: MLP, pred_h: Predictor, pred_m: Predictor, 
     lib = load()
     ca, cm, cph, cpm, ck = attn.c(), mlp.c(), pred_h.c(), pred_m.c(), kv.c()
     cl = ln.c() if ln is not None else None
+    _tensor("x", x, _F32, 2, (None, ca.d), dev=False)
     B = x.shape[0]
+    _tensor("out", out, _F32, 2, (B, ca.d), optional=True, dev=False)
+    _tensor("heads_out", heads_out, _I32, 2, (B, k_heads), optional=True, dev=False)
+    _tensor("idx_out", idx_out, _I32, 2, (B, k_mlp), optional=True, dev=False)
+    _gpu("arguments", x, out, heads_out, idx_out)
     if out is None:
         out = torch.empty_like(x)
     if heads_out is None:
@@ -292,7 +412,7 @@ def dv_sparse_block(attn: Attn, mlp: MLP, pred_h: Predictor, pred_m: Predictor, 
     st = lib.dv_sparse_block(ctypes.byref(ca), ctypes.byref(cm), ctypes.byref(cph), ctypes.byref(cpm),
                              ctypes.byref(cl) if cl is not None else None, ctypes.byref(ck), _ptr(x),
                              _ptr(out), B, k_heads, k_mlp, mode, batch_mode, scale, _ptr(heads_out),
-                             _ptr(idx_out), _ptr(ws), ws.numel(), flags, _stream(stream))
+                             _ptr(idx_out), *_wsarg(ws), flags, _stream(stream))
     _check("dv_sparse_block", st)
     return out, heads_out, idx_out
 
@@ -317,6 +437,19 @@ def attn_workspace_bytes(attn, kv, B, n_heads) -> int:
 def predict_workspace_bytes(pred, B) -> int:
     cp = pred.c()
     return load().dv_predict_workspace_bytes(ctypes.byref(cp), B)
+
+
+def dv_stream_read(buf: torch.Tensor, sink: torch.Tensor, nbytes: Optional[int] = None, stream=None):
+    """One plain contiguous read of `nbytes` (default: all) of `buf`: the measured
+    bandwidth ceiling the gathered kernels are compared with."""
+    if not isinstance(buf, torch.Tensor) or not buf.is_contiguous():
+        raise ValueError("buf must be a contiguous tensor")
+    _tensor("sink", sink, _F32)
+    _gpu("buf", buf)
+    n = buf.numel() * buf.element_size() if nbytes is None else int(nbytes)
+    if n > buf.numel() * buf.element_size():
+        raise ValueError("nbytes exceeds the buffer")
+    _check("dv_stream_read", load().dv_stream_read(buf.data_ptr(), n, sink.data_ptr(), _stream(stream)))
 
 
 # --------------------------------------------------------- per-launch timing

@@ -5,6 +5,9 @@
 // carves its scratch buffers out of the caller's workspace and enqueues its kernels
 // on the caller's stream.
 #include <atomic>
+#include <mutex>
+#include <set>
+#include <utility>
 #include <string.h>
 #include <math.h>
 
@@ -12,19 +15,53 @@
 
 namespace dv {
 
-int device_cu_count() {
-  static std::atomic<int> cache[64];
+// Device properties, read once per device (up to 64 devices) and kept in atomics:
+// concurrent first calls may both query, and store the same value.
+namespace {
+std::atomic<int> g_cus[64], g_lds[64];
+
+int current_device() {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0) dev = 0;
+  return dev;
+}
+
+int cached_attr(std::atomic<int>* cache, hipDeviceAttribute_t attr, int fallback) {
+  const int dev = current_device();
   if (dev < 64) {
-    int v = cache[dev].load(std::memory_order_relaxed);
+    const int v = cache[dev].load(std::memory_order_relaxed);
     if (v > 0) return v;
   }
-  int cus = 0;
-  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
-    cus = 256;
-  if (dev < 64) cache[dev].store(cus, std::memory_order_relaxed);
-  return cus;
+  int v = 0;
+  if (hipDeviceGetAttribute(&v, attr, dev) != hipSuccess || v <= 0) v = fallback;
+  if (dev < 64) cache[dev].store(v, std::memory_order_relaxed);
+  return v;
+}
+}  // namespace
+
+int device_cu_count() { return cached_attr(g_cus, hipDeviceAttributeMultiprocessorCount, 256); }
+
+int device_lds_per_block() { return cached_attr(g_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, 65536); }
+
+hipError_t ensure_dyn_lds(const void* kern, size_t bytes) {
+  if (bytes <= 65536) return hipSuccess;
+  static std::mutex mu;
+  static std::set<std::pair<const void*, int>> done;
+  const int dev = current_device();
+  {
+    std::lock_guard<std::mutex> g(mu);
+    if (done.count({kern, dev})) return hipSuccess;
+  }
+  hipFuncAttributes fa{};
+  hipError_t e = hipFuncGetAttributes(&fa, kern);
+  if (e != hipSuccess) return e;
+  const int limit = device_lds_per_block() - (int)fa.sharedSizeBytes;
+  if ((long)bytes > (long)limit) return hipErrorInvalidValue;
+  e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, limit);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> g(mu);
+  done.insert({kern, dev});
+  return hipSuccess;
 }
 
 namespace {

@@ -80,8 +80,7 @@ static hipError_t launch_qkv_t(const QkvArgs& a, hipStream_t st) {
   size_t lds = (size_t)(a.d + NW) * sizeof(float) + (size_t)a.n_heads * sizeof(int32_t) +
                (size_t)rowdot_flat_part(nrows, blocks, NW) * sizeof(float) + 16;
   if (a.sel_n > 0) lds = max(lds, (size_t)kSelBins * 4 + kSelSm(NT) * sizeof(int));
-  static int cur = 0;   // (wide inputs and many rows per workgroup pass 64 KB)
-  const hipError_t e = ensure_dyn_lds(reinterpret_cast<const void*>(k_qkv<T, KT, NW, U, KX>), lds, &cur);
+  const hipError_t e = ensure_dyn_lds(reinterpret_cast<const void*>(k_qkv<T, KT, NW, U, KX>), lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((k_qkv<T, KT, NW, U, KX>), dim3(blocks + (a.sel_n > 0 ? 1 : 0)), dim3(NW * 64), lds, st, a);
   return hipGetLastError();

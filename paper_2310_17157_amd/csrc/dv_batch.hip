@@ -39,18 +39,6 @@ __device__ __forceinline__ v4s_t ds_read_tr16(const _Float16* p) {
       (v4s_t __attribute__((address_space(3)))*)(const_cast<_Float16*>(p)));
 }
 
-static int lds_budget() {
-  static int cached = 0;
-  if (cached == 0) {
-    int dev = 0, v = 0;
-    (void)hipGetDevice(&dev);
-    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || v <= 0) v = 65536;
-    cached = v;
-  }
-  return cached;
-}
-
-
 // ------------------------------------------------------------------ union
 // Union of B ascending sets sets[b][0..k) in [0, n) in one launch, one workgroup per
 // chunk of kUnionChunk indices. Every workgroup reads all B * k entries (they stay
@@ -66,9 +54,11 @@ static_assert(kUnionChunk == 2 * kUnionNT, "two indices of the chunk per thread"
 
 // Calls fn(e, v) for every entry e of sets[0..total) with value v. The entries are
 // read as aligned int4 with all of a thread's loads in flight (one round trip for up
-// to PER * 4 * kUnionNT entries; rounds of loads past the end are not issued). sets need only be 4-byte aligned: the quads start
-// at its 16-byte block, and a 16-byte aligned block never crosses a page, so the
-// words before the first entry and after the last are readable; they are skipped.
+// to PER * 4 * kUnionNT entries; rounds of loads past the end are not issued). sets
+// need only be 4-byte aligned: the quads start at its 16-byte block, so the first and
+// the last quad may reach up to 12 bytes outside [sets, sets + total). Those bytes share
+// an aligned 16-byte block with an entry, and such a block never crosses a page (GPU
+// pages are at least 4 KB), so they are readable; their values are skipped.
 template <class Fn>
 __device__ __forceinline__ void union_scan(const int32_t* __restrict__ sets, int total, Fn fn) {
   constexpr int PER = 16;
@@ -158,10 +148,9 @@ hipError_t launch_union(const int32_t* sets, int B, int k, int n, int32_t* U, in
                         hipStream_t st) {
   const int nc = (n + kUnionChunk - 1) / kUnionChunk;
   const size_t lds = union_lds_bytes(n);
-  static int cur[2] = {0, 0};
   const void* kern = mask != nullptr ? reinterpret_cast<const void*>(k_union<true>)
                                      : reinterpret_cast<const void*>(k_union<false>);
-  const hipError_t e = ensure_dyn_lds(kern, lds, &cur[mask != nullptr]);
+  const hipError_t e = ensure_dyn_lds(kern, lds);
   if (e != hipSuccess) return e;
   if (mask != nullptr)
     hipLaunchKernelGGL(k_union<true>, dim3(nc), dim3(kUnionNT), lds, st, sets, B, k, n, U, count, mask);
@@ -253,10 +242,9 @@ hipError_t launch_cast_union(const float* x, int B, int NB, int d, int Kpad, con
   static_assert(kUnionNT == 1024, "the cast and the union share the workgroup size");
   const int nc = (n + kUnionChunk - 1) / kUnionChunk;
   const size_t lds = union_lds_bytes(n);
-  static int cur[2] = {0, 0};
   const void* kern = mask != nullptr ? reinterpret_cast<const void*>(k_cast_union<true>)
                                      : reinterpret_cast<const void*>(k_cast_union<false>);
-  const hipError_t e = ensure_dyn_lds(kern, lds, &cur[mask != nullptr]);
+  const hipError_t e = ensure_dyn_lds(kern, lds);
   if (e != hipSuccess) return e;
   if (mask != nullptr)
     hipLaunchKernelGGL(k_cast_union<true>, dim3(NB + nc), dim3(1024), lds, st, x, B, d, Kpad, g, be, eps, X16, NB,
@@ -432,7 +420,7 @@ __global__ void __launch_bounds__(NW * 64) k_mfma_rows(MrowsArgs a) {
 static constexpr int kMrU = 8, kMrNW = 8;
 static constexpr int kMrTileBytes = kMrNW * 16 * 64 * 2;
 void mrows_split(int Kpad, int NB, int* S, int* Ks) {
-  const int budget = min(lds_budget() - kMrTileBytes, 98304 + NB * 16);
+  const int budget = min(device_lds_per_block() - kMrTileBytes, 98304 + NB * 16);
   const int unit = 32 * kMrU;
   int kmax = ((budget / (NB * 2) - 8) / unit) * unit;
   if (kmax < unit) kmax = unit;
@@ -446,8 +434,7 @@ template <int NB, int MODE>
 static hipError_t launch_mrows_t(MrowsArgs a, hipStream_t st) {
   const size_t lds = (size_t)NB * (a.Ks + 8) * 2 + kMrTileBytes;
   const auto kern = k_mfma_rows<NB, kMrNW, kMrU, MODE>;
-  static int cur = 0;
-  const hipError_t e = ensure_dyn_lds(reinterpret_cast<const void*>(kern), lds, &cur);
+  const hipError_t e = ensure_dyn_lds(reinterpret_cast<const void*>(kern), lds);
   if (e != hipSuccess) return e;
   const int G = max(1, device_cu_count() / a.S);
   hipLaunchKernelGGL(kern, dim3(G * a.S), dim3(kMrNW * 64), lds, st, a);

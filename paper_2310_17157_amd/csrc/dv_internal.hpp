@@ -355,15 +355,13 @@ struct AxpyArgs {
 constexpr int kAxpyMaxRowSplit = 32;
 constexpr int kAxpyMaxSpans = 64;     // column spans of 64 x 16 bytes at d <= 16000
 
-// Raises a kernel's dynamic LDS limit to the bytes a launch needs (above the 64 KB
-// default; the limit is per kernel, kept in *cur). The limit is the request itself,
-// not the device maximum: the kernel's static LDS has to fit beside it.
-inline hipError_t ensure_dyn_lds(const void* kern, size_t bytes, int* cur) {
-  if (bytes <= 65536 || (int)bytes <= *cur) return hipSuccess;
-  const hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-  if (e == hipSuccess) *cur = (int)bytes;
-  return e;
-}
+// Raises a kernel's dynamic LDS limit on the current device when a launch needs more
+// than the 64 KB default. The limit set is always the same for a kernel and device (the
+// device's LDS per workgroup less the kernel's static LDS), so concurrent callers
+// agree; which (kernel, device) pairs are done is kept in a mutex-guarded set. A
+// request above that limit returns hipErrorInvalidValue.
+hipError_t ensure_dyn_lds(const void* kern, size_t bytes);
+int device_lds_per_block();   // cached per device
 
 // Clears n counters for a later row-axpy of the same call (agent-scope stores: the
 // counters are read by atomics from every XCD).

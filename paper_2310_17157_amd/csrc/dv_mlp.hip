@@ -51,10 +51,9 @@ static hipError_t launch_fc1_t(const Fc1Args& a, hipStream_t st) {
   constexpr int NW = 16, U = 2;
   const int blocks = max(1, min(a.k, device_cu_count()));
   const size_t lds = (size_t)(a.d + NW + rowdot_flat_part(a.k, blocks, NW)) * sizeof(float);
-  static int cur[2] = {0, 0};   // (wide inputs and many rows per workgroup pass 64 KB)
   const void* kern = a.g != nullptr ? reinterpret_cast<const void*>(k_fc1<T, NW, U, KX, true>)
                                     : reinterpret_cast<const void*>(k_fc1<T, NW, U, KX, false>);
-  const hipError_t e = ensure_dyn_lds(kern, lds, &cur[a.g != nullptr]);
+  const hipError_t e = ensure_dyn_lds(kern, lds);
   if (e != hipSuccess) return e;
   if (a.g != nullptr)
     hipLaunchKernelGGL((k_fc1<T, NW, U, KX, true>), dim3(blocks), dim3(NW * 64), lds, st, a);

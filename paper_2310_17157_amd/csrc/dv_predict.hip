@@ -40,10 +40,9 @@ static hipError_t launch_pred_hidden_t(const PredHidArgs& a, hipStream_t st) {
   const int nrows = a.r0 + a.r1;
   const dim3 grid(max(1, min(nrows, device_cu_count())), a.B);
   const size_t lds = (size_t)(a.d + NW + rowdot_flat_part(nrows, grid.x, NW)) * sizeof(float);
-  static int cur[2] = {0, 0};   // (wide inputs and many rows per workgroup pass 64 KB)
   const void* kern = a.g != nullptr ? reinterpret_cast<const void*>(k_pred_hidden<T, NW, U, KX, true>)
                                     : reinterpret_cast<const void*>(k_pred_hidden<T, NW, U, KX, false>);
-  const hipError_t e = ensure_dyn_lds(kern, lds, &cur[a.g != nullptr]);
+  const hipError_t e = ensure_dyn_lds(kern, lds);
   if (e != hipSuccess) return e;
   if (a.g != nullptr)
     hipLaunchKernelGGL((k_pred_hidden<T, NW, U, KX, true>), grid, dim3(NW * 64), lds, st, a);
@@ -237,8 +236,7 @@ __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2 
 // (ranks of two predictors staged together pass 64 KB: up to 2 x 16000 floats)
 template <typename T, int NW, int G, int RU, int NR, bool EARLY>
 static hipError_t launch_scores_k(const PredScoreArgs& a, dim3 grid, size_t lds, hipStream_t st) {
-  static int cur = 0;
-  const hipError_t e = ensure_dyn_lds(reinterpret_cast<const void*>(k_pred_scores<T, NW, G, RU, NR, EARLY>), lds, &cur);
+  const hipError_t e = ensure_dyn_lds(reinterpret_cast<const void*>(k_pred_scores<T, NW, G, RU, NR, EARLY>), lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((k_pred_scores<T, NW, G, RU, NR, EARLY>), grid, dim3(NW * 64), lds, st, a);
   return hipGetLastError();

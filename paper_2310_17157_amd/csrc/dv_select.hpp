@@ -22,10 +22,6 @@ namespace dv {
 
 constexpr int kSelBins = 8192;   // LDS histogram bins (13-bit digits)
 
-// Phase marks for an external timing harness; empty in the library build.
-#ifndef DV_SELECT_MARK
-#define DV_SELECT_MARK(i)
-#endif
 // Scratch ints needed by the selection routines for an NT-thread workgroup.
 constexpr int kSelSm(int NT) { return 2 * (NT / 64) + 8; }
 
@@ -263,7 +259,6 @@ __device__ void wg_select_reg(const float* __restrict__ s, int n, int mode, int 
       }
     }
   }
-  DV_SELECT_MARK(10);
   uint32_t prefix = 0u;
   int pbits = 0;
   int eq_take = INT_MAX;
@@ -301,7 +296,6 @@ __device__ void wg_select_reg(const float* __restrict__ s, int n, int mode, int 
         }
       }
       __syncthreads();
-      DV_SELECT_MARK(11 + 2 * p);
       int dig, above;
       find_digit<NT>(hist, nb, krem, sm, &dig, &above);
       const int cnt = (int)hist[dig];
@@ -309,7 +303,6 @@ __device__ void wg_select_reg(const float* __restrict__ s, int n, int mode, int 
       prefix = (prefix << D) | (uint32_t)dig;
       pbits += D;
       __syncthreads();
-      DV_SELECT_MARK(12 + 2 * p);
       if (cnt == krem) {
         eq_take = INT_MAX;
         break;
@@ -317,7 +310,6 @@ __device__ void wg_select_reg(const float* __restrict__ s, int n, int mode, int 
       eq_take = krem;
     }
   }
-  DV_SELECT_MARK(17);
   volatile int* bound = sm + 2 * NW + 4;   // prefix, shift
   if (tid == 0) {
     bound[0] = (int)prefix;
@@ -358,7 +350,6 @@ __device__ void wg_select_reg(const float* __restrict__ s, int n, int mode, int 
     teq += b;
   }
   const int total = tgt + min(teq, eq_take);
-  DV_SELECT_MARK(18);
   prefix = (uint32_t)__builtin_amdgcn_readfirstlane(bound[0]);
   sh = __builtin_amdgcn_readfirstlane(bound[1]);
   // Write walk: group by group; inside a group, lanes in order, then elements. The
@@ -444,7 +435,6 @@ __device__ void wg_select_reg(const float* __restrict__ s, int n, int mode, int 
       }
     });
   }
-  DV_SELECT_MARK(19);
   if (tid == 0 && count_out) *count_out = total;
   __syncthreads();
 }

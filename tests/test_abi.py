@@ -149,3 +149,42 @@ def test_batched_path_limits(lib):
                               1 << 30, 0, None) == B.DV_ERR_UNSUPPORTED
     kv2 = _kv(Bn=2, pos=(3, 9))
     assert lib.dv_sparse_attn_workspace_bytes(ctypes.byref(a), ctypes.byref(kv2), 2, 2) > 0
+
+
+def test_binding_rejects_bad_tensors_before_the_library():
+    """The binding checks dtype, shape, contiguity and device of every tensor before a
+    pointer reaches the C ABI (CPU tensors here: every case fails in Python)."""
+    import torch
+    h16 = lambda *s: torch.zeros(*s, dtype=torch.float16)
+    f32 = lambda *s: torch.zeros(*s, dtype=torch.float32)
+    # a weight struct whose matrices differ in dtype
+    with pytest.raises(TypeError):
+        B.MLP(h16(8, 16), f32(8, 16)).c()
+    with pytest.raises(TypeError):
+        B.Attn(h16(8, 16), h16(8, 16), f32(8, 16), h16(8, 16), 2).c()
+    with pytest.raises(TypeError):
+        B.Predictor(h16(4, 16), f32(8, 4)).c()
+    with pytest.raises(TypeError):
+        B.KVCache(h16(1, 2, 4, 8), f32(1, 2, 4, 8), [0]).c()
+    # fp16 biases, wrong shapes, a transposed (non-contiguous) view
+    with pytest.raises(TypeError):
+        B.MLP(h16(8, 16), h16(8, 16), b1=h16(8)).c()
+    with pytest.raises(ValueError):
+        B.MLP(h16(8, 16), h16(8, 16), b2=f32(15)).c()
+    with pytest.raises(ValueError):
+        B.MLP(h16(16, 8).t(), h16(8, 16)).c()
+    with pytest.raises(ValueError):
+        B.Attn(h16(9, 16), h16(9, 16), h16(9, 16), h16(9, 16), 2).c()      # 9 rows, 2 heads
+    # CPU tensors of the right dtype are rejected as not on the GPU
+    with pytest.raises(ValueError, match="GPU"):
+        B.MLP(h16(8, 16), h16(8, 16)).c()
+    # entry-point arguments: an int64 index set, an fp16 input
+    class _M(B.MLP):
+        def c(self):
+            return B.CMlp(16, 8, B.DV_F16, 0, FAKE, None, FAKE, None)
+    m = _M(h16(8, 16), h16(8, 16))
+    with pytest.raises(TypeError, match="int32"):
+        B.dv_sparse_mlp(m, f32(1, 16).cuda() if torch.cuda.is_available() else f32(1, 16),
+                        torch.tensor([1, 2], dtype=torch.int64))
+    with pytest.raises(TypeError, match="float32"):
+        B.dv_sparse_mlp(m, h16(1, 16), torch.tensor([1, 2], dtype=torch.int32))

@@ -69,3 +69,35 @@ def test_opt175b_batch1_totals():
     assert b.pred == (d * 1000 + 1000 * 96 + d * 1000 + 1000 * 49152) * 2
     assert round(b.block / 1e6, 2) == 556.97
     assert round(b.total / 1e6, 1) == 704.6
+
+
+@pytest.mark.parametrize("name", ["opt125m_b1", "opt6.7b_b1", "opt66b_b1", "opt175b_b1"])
+def test_bench_per_kernel_bytes_sum_to_the_layer_accounting(name):
+    """bench.py's per-launch bytes (what each kernel of one layer reads) add up to the
+    pinned per-layer accounting: the five block kernels to the sparse block, the two
+    predictor launches to both predictors."""
+    import bench
+    from paper_2310_17157_amd import accounting
+    from synth import get_config
+    cfg = get_config(name)
+    kb = bench.kernel_bytes(cfg, cfg.L - 1)
+    b = accounting.layer_bytes(cfg)
+    assert sum(kb[k] for k in bench.BLOCK_KERNELS) == b.block
+    assert kb["pred_hidden"] + kb["pred_scores"] == b.pred
+    assert kb["fc1"] + kb["fc2"] == b.mlp and kb["qkv"] + kb["oproj"] == b.attn_w and kb["attn"] == b.kv
+
+
+def test_bench_batch_bytes_match_the_batch_accounting():
+    import numpy as np
+    import bench
+    from paper_2310_17157_amd import accounting
+    from synth import get_config, uniform_head_sets, zipf_mlp_sets
+    from synth.gen import positions
+    cfg = get_config("opt175b_b32")
+    heads, sets, pos = uniform_head_sets(cfg, 4), zipf_mlp_sets(cfg, 4), positions(cfg, 4)
+    kb, nu, nu_h = bench.batch_kernel_bytes(cfg, heads, sets, pos)
+    assert nu == len(np.unique(sets)) and nu_h == len(np.unique(heads))
+    ref = accounting.batch_bytes(cfg, nu, nu_h, int(sum(len(h) * (int(p) + 1) for h, p in zip(heads, pos))))
+    assert kb["fc1"] + kb["fc2"] == ref["mlp"]
+    assert kb["qkv"] + kb["oproj"] == ref["attn_w"]
+    assert kb["attn"] == ref["kv"]

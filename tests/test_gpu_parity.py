@@ -182,7 +182,7 @@ def test_select_streaming_path_agrees_with_oracle():
 
 
 # ------------------------------------------------------------------ sparse MLP
-@pytest.mark.parametrize("name", SMALL + ["opt6.7b_b1"])
+@pytest.mark.parametrize("name", SMALL + ["opt6.7b_b1", "opt66b_b1", "opt175b_b1"])
 def test_sparse_mlp(name):
     cfg, t = layer(name, 21, biases=True)
     _, mlp, *_ = layer_objects(t, cfg.H)
@@ -241,7 +241,7 @@ def _attn_case(name, seed, heads=None, pos=None, kv_scale=1.0):
     return cfg, t, heads, p, out, ref, K0, V0, Kn, Vn
 
 
-@pytest.mark.parametrize("name", SMALL + ["opt6.7b_b1"])
+@pytest.mark.parametrize("name", SMALL + ["opt6.7b_b1", "opt66b_b1", "opt175b_b1"])
 def test_sparse_attn(name):
     cfg, t, heads, p, out, ref, K0, V0, Kn, Vn = _attn_case(name, 31)
     assert rel_l2(host(out)[0], ref) < REL_TOL
@@ -333,7 +333,22 @@ def _block(name, seed, mode, biases=True, ln=True, k_heads=None, k_mlp=None):
     g = host(out)[0]
     assert rel_l2(g - y, r["out"] - y) < REL_TOL
     assert rel_l2(g, r["out"]) < REL_TOL
+    check_cache_contract(host(t["K"])[0], host(t["V"])[0], K0, V0, r["K_new"], r["V_new"], gh, int(t["pos"][0]))
     return cfg, t, out, hs, ms, r
+
+
+def check_cache_contract(Kg, Vg, K0, V0, Kn, Vn, heads, p):
+    """Section 4.2: only row p of the selected heads changes (bit for bit elsewhere), and
+    it holds the fresh key / value."""
+    allowed = np.zeros(Kg.shape[:2], dtype=bool)
+    for h in heads:
+        allowed[h, p] = True
+        assert rel_l2(Kg[h, p].astype(np.float64), Kn[h, p]) < REL_TOL, h
+        assert rel_l2(Vg[h, p].astype(np.float64), Vn[h, p]) < REL_TOL, h
+    for C, C0 in ((Kg, K0), (Vg, V0)):
+        bits = np.uint16 if C.dtype == np.float16 else np.uint32
+        changed = (np.ascontiguousarray(C).view(bits) != np.ascontiguousarray(C0).view(bits)).any(axis=-1)
+        assert not (changed & ~allowed).any(), np.argwhere(changed & ~allowed)[:5]
 
 
 @pytest.mark.parametrize("name", SMALL)
@@ -363,6 +378,21 @@ def test_sparse_block_is_deterministic():
         _sync()
         outs.append((host(out).tobytes(), host(hs).tobytes(), host(ms).tobytes()))
     assert outs[0] == outs[1]
+
+
+def test_sparse_block_full_size_is_deterministic():
+    """Two identical OPT-175B-shaped block calls give bitwise identical outputs and sets:
+    the row-axpy split sums (10 row splits over 24 column spans, the last split of each
+    span to arrive adds them) run in split order whatever the arrival order."""
+    cfg, t = layer("opt175b_b1", 49, biases=True, ln_random=True)
+    attn, mlp, ph, pm, kv, lnp = layer_objects(t, cfg.H)
+    outs = []
+    for _ in range(3):
+        out, hs, ms = Bd.dv_sparse_block(attn, mlp, ph, pm, lnp, kv, t["x"], cfg.k_heads, cfg.k_mlp,
+                                         1.0 / np.sqrt(cfg.dh))
+        _sync()
+        outs.append((host(out).tobytes(), host(hs).tobytes(), host(ms).tobytes()))
+    assert outs[0] == outs[1] == outs[2]
 
 
 def test_sparse_block_at_the_width_limit():
