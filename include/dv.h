@@ -242,6 +242,28 @@ dv_status dv_sparse_block(const dv_attn *a, const dv_mlp *m, const dv_predictor 
                           int32_t *heads_out, int32_t *idx_out, void *ws, size_t ws_bytes,
                           uint32_t flags, void *stream);
 
+/* ------------------------------------------------- decoder layer, no allocation
+ * dv_sparse_block_noalloc: for callers that cannot allocate device memory (work being
+ * captured into a graph, serving loops or harnesses that forbid the allocator). The
+ * same layer, arguments and results as dv_sparse_block, without a workspace: its
+ * scratch space is a fixed array of DV_STATIC_SCRATCH_BYTES inside the library, one
+ * per device, held until the process ends. The call allocates nothing (no hipMalloc,
+ * no allocating library routine); its first call on a device looks up that device's
+ * copy of the array.
+ *   Limit.  A call whose dv_sparse_block_workspace_bytes exceeds DV_STATIC_SCRATCH_BYTES
+ *           returns DV_ERR_WORKSPACE and enqueues nothing (batch 1 at the OPT-175B
+ *           shape needs about 2.2 MB).
+ *   Races.  Every call on one device uses the same array: calls that overlap in time
+ *           on one device (other streams, other threads) must be ordered by the
+ *           caller. Nothing in the array needs to start cleared.
+ */
+#define DV_STATIC_SCRATCH_BYTES (16u << 20)
+dv_status dv_sparse_block_noalloc(const dv_attn *a, const dv_mlp *m, const dv_predictor *pa,
+                                  const dv_predictor *pm, const dv_ln *ln, const dv_kv *kv,
+                                  const float *x_in, float *x_out, int32_t B, int32_t k_heads,
+                                  int32_t k_mlp, int32_t mode, int32_t batch_mode, float scale,
+                                  int32_t *heads_out, int32_t *idx_out, uint32_t flags, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -75,6 +75,10 @@ _SIGS = {
     "dv_launch_label": (c_char_p, [c_int32]),
     "dv_abi_version": (c_int32, []),
     "dv_stream_read": (c_int32, [c_void_p, c_size_t, c_void_p, c_void_p]),
+    "dv_sparse_block_noalloc": (c_int32, [POINTER(CAttn), POINTER(CMlp), POINTER(CPredictor), POINTER(CPredictor),
+                                          POINTER(CLN), POINTER(CKV), c_void_p, c_void_p, c_int32, c_int32,
+                                          c_int32, c_int32, c_int32, c_float, c_void_p, c_void_p, c_uint32,
+                                          c_void_p]),
     "dv_predict_workspace_bytes": (c_size_t, [POINTER(CPredictor), c_int32]),
     "dv_predict_mlp": (c_int32, _PRED_ARGS),
     "dv_predict_heads": (c_int32, _PRED_ARGS),
@@ -414,6 +418,31 @@ def dv_sparse_block(attn: Attn, mlp: MLP, pred_h: Predictor, pred_m: Predictor, 
                              _ptr(out), B, k_heads, k_mlp, mode, batch_mode, scale, _ptr(heads_out),
                              _ptr(idx_out), *_wsarg(ws), flags, _stream(stream))
     _check("dv_sparse_block", st)
+    return out, heads_out, idx_out
+
+
+STATIC_SCRATCH_BYTES = 16 << 20   # DV_STATIC_SCRATCH_BYTES
+
+
+def dv_sparse_block_noalloc(attn: Attn, mlp: MLP, pred_h: Predictor, pred_m: Predictor, ln: Optional[LN],
+                            kv: KVCache, x, k_heads, k_mlp, scale, out, heads_out, idx_out,
+                            mode=DV_LOOKAHEAD, batch_mode=DV_MLP_UNION, flags=0, stream=None):
+    """dv_sparse_block without a workspace (the library's own per-device scratch); the
+    outputs must be given, since this call allocates nothing."""
+    lib = load()
+    ca, cm, cph, cpm, ck = attn.c(), mlp.c(), pred_h.c(), pred_m.c(), kv.c()
+    cl = ln.c() if ln is not None else None
+    _tensor("x", x, _F32, 2, (None, ca.d), dev=False)
+    B = x.shape[0]
+    _tensor("out", out, _F32, 2, (B, ca.d), dev=False)
+    _tensor("heads_out", heads_out, _I32, 2, (B, k_heads), optional=True, dev=False)
+    _tensor("idx_out", idx_out, _I32, 2, (B, k_mlp), optional=True, dev=False)
+    _gpu("arguments", x, out, heads_out, idx_out)
+    st = lib.dv_sparse_block_noalloc(ctypes.byref(ca), ctypes.byref(cm), ctypes.byref(cph), ctypes.byref(cpm),
+                                     ctypes.byref(cl) if cl is not None else None, ctypes.byref(ck), _ptr(x),
+                                     _ptr(out), B, k_heads, k_mlp, mode, batch_mode, scale, _ptr(heads_out),
+                                     _ptr(idx_out), flags, _stream(stream))
+    _check("dv_sparse_block_noalloc", st)
     return out, heads_out, idx_out
 
 

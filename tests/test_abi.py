@@ -188,3 +188,22 @@ def test_binding_rejects_bad_tensors_before_the_library():
                         torch.tensor([1, 2], dtype=torch.int64))
     with pytest.raises(TypeError, match="float32"):
         B.dv_sparse_mlp(m, h16(1, 16), torch.tensor([1, 2], dtype=torch.int32))
+
+
+def test_noalloc_block_rejects_what_its_scratch_cannot_hold(lib):
+    """dv_sparse_block_noalloc has a fixed scratch of DV_STATIC_SCRATCH_BYTES per device:
+    a layer whose workspace would exceed it is rejected before any device call (here a
+    neuron predictor scoring 2^23 neurons needs 32 MB of scores alone)."""
+    a, kv = _attn(), _kv()
+    n = 1 << 23
+    m = _mlp(n=n)
+    ph = B.CPredictor(64, 16, 4, B.DV_F16, FAKE, FAKE)
+    pm = B.CPredictor(64, 16, n, B.DV_F16, FAKE, FAKE)
+    need = lib.dv_sparse_block_workspace_bytes(ctypes.byref(a), ctypes.byref(m), ctypes.byref(ph),
+                                               ctypes.byref(pm), ctypes.byref(kv), 1, 2, 8)
+    assert need > B.STATIC_SCRATCH_BYTES
+    st = lib.dv_sparse_block_noalloc(ctypes.byref(a), ctypes.byref(m), ctypes.byref(ph), ctypes.byref(pm), None,
+                                     ctypes.byref(kv), FAKE, FAKE + 4096, 1, 2, 8, 0, 0, 0.25, None, None, 0, None)
+    assert st == B.DV_ERR_WORKSPACE
+    hdr = open(HEADER).read()
+    assert f"#define DV_STATIC_SCRATCH_BYTES (16u << 20)" in hdr and B.STATIC_SCRATCH_BYTES == 16 << 20
