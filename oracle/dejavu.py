@@ -310,6 +310,49 @@ def sparse_block(y, attn: Dict, mlp: Dict, K, V, pos: int, scale: float, *,
     return res
 
 
+def lookahead_layers(y, layers: Sequence[Dict], scale: float, k_heads: int, k_mlp: int,
+                     S0: Optional[Tuple] = None) -> Dict:
+    """Several decoder layers with the cross-layer look-ahead of Section 4.3 ("Approach").
+
+    The sets used by layer l come from its predictors applied to the normalised input of
+    the layer before it, so that they can be computed while that layer runs:
+        S^0     = (top-k_heads(SP_A^0(x_0)), top-k_mlp(SP_M^0(x_0))),  x_0 = LN1^0(y_0)
+        S^{l+1} = (top-k_heads(SP_A^{l+1}(x_l)), top-k_mlp(SP_M^{l+1}(x_l))), x_l = LN1^l(y_l)
+        y_{l+1} = sparse_block_l(y_l; S^l)
+    (the paper writes the predictor that produces S^{l+1} from y_l as SP^l; here it is
+    stored with layer l+1, whose heads and neurons it scores, reading R10). S0, if given,
+    replaces the prediction of S^0. layers[l] holds attn, mlp, K, V (the layer's cache
+    of this sequence), pos, pred_h and pred_m ({AT, BT}) and ln.
+    Returns {out, y: [y_0..y_L], S_A, S_M (per layer), K_new, V_new (per layer)}.
+    """
+    y = _f64(y)
+
+    def predict(layer, x):
+        s_h = predictor_scores(x, layer["pred_h"]["AT"], layer["pred_h"]["BT"])
+        s_m = predictor_scores(x, layer["pred_m"]["AT"], layer["pred_m"]["BT"])
+        return select_topk(s_h, k_heads), select_topk(s_m, k_mlp)
+
+    def norm1(layer, v):
+        ln = layer.get("ln") or {}
+        return layer_norm(v, ln.get("g1"), ln.get("be1"), ln.get("eps", 1e-5))
+
+    sets = S0 if S0 is not None else predict(layers[0], norm1(layers[0], y))
+    res = {"y": [y], "S_A": [], "S_M": [], "K_new": [], "V_new": []}
+    for l, layer in enumerate(layers):
+        nxt = predict(layers[l + 1], norm1(layer, y)) if l + 1 < len(layers) else None
+        r = sparse_block(y, layer["attn"], layer["mlp"], layer["K"], layer["V"], layer["pos"], scale,
+                         S_A=sets[0], S_M=sets[1], ln=layer.get("ln"))
+        res["S_A"].append(np.asarray(sets[0]))
+        res["S_M"].append(np.asarray(sets[1]))
+        res["K_new"].append(r["K_new"])
+        res["V_new"].append(r["V_new"])
+        y = r["out"]
+        res["y"].append(y)
+        sets = nxt
+    res["out"] = y
+    return res
+
+
 def dense_block(y, attn: Dict, mlp: Dict, K, V, pos: int, scale: float,
                 ln: Optional[Dict] = None) -> np.ndarray:
     """The dense layer: y~ = y + MHA(LN1(y)), y^ = y~ + MLP(LN2(y~))."""

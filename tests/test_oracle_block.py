@@ -116,3 +116,69 @@ def test_union_rows_matrix_form_equals_gather_form(step):
     assert _rel(got[2], O.mlp_sparse(Y[2], W1, None, W2, None, U)) < 1e-13
     # the empty union leaves b2
     assert np.array_equal(O.mlp_union_rows(Y, W1, None, W2, mlp["b2"], [])[3], mlp["b2"])
+
+
+def _stack(rng, L, **kw):
+    layers = []
+    for _ in range(L):
+        attn, mlp, K, V, ph, pm, ln = _layer(rng, **kw)
+        layers.append(dict(attn=attn, mlp=mlp, K=K, V=V, pos=6, pred_h=ph, pred_m=pm, ln=ln))
+    return layers
+
+
+def test_lookahead_one_layer_is_the_single_layer_call():
+    """With one layer the look-ahead recurrence is the single-layer look-ahead call:
+    both sets from LN1(y) of that layer (reading R8)."""
+    rng = np.random.default_rng(35)
+    (lay,) = _stack(rng, 1)
+    y = rng.normal(size=24)
+    r = O.lookahead_layers(y, [lay], 0.4, 2, 9)
+    ref = O.sparse_block(y, lay["attn"], lay["mlp"], lay["K"], lay["V"], 6, 0.4, pred_h=lay["pred_h"],
+                         pred_m=lay["pred_m"], k_heads=2, k_mlp=9, ln=lay["ln"], mode="lookahead")
+    assert np.array_equal(r["out"], ref["out"])
+    assert np.array_equal(r["S_A"][0], ref["S_A"]) and np.array_equal(r["S_M"][0], ref["S_M"])
+    assert np.array_equal(r["K_new"][0], ref["K_new"])
+
+
+@pytest.mark.parametrize("L", [2, 4])
+def test_lookahead_full_sets_are_the_dense_recurrence(L):
+    """Every head and neuron selected: L look-ahead layers equal L dense layers applied in
+    turn, each on its own cache."""
+    rng = np.random.default_rng(36)
+    layers = _stack(rng, L)
+    y = rng.normal(size=24)
+    r = O.lookahead_layers(y, layers, 0.4, 4, 48)
+    ref = y
+    for lay in layers:
+        ref = O.dense_block(ref, lay["attn"], lay["mlp"], lay["K"], lay["V"], 6, 0.4, ln=lay["ln"])
+    assert _rel(r["out"], ref) < 1e-12
+    assert len(r["y"]) == L + 1 and np.array_equal(r["y"][0], y)
+
+
+def test_lookahead_sets_come_from_the_previous_layers_input():
+    """A construction whose sets are known in closed form: each predictor reads
+    coordinates 0-3 of its input (AT selects them, BT is the identity), so its top-2 are
+    the two largest of those coordinates. y_0 ranks coordinates 0, 1 first; layer 0's
+    MLP bias flips the order, so y_1 ranks 2, 3 first. S^1 is predicted from layer 0's
+    input, hence {0, 1}; S^2 from layer 1's input, hence {2, 3}. (A predictor fed the
+    layer's own input would give {2, 3} for S^1.)"""
+    rng = np.random.default_rng(37)
+    layers = _stack(rng, 3, d=24, N=4, H=4, dh=6, r=4)
+    for l, lay in enumerate(layers):
+        for p in ("pred_h", "pred_m"):
+            AT = np.zeros((4, 24))
+            AT[np.arange(4), np.arange(4)] = 1.0
+            lay[p] = dict(AT=AT, BT=np.eye(4))
+        for n in ("Wq", "Wk", "Wv", "WoT"):
+            lay["attn"][n] = lay["attn"][n] * 1e-3
+        lay["attn"]["bo"] = np.zeros(24)
+        lay["mlp"]["W2T"] = lay["mlp"]["W2T"] * 1e-3
+        lay["mlp"]["b2"] = np.zeros(24)
+        lay["ln"].update(g1=np.ones(24), be1=np.zeros(24))
+    layers[0]["mlp"]["b2"][:4] = [-20.0, -20.0, 20.0, 20.0]
+    y = np.concatenate([[5.0, 4.0, -3.0, -4.0], rng.normal(0, 0.1, 20)])
+    r = O.lookahead_layers(y, layers, 0.4, 2, 2)
+    want = [[0, 1], [0, 1], [2, 3]]
+    assert [s.tolist() for s in r["S_A"]] == want
+    assert [s.tolist() for s in r["S_M"]] == want
+    assert np.argsort(-r["y"][1][:4])[:2].tolist() == [2, 3]
