@@ -275,13 +275,13 @@ def stream_ceiling(nbytes_list, steps, replicas=4):
     return out
 
 
-def _measure(stream, step, n, calls_per_step, only=None, every=1):
+def _measure(stream, step, n, calls_per_step, only=None, every=1, pairs=16):
     """Run n steps; per-call LaunchTimers (all launches, or only label `only`) on the
     steps i with i % every == 0. Returns (ms per step from events on `stream`, wall
     seconds, {label: [ms, ...]})."""
     import torch
     from paper_2310_17157_amd import binding as Bd
-    timers = [[Bd.LaunchTimer(16, only=only) for _ in range(calls_per_step)] if i % every == 0 else None
+    timers = [[Bd.LaunchTimer(pairs, only=only) for _ in range(calls_per_step)] if i % every == 0 else None
               for i in range(n)]
     torch.cuda.synchronize()
     ev0 = torch.cuda.Event(enable_timing=True)
@@ -419,6 +419,8 @@ def bench_b1(args, cfg):
            "sparse_block_kernels_us": block["us"], "sparse_block_kernels_frac": block["frac"],
            "stream_ceiling": ceil}
 
+    loop = lookahead_loop(args, cfg, layers, stream, scale, b.total)
+
     cpu = None
     if not args.no_cpu_baseline:
         print("[bench] timing the fp64 oracle on the host", file=sys.stderr, flush=True)
@@ -436,9 +438,44 @@ def bench_b1(args, cfg):
                    "kv_len": cfg.L, "rank": cfg.r, "k_mlp": cfg.k_mlp, "k_heads": cfg.k_heads, "batch": 1,
                    "weights": cfg.wdtype, "kv": cfg.kvdtype, "mode": args.mode, "replicas": args.replicas,
                    "parallelism": "none (1 GPU)"},
-        "roofline": roofline, "cpu_baseline": cpu, "hbm": hbm, "step_spread": spread, "kernels": kernels,
+        "roofline": roofline, "cpu_baseline": cpu, "hbm": hbm, "step_spread": spread, "lookahead_loop": loop,
+        "kernels": kernels,
         "wall_s_timed": round(wall, 4), "ms_per_step_all_launch_events": round(ms_all_events, 5),
     }
+
+
+def lookahead_loop(args, cfg, layers, stream, scale, layer_bytes):
+    """The replicas as consecutive layers of one token (dv_sparse_decode): the sets of
+    layer l+1 predicted from layer l's input inside layer l's launches (Section 4.3),
+    per layer and token, beside the single-layer calls timed above."""
+    import torch
+    from paper_2310_17157_amd import binding as Bd
+    objs = [L[1] for L in layers]
+    n = len(objs)
+    arr = Bd._layers_c(objs)
+    x = layers[0][0]["x"]
+    ws = torch.empty(Bd.decode_workspace_bytes(objs, cfg.k_heads, cfg.k_mlp), dtype=torch.uint8, device="cuda")
+    out = torch.empty_like(x)
+    hs = torch.empty((n, cfg.k_heads), dtype=torch.int32, device="cuda")
+    ms = torch.empty((n, cfg.k_mlp), dtype=torch.int32, device="cuda")
+
+    def step(i, timers=None):
+        if timers:
+            timers[0].arm()
+        Bd.dv_sparse_decode(objs, x, cfg.k_heads, cfg.k_mlp, scale, out=out, heads_out=hs, idx_out=ms, ws=ws,
+                            stream=stream, _arr=arr)
+        if timers:
+            timers[0].disarm()
+
+    for i in range(args.warmup):
+        step(i)
+    ms_call, _, _ = _measure(stream, step, args.steps, 1, every=10 ** 9)
+    _, _, per = _measure(stream, step, max(4, args.steps // 4), 1, pairs=64)
+    us = ms_call * 1e3 / n
+    gbps = layer_bytes / (us * 1e-6) / 1e9
+    return {"layers_per_call": n, "calls": args.steps, "us_per_layer_token": round(us, 2),
+            "GBps": round(gbps, 1), "frac": round(gbps / PEAK_HBM_GBPS, 4),
+            "launch_avg_us": {k: round(statistics.mean(v) * 1e3, 2) for k, v in per.items()}}
 
 
 def cpu_baseline_b32(cfg, th, heads, sets, pos):

@@ -242,6 +242,40 @@ dv_status dv_sparse_block(const dv_attn *a, const dv_mlp *m, const dv_predictor 
                           int32_t *heads_out, int32_t *idx_out, void *ws, size_t ws_bytes,
                           uint32_t flags, void *stream);
 
+/* ------------------------------------------------- several layers, look-ahead
+ * dv_sparse_decode: n_layers decoder layers for one token (B = 1) with the cross-layer
+ * look-ahead of Section 4.3 ("Approach"): the sets of layer l+1 are predicted from the
+ * input of layer l, so the prediction needs nothing layer l computes.
+ *   x_0 = LN1^0(y_0),  x_l = LN1^l(y_l)           (layer l's first layer norm)
+ *   S^0     = (top-k_heads(SP_A^0(x_0)), top-k_mlp(SP_M^0(x_0)))
+ *   S^{l+1} = (top-k_heads(SP_A^{l+1}(x_l)), top-k_mlp(SP_M^{l+1}(x_l)))
+ *   y_{l+1} = y~ + MLP^l_{S_M^l}(LN2^l(y~)),  y~ = y_l + MHA^l_{S_A^l}(x_l)
+ *   x_out   = y_{n_layers}
+ * SP^j are layer j's predictors (pa, pm of layers[j], which score layer j's heads and
+ * neurons). Layer l+1's predictor work runs inside layer l's launches (its first layer
+ * beside the Q/K/V rows over the same staged x_l, its scores and head set in a launch
+ * before the out-projection, its neuron set in the next QKV launch), so a layer costs
+ * five launches and layer 0 two more. Each layer updates its own KV cache as
+ * dv_sparse_attn does.
+ *   layers       [n_layers] layer descriptors; every layer has layer 0's shapes and types;
+ *                kv.B must be 1.
+ *   heads_out    [n_layers][k_heads] or NULL: S_A^l, ascending.
+ *   idx_out      [n_layers][k_mlp] or NULL: S_M^l, ascending.
+ * The sets are produced inside the call, so DV_VALIDATE has nothing to check here. */
+typedef struct dv_layer {
+  dv_attn attn;
+  dv_mlp mlp;
+  dv_predictor pa, pm;   /* head predictor (n_out = H), neuron predictor (n_out = N) */
+  dv_ln ln;
+  dv_kv kv;
+} dv_layer;
+
+size_t dv_sparse_decode_workspace_bytes(const dv_layer *layers, int32_t n_layers, int32_t k_heads,
+                                        int32_t k_mlp);
+dv_status dv_sparse_decode(const dv_layer *layers, int32_t n_layers, const float *x_in, float *x_out,
+                           int32_t k_heads, int32_t k_mlp, float scale, int32_t *heads_out,
+                           int32_t *idx_out, void *ws, size_t ws_bytes, uint32_t flags, void *stream);
+
 /* ------------------------------------------------- decoder layer, no allocation
  * dv_sparse_block_noalloc: for callers that cannot allocate device memory (work being
  * captured into a graph, serving loops or harnesses that forbid the allocator). The

@@ -67,6 +67,10 @@ class CLN(ctypes.Structure):
                 ("eps", c_float)]
 
 
+class CLayer(ctypes.Structure):
+    _fields_ = [("attn", CAttn), ("mlp", CMlp), ("pa", CPredictor), ("pm", CPredictor), ("ln", CLN), ("kv", CKV)]
+
+
 _PRED_ARGS = [POINTER(CPredictor), c_void_p, c_int32, c_int32, c_int32, c_float, c_void_p, c_int32,
               c_void_p, c_void_p, c_void_p, c_size_t, c_uint32, c_void_p]
 _SIGS = {
@@ -75,6 +79,9 @@ _SIGS = {
     "dv_launch_label": (c_char_p, [c_int32]),
     "dv_abi_version": (c_int32, []),
     "dv_stream_read": (c_int32, [c_void_p, c_size_t, c_void_p, c_void_p]),
+    "dv_sparse_decode_workspace_bytes": (c_size_t, [POINTER(CLayer), c_int32, c_int32, c_int32]),
+    "dv_sparse_decode": (c_int32, [POINTER(CLayer), c_int32, c_void_p, c_void_p, c_int32, c_int32, c_float,
+                                   c_void_p, c_void_p, c_void_p, c_size_t, c_uint32, c_void_p]),
     "dv_sparse_block_noalloc": (c_int32, [POINTER(CAttn), POINTER(CMlp), POINTER(CPredictor), POINTER(CPredictor),
                                           POINTER(CLN), POINTER(CKV), c_void_p, c_void_p, c_int32, c_int32,
                                           c_int32, c_int32, c_int32, c_float, c_void_p, c_void_p, c_uint32,
@@ -418,6 +425,49 @@ def dv_sparse_block(attn: Attn, mlp: MLP, pred_h: Predictor, pred_m: Predictor, 
                              _ptr(out), B, k_heads, k_mlp, mode, batch_mode, scale, _ptr(heads_out),
                              _ptr(idx_out), *_wsarg(ws), flags, _stream(stream))
     _check("dv_sparse_block", st)
+    return out, heads_out, idx_out
+
+
+def _layers_c(layers):
+    """layers: sequence of (attn, mlp, pred_h, pred_m, kv, ln) tuples -> a dv_layer array."""
+    arr = (CLayer * len(layers))()
+    for i, (attn, mlp, ph, pm, kv, ln) in enumerate(layers):
+        arr[i] = CLayer(attn.c(), mlp.c(), ph.c(), pm.c(), ln.c() if ln is not None else CLN(None, None, None, None,
+                                                                                                 1e-5), kv.c())
+    return arr
+
+
+def decode_workspace_bytes(layers, k_heads, k_mlp) -> int:
+    arr = _layers_c(layers)
+    return load().dv_sparse_decode_workspace_bytes(arr, len(layers), k_heads, k_mlp)
+
+
+def dv_sparse_decode(layers, x, k_heads, k_mlp, scale, out=None, heads_out=None, idx_out=None, ws=None,
+                     flags=0, stream=None, _arr=None):
+    """Several layers for one token with the cross-layer look-ahead (Section 4.3): the
+    sets of layer l+1 are predicted from layer l's input inside layer l's launches.
+    layers: sequence of (attn, mlp, pred_h, pred_m, kv, ln). Returns
+    (out, heads [L, k_heads], idx [L, k_mlp])."""
+    lib = load()
+    arr = _arr if _arr is not None else _layers_c(layers)
+    L = len(layers)
+    d = arr[0].attn.d
+    _tensor("x", x, _F32, 2, (1, d), dev=False)
+    _tensor("out", out, _F32, 2, (1, d), optional=True, dev=False)
+    _tensor("heads_out", heads_out, _I32, 2, (L, k_heads), optional=True, dev=False)
+    _tensor("idx_out", idx_out, _I32, 2, (L, k_mlp), optional=True, dev=False)
+    _gpu("arguments", x, out, heads_out, idx_out)
+    if out is None:
+        out = torch.empty_like(x)
+    if heads_out is None:
+        heads_out = torch.empty((L, k_heads), dtype=torch.int32, device=x.device)
+    if idx_out is None:
+        idx_out = torch.empty((L, k_mlp), dtype=torch.int32, device=x.device)
+    if ws is None:
+        ws = _workspace(lib.dv_sparse_decode_workspace_bytes(arr, L, k_heads, k_mlp), x.device)
+    st = lib.dv_sparse_decode(arr, L, _ptr(x), _ptr(out), k_heads, k_mlp, scale, _ptr(heads_out), _ptr(idx_out),
+                              *_wsarg(ws), flags, _stream(stream))
+    _check("dv_sparse_decode", st)
     return out, heads_out, idx_out
 
 

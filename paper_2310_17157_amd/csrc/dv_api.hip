@@ -119,12 +119,11 @@ extern "C" const char* dv_launch_label(int32_t i) {
 }
 
 // ------------------------------------------------------------------ helpers
-static bool dtype_ok(int t) { return t == DV_F16 || t == DV_F32; }
-static int chunk_elems(int t) { return 16 / elem_bytes(t); }
-static bool ws_ok(void* ws) { return ws != nullptr && (reinterpret_cast<uintptr_t>(ws) & 255u) == 0; }
-static constexpr int kMaxWidth = 16000;
+bool dv::dtype_ok(int t) { return t == DV_F16 || t == DV_F32; }
+int dv::chunk_elems(int t) { return 16 / elem_bytes(t); }
+bool dv::ws_ok(void* ws) { return ws != nullptr && (reinterpret_cast<uintptr_t>(ws) & 255u) == 0; }
 
-static dv_status check_mlp(const dv_mlp* m) {
+dv_status dv::check_mlp(const dv_mlp* m) {
   if (m == nullptr || m->W1T == nullptr || m->W2T == nullptr) return DV_ERR_NULL;
   if (!dtype_ok(m->wtype)) return DV_ERR_DTYPE;
   if (m->reserved != 0) return DV_ERR_ARG;
@@ -135,7 +134,7 @@ static dv_status check_mlp(const dv_mlp* m) {
   return DV_OK;
 }
 
-static dv_status check_attn(const dv_attn* a) {
+dv_status dv::check_attn(const dv_attn* a) {
   if (a == nullptr || a->Wq == nullptr || a->Wk == nullptr || a->Wv == nullptr || a->WoT == nullptr)
     return DV_ERR_NULL;
   if (!dtype_ok(a->wtype)) return DV_ERR_DTYPE;
@@ -146,7 +145,7 @@ static dv_status check_attn(const dv_attn* a) {
   return DV_OK;
 }
 
-static dv_status check_kv(const dv_kv* kv, const dv_attn* a, int B) {
+dv_status dv::check_kv(const dv_kv* kv, const dv_attn* a, int B) {
   if (kv == nullptr || kv->K == nullptr || kv->V == nullptr || kv->pos == nullptr) return DV_ERR_NULL;
   if (!dtype_ok(kv->ktype)) return DV_ERR_DTYPE;
   if (kv->reserved != 0) return DV_ERR_ARG;
@@ -158,7 +157,7 @@ static dv_status check_kv(const dv_kv* kv, const dv_attn* a, int B) {
   return DV_OK;
 }
 
-static dv_status check_ln(const dv_ln* ln) {
+dv_status dv::check_ln(const dv_ln* ln) {
   if (ln == nullptr) return DV_OK;
   const float* p[4] = {ln->g1, ln->be1, ln->g2, ln->be2};
   for (const float* q : p)
@@ -194,7 +193,7 @@ struct MlpWs {
 };
 
 // Row-split partial sums of a gathered row-axpy of width d.
-static size_t axpy_partial_bytes(int d) { return (size_t)kAxpyMaxRowSplit * d * sizeof(float); }
+size_t dv::axpy_partial_bytes(int d) { return (size_t)kAxpyMaxRowSplit * d * sizeof(float); }
 
 static size_t mlp_ws_layout(const dv_mlp* m, int B, int n_idx, Workspace& w, MlpWs* o) {
   o->h = w.take<float>((size_t)B * n_idx * sizeof(float));
@@ -383,7 +382,7 @@ extern "C" size_t dv_sparse_block_workspace_bytes(const dv_attn* a, const dv_mlp
   return block_ws_layout(a, m, pa, pm, kv->cap, B, k_heads, k_mlp, w, &o);
 }
 
-static dv_status check_predictor_for(const dv_predictor* p, int d, int n_out) {
+dv_status dv::check_predictor_for(const dv_predictor* p, int d, int n_out) {
   if (p == nullptr || p->AT == nullptr || p->BT == nullptr) return DV_ERR_NULL;
   if (!dtype_ok(p->wtype)) return DV_ERR_DTYPE;
   if (p->d != d || p->n_out != n_out || p->r <= 0) return DV_ERR_SHAPE;

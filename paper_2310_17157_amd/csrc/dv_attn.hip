@@ -17,7 +17,7 @@
 
 namespace dv {
 
-template <typename T, typename KT, int NW, int U, int KX>
+template <typename T, typename KT, int NW, int U, int KX, bool LN>
 __global__ void __launch_bounds__(NW * 64) k_qkv(QkvArgs a) {
   extern __shared__ float smem[];
   constexpr int NT = NW * 64;
@@ -35,8 +35,13 @@ __global__ void __launch_bounds__(NW * 64) k_qkv(QkvArgs a) {
   __syncthreads();
   if (wg == 0 && a.heads_ws != nullptr)
     for (int i = threadIdx.x; i < a.n_heads; i += NT) a.heads_ws[i] = hset[i];
-  const int per_mat = a.n_heads * a.dh;
+  const int per_mat = a.n_heads * a.dh, nqkv = 3 * per_mat;
   auto row_ptr = [&](int row) {
+    if (row >= nqkv) {   // appended predictor rows
+      const int p = row - nqkv;
+      return p < a.r0 ? static_cast<const T*>(a.AT0) + (size_t)p * a.d
+                      : static_cast<const T*>(a.AT1) + (size_t)(p - a.r0) * a.d;
+    }
     const int m = row / per_mat;
     const int rem = row - m * per_mat;
     const int j = rem / a.dh, t = rem - j * a.dh;
@@ -44,6 +49,14 @@ __global__ void __launch_bounds__(NW * 64) k_qkv(QkvArgs a) {
     return static_cast<const T*>(W) + ((size_t)hset[j] * a.dh + t) * a.d;
   };
   auto epi = [&](int row, float v) {
+    if (row >= nqkv) {
+      const int p = row - nqkv;
+      if (p < a.r0)
+        a.hid0[p] = v;
+      else
+        a.hid1[p - a.r0] = v;
+      return;
+    }
     const int m = row / per_mat;
     const int rem = row - m * per_mat;
     const int j = rem / a.dh, t = rem - j * a.dh;
@@ -58,8 +71,8 @@ __global__ void __launch_bounds__(NW * 64) k_qkv(QkvArgs a) {
       C[((size_t)head * a.cap + a.pos) * a.dh + t] = (KT)v;
     }
   };
-  rowdot_flat<T, NW, U, KX, false>(row_ptr, epi, 3 * per_mat, a.d, a.x, nullptr, nullptr, 0.f, xs, red, part,
-                                         nullptr, wg, nwg);
+  rowdot_flat<T, NW, U, KX, LN>(row_ptr, epi, nqkv + a.r0 + a.r1, a.d, a.x, a.g, a.be, a.eps, xs, red, part, nullptr,
+                                wg, nwg);
 }
 
 // CUs left without a QKV workgroup when a selection is hosted in the launch.
@@ -72,7 +85,7 @@ static hipError_t launch_qkv_t(const QkvArgs& a, hipStream_t st) {
   // fabric arbitration race ahead of the others
   constexpr int NW = 16, U = 2;
   constexpr int NT = NW * 64;
-  const int nrows = 3 * a.n_heads * a.dh;
+  const int nrows = 3 * a.n_heads * a.dh + a.r0 + a.r1;
   // One workgroup per CU, each a contiguous range of rows (rowdot_flat). A hosted
   // selection gets one more workgroup, and a few CUs are left free for it to start at once.
   const int cus = device_cu_count();
@@ -80,9 +93,16 @@ static hipError_t launch_qkv_t(const QkvArgs& a, hipStream_t st) {
   size_t lds = (size_t)(a.d + NW) * sizeof(float) + (size_t)a.n_heads * sizeof(int32_t) +
                (size_t)rowdot_flat_part(nrows, blocks, NW) * sizeof(float) + 16;
   if (a.sel_n > 0) lds = max(lds, (size_t)kSelBins * 4 + kSelSm(NT) * sizeof(int));
-  const hipError_t e = ensure_dyn_lds(reinterpret_cast<const void*>(k_qkv<T, KT, NW, U, KX>), lds);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((k_qkv<T, KT, NW, U, KX>), dim3(blocks + (a.sel_n > 0 ? 1 : 0)), dim3(NW * 64), lds, st, a);
+  const dim3 grid(blocks + (a.sel_n > 0 ? 1 : 0));
+  if (a.g != nullptr) {
+    const hipError_t e = ensure_dyn_lds(reinterpret_cast<const void*>(k_qkv<T, KT, NW, U, KX, true>), lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((k_qkv<T, KT, NW, U, KX, true>), grid, dim3(NW * 64), lds, st, a);
+  } else {
+    const hipError_t e = ensure_dyn_lds(reinterpret_cast<const void*>(k_qkv<T, KT, NW, U, KX, false>), lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((k_qkv<T, KT, NW, U, KX, false>), grid, dim3(NW * 64), lds, st, a);
+  }
   return hipGetLastError();
 }
 

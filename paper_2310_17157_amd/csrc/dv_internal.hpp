@@ -299,7 +299,8 @@ hipError_t launch_pred_scores(int wtype, const PredScoreArgs& a, hipStream_t st)
 // Gathered row-dot for Q/K/V of the selected heads (B = 1).
 struct QkvArgs {
   int d, H, dh, cap, pos, n_heads;
-  const float* x;                   // input, already layer-normalised where the block asks for it
+  const float* x;                   // input (layer-normalised here if g is set)
+  const float* g; const float* be; float eps;   // optional LN of x inside the launch (g NULL: none)
   const void* Wq; const void* Wk; const void* Wv;
   const float* bq; const float* bk; const float* bv;
   void* K; void* V;                 // [H][cap][dh] of this sequence
@@ -309,6 +310,11 @@ struct QkvArgs {
   // Top-k selection run by one extra workgroup of the launch (sel_n == 0: none).
   const float* sel_scores; int sel_n; int sel_k; int32_t* sel_idx; int32_t* sel_idx_out;
   uint32_t* clear; int clear_n;     // counters of a later row-axpy to zero (optional)
+  // Rows of up to two more matrices of the weights' type dotted with the same input
+  // after the Q/K/V rows (the next layer's predictor first layers, which read this
+  // layer's normalised input): hid0[j] = x-hat . AT0[j] (j < r0), likewise AT1 (r0, r1 = 0: none).
+  const void* AT0; int r0; float* hid0;
+  const void* AT1; int r1; float* hid1;
 };
 hipError_t launch_qkv(int wtype, int kvtype, const QkvArgs& a, hipStream_t st);
 
@@ -490,6 +496,18 @@ dv_status batch_block(const dv_attn* a, const dv_mlp* m, const dv_predictor* pa,
                       size_t ws_bytes, hipStream_t hs);
 // DV_VALIDATE: check B ascending sets of n indices in [0, range) (synchronises `st`).
 dv_status validate_sets_sync(const int32_t* set, int B, int n, int range, int32_t* flag, hipStream_t st);
+
+// Host-side argument checks shared by the entry points (dv_api.hip).
+constexpr int kMaxWidth = 16000;   // widest row the row-dot kernels stage in LDS
+bool dtype_ok(int t);
+int chunk_elems(int t);            // elements per 16-byte chunk
+bool ws_ok(void* ws);              // non-NULL and 256-byte aligned
+dv_status check_mlp(const dv_mlp* m);
+dv_status check_attn(const dv_attn* a);
+dv_status check_kv(const dv_kv* kv, const dv_attn* a, int B);
+dv_status check_ln(const dv_ln* ln);
+dv_status check_predictor_for(const dv_predictor* p, int d, int n_out);
+size_t axpy_partial_bytes(int d);  // row-split partial sums of a row-axpy of width d
 
 // Split-KV chunk length (positions per attention workgroup); at most kAttnMaxSplit
 // chunks per head.
