@@ -478,6 +478,131 @@ def lookahead_loop(args, cfg, layers, stream, scale, layer_bytes):
             "launch_avg_us": {k: round(statistics.mean(v) * 1e3, 2) for k, v in per.items()}}
 
 
+PAPER_KERNEL_CLAIMS = ("context, not a target (A100, Triton, 8-way tensor parallel): the fused sparse MLP up to "
+                       "4.5x and sparse attention up to 5x faster than index-then-multiply in PyTorch, both faster "
+                       "than dense up to density 0.8 (Appendix E); the unfused gather moves 3x the bytes (Section 4.4)")
+
+
+def density_sweep(args, cfg, densities=(0.05, 0.1, 0.2, 0.3, 0.4, 0.5, 0.6, 0.7, 0.8, 0.9, 1.0), reps=20):
+    """Appendix E's kernel benchmark on this GPU: the sparse MLP and the sparse attention
+    at a range of densities, three ways each: the fused gathered kernels of this library
+    (dv_sparse_mlp, dv_sparse_attn), the dense layer with torch's library GEMVs, and the
+    unfused form (index_select of the selected rows into a new tensor, then the same
+    GEMVs on it). Weights are cycled over replicas beyond the 256 MB last-level cache;
+    each point is the median of `reps` calls timed with events on the stream."""
+    import numpy as np
+    import torch
+    import torch.nn.functional as F
+    from paper_2310_17157_amd import binding as Bd
+    from synth import make_layer
+
+    R = 2
+    reps_ = [make_layer(cfg, seed=r, device="cuda", with_predictors=False) for r in range(R)]
+    scale = 1.0 / float(np.sqrt(cfg.dh))
+    d, N, H, dh = cfg.d, cfg.N, cfg.H, cfg.dh
+    x = reps_[0]["x"]
+    x16 = x.half()
+    stream = torch.cuda.current_stream()
+
+    def med_us(fn):
+        for i in range(3):
+            fn(i)
+        ts = []
+        for i in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn(i)
+            b.record(stream)
+            b.synchronize()
+            ts.append(a.elapsed_time(b) * 1e3)
+        return round(statistics.median(ts), 2)
+
+    rng = np.random.default_rng(5)
+    mlp_objs = [Bd.MLP(t["W1T"], t["W2T"], t["b1"], t["b2"]) for t in reps_]
+    attn_objs = [Bd.Attn(t["Wq"], t["Wk"], t["Wv"], t["WoT"], H, t["bq"], t["bk"], t["bv"], t["bo"]) for t in reps_]
+    kvs = [Bd.KVCache(t["K"], t["V"], [cfg.L - 1]) for t in reps_]
+    pos = cfg.L - 1
+
+    def dense_mlp(i):
+        t = reps_[i % R]
+        h = torch.relu(F.linear(x16, t["W1T"], t["b1"].half()))
+        return torch.matmul(h, t["W2T"]) + t["b2"]
+
+    def dense_attn(i):
+        t = reps_[i % R]
+        q, k, v = (F.linear(x16, t[w], t[b].half()).view(H, 1, dh) for w, b in (("Wq", "bq"), ("Wk", "bk"),
+                                                                                   ("Wv", "bv")))
+        Kc, Vc = t["K"][0], t["V"][0]
+        Kc[:, pos] = k[:, 0]
+        Vc[:, pos] = v[:, 0]
+        sc = torch.matmul(Kc[:, :pos + 1], q.transpose(1, 2).contiguous()).float() * scale      # [H, L, 1]
+        p = torch.softmax(sc, dim=1).half()
+        o = torch.matmul(p.transpose(1, 2).contiguous(), Vc[:, :pos + 1])                       # [H, 1, dh]
+        return torch.matmul(o.reshape(1, H * dh), t["WoT"]) + t["bo"]
+
+    t_dense_mlp = med_us(dense_mlp)
+    t_dense_attn = med_us(dense_attn)
+    mlp_bytes_dense = 2 * N * d * cfg.wbytes
+    attn_bytes_dense = 4 * H * dh * d * cfg.wbytes + 2 * H * (pos + 1) * dh * cfg.kvbytes
+    out = {"mlp": [], "attn": []}
+    for p in densities:
+        k = max(1, int(round(p * N)))
+        S = [torch.tensor(np.sort(rng.choice(N, k, replace=False)).astype(np.int32), device="cuda") for _ in range(R)]
+        o_m = torch.empty_like(x)
+        ws_m = torch.empty(Bd.mlp_workspace_bytes(mlp_objs[0], 1, k), dtype=torch.uint8, device="cuda")
+        fused = med_us(lambda i: Bd.dv_sparse_mlp(mlp_objs[i % R], x, S[i % R], out=o_m, ws=ws_m))
+
+        def unfused_mlp(i):
+            t, idx = reps_[i % R], S[i % R].long()
+            W1s = t["W1T"].index_select(0, idx)
+            W2s = t["W2T"].index_select(0, idx)
+            h = torch.relu(F.linear(x16, W1s, t["b1"].half().index_select(0, idx)))
+            return torch.matmul(h, W2s) + t["b2"]
+
+        unfused = med_us(unfused_mlp)
+        b = 2 * k * d * cfg.wbytes
+        out["mlp"].append({"density": p, "k": k, "fused_us": fused, "unfused_us": unfused, "dense_us": t_dense_mlp,
+                           "fused_GBps": round(b / fused / 1e3, 1),
+                           "unfused_over_fused": round(unfused / fused, 2), "dense_over_fused": round(t_dense_mlp / fused, 2)})
+        kh = max(1, int(round(p * H)))
+        Hs = [torch.tensor(np.sort(rng.choice(H, kh, replace=False)).astype(np.int32), device="cuda").view(1, -1)
+              for _ in range(R)]
+        o_a = torch.empty_like(x)
+        ws_a = torch.empty(Bd.attn_workspace_bytes(attn_objs[0], kvs[0], 1, kh), dtype=torch.uint8, device="cuda")
+        fused_a = med_us(lambda i: Bd.dv_sparse_attn(attn_objs[i % R], x, kvs[i % R], Hs[i % R], scale, out=o_a,
+                                                     ws=ws_a))
+
+        def unfused_attn(i):
+            t, hs = reps_[i % R], Hs[i % R].view(-1).long()
+            rows = (hs[:, None] * dh + torch.arange(dh, device="cuda")[None, :]).reshape(-1)
+            q, k_, v = (F.linear(x16, t[w].index_select(0, rows), t[b].half().index_select(0, rows)).view(kh, 1, dh)
+                        for w, b in (("Wq", "bq"), ("Wk", "bk"), ("Wv", "bv")))
+            t["K"][0][hs, pos] = k_[:, 0]
+            t["V"][0][hs, pos] = v[:, 0]
+            Kc = t["K"][0].index_select(0, hs)
+            Vc = t["V"][0].index_select(0, hs)
+            sc = torch.matmul(Kc[:, :pos + 1], q.transpose(1, 2).contiguous()).float() * scale
+            pr = torch.softmax(sc, dim=1).half()
+            o = torch.matmul(pr.transpose(1, 2).contiguous(), Vc[:, :pos + 1])
+            return torch.matmul(o.reshape(1, kh * dh), t["WoT"].index_select(0, rows)) + t["bo"]
+
+        unfused_a = med_us(unfused_attn)
+        ba = 4 * kh * dh * d * cfg.wbytes + 2 * kh * (pos + 1) * dh * cfg.kvbytes
+        out["attn"].append({"density": round(kh / H, 4), "k_heads": kh, "fused_us": fused_a, "unfused_us": unfused_a,
+                            "dense_us": t_dense_attn, "fused_GBps": round(ba / fused_a / 1e3, 1),
+                            "unfused_over_fused": round(unfused_a / fused_a, 2),
+                            "dense_over_fused": round(t_dense_attn / fused_a, 2)})
+    cross = {}
+    for part in ("mlp", "attn"):
+        faster = [r["density"] for r in out[part] if r["fused_us"] < r["dense_us"]]
+        cross[part] = {"fused_faster_than_dense_up_to_density": max(faster) if faster else None,
+                       "max_unfused_over_fused": max(r["unfused_over_fused"] for r in out[part])}
+    return {"sweep": "density", "workload": cfg.name, "reps": reps, "replicas": R,
+            "dense_mlp_us": t_dense_mlp, "dense_mlp_GBps": round(mlp_bytes_dense / t_dense_mlp / 1e3, 1),
+            "dense_attn_us": t_dense_attn, "dense_attn_GBps": round(attn_bytes_dense / t_dense_attn / 1e3, 1),
+            "summary": cross, "paper": PAPER_KERNEL_CLAIMS, **out}
+
+
 def cpu_baseline_b32(cfg, th, heads, sets, pos):
     """The fp64 oracle's attention (own heads and cache) + union MLP for one sequence."""
     import numpy as np
@@ -596,6 +721,9 @@ def main():
     ap.add_argument("--replicas", type=int, default=4)
     ap.add_argument("--mode", choices=["lookahead", "sequential"], default="lookahead")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sweep", choices=["density"], default=None,
+                    help="instead of the step: the sparse MLP and attention at densities 0.05-1.0, fused vs dense "
+                         "vs index-then-multiply (Appendix E)")
     ap.add_argument("--no-b32", dest="b32", action="store_false",
                     help="skip the batch-32 sub-record of the default batch-1 run")
     ap.add_argument("--copy-calib-gib", type=float, default=0.0,
@@ -622,6 +750,9 @@ def main():
         return
 
     cfg = get_config(args.workload)
+    if args.sweep == "density":
+        print(json.dumps(density_sweep(args, cfg)))
+        return
     rec = bench_b1(args, cfg) if cfg.B == 1 else bench_batch(args, cfg)
     if cfg.B == 1 and args.b32 and cfg.name == "opt175b_b1":
         # the batch-32 workload of the same layer shape, as a sub-record of the line
