@@ -238,6 +238,40 @@ def mha_sparse(y, attn: Dict, K, V, pos: int, S_A, scale: float
     return out, K_new, V_new, heads
 
 
+def mha_sparse_kvfill(y, attn: Dict, K, V, Y, valid, pos: int, S_A, scale: float):
+    """Sparsified MHA for one token with the missing-KV rule of Section 4.2 ("Approach").
+
+    Keys and values are computed only for the selected heads, so a head that was not
+    selected at some past token has no cache row there. The token's attention input y
+    is kept for every token (Y[pos] = y); when a head is selected, the rows it is
+    missing are computed from the kept inputs (K[h, t] = Y[t] W^K_h + b, likewise V)
+    before the head attends, and marked present. valid[h, t] is True where row t of
+    head h holds that token's key and value; after the call it is True for every row
+    0..pos of the selected heads and False at pos for the others.
+    Y: [cap, d]; valid: [H, cap] bool (neither is modified; copies are returned).
+    Returns (out [d], K_new, V_new, Y_new, valid_new).
+    """
+    y = _f64(y)
+    H, cap, dh = np.asarray(K).shape
+    K_fill = _f64(K).copy()
+    V_fill = _f64(V).copy()
+    Y_new = _f64(Y).copy()
+    valid_new = np.asarray(valid, dtype=bool).copy()
+    Y_new[pos] = y
+    for i in S_A:
+        i = int(i)
+        for t in range(pos):
+            if not valid_new[i, t]:
+                K_fill[i, t] = head_projection(Y_new[t], attn["Wk"], attn.get("bk"), i, dh)
+                V_fill[i, t] = head_projection(Y_new[t], attn["Wv"], attn.get("bv"), i, dh)
+                valid_new[i, t] = True
+    out, K_new, V_new, _ = mha_sparse(y, attn, K_fill, V_fill, pos, S_A, scale)
+    sel = set(int(i) for i in S_A)
+    for i in range(H):
+        valid_new[i, pos] = i in sel
+    return out, K_new, V_new, Y_new, valid_new
+
+
 def mha_dense_einsum(y, attn: Dict, K, V, pos: int, scale: float) -> np.ndarray:
     """Dense multi-head attention written as textbook batched tensor algebra.
 

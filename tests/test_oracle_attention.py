@@ -128,3 +128,72 @@ def test_pos_zero_attends_only_the_fresh_token():
     v2 = a["Wv"][8:12] @ y
     assert np.allclose(heads[2], v2, rtol=0, atol=1e-14)
     assert np.allclose(out, v2 @ a["WoT"][8:12], rtol=0, atol=1e-14)
+
+
+def _kv_layer(rng, d=16, H=5, dh=4, cap=12):
+    attn = {n: rng.normal(0, 0.3, (H * dh, d)) for n in ("Wq", "Wk", "Wv", "WoT")}
+    attn.update(bq=rng.normal(0, 0.1, H * dh), bk=rng.normal(0, 0.1, H * dh), bv=rng.normal(0, 0.1, H * dh),
+                bo=rng.normal(0, 0.1, d))
+    return attn
+
+
+def test_kvfill_decode_equals_a_run_with_every_heads_cache_written():
+    """Section 4.2's missing-KV rule over 10 tokens with changing head sets: each step's
+    output is the output of a run in which every head's key and value were written at
+    every token (same arithmetic, computed when the head is next selected instead of
+    at its own token), bit for bit; and every selected head's cache is complete."""
+    rng = np.random.default_rng(40)
+    d, H, dh, cap, T = 16, 5, 4, 12, 10
+    attn = _kv_layer(rng, d, H, dh, cap)
+    K = np.zeros((H, cap, dh))
+    V = np.zeros((H, cap, dh))
+    Y = np.zeros((cap, d))
+    valid = np.zeros((H, cap), dtype=bool)
+    Kf, Vf = K.copy(), V.copy()                       # the reference: all heads written
+    for pos in range(T):
+        y = rng.normal(size=d)
+        S = np.sort(rng.choice(H, 2, replace=False))
+        out, K, V, Y, valid = O.mha_sparse_kvfill(y, attn, K, V, Y, valid, pos, S, 0.5)
+        _, Kf, Vf, _ = O.mha_sparse(y, attn, Kf, Vf, pos, range(H), 0.5)   # writes all heads' rows
+        ref, _, _, _ = O.mha_sparse(y, attn, Kf, Vf, pos, S, 0.5)
+        assert np.array_equal(out, ref), pos
+        for h in S:
+            assert valid[h, :pos + 1].all()
+            assert np.array_equal(K[h, :pos + 1], Kf[h, :pos + 1]) and np.array_equal(V[h, :pos + 1], Vf[h, :pos + 1])
+        for h in set(range(H)) - set(S.tolist()):
+            assert not valid[h, pos]
+        assert np.array_equal(Y[pos], y)
+
+
+def test_kvfill_with_a_complete_cache_is_the_plain_sparse_attention():
+    """Nothing missing: the rule reduces to mha_sparse (nothing recomputed)."""
+    rng = np.random.default_rng(41)
+    attn = _kv_layer(rng)
+    K = rng.normal(size=(5, 12, 4))
+    V = rng.normal(size=(5, 12, 4))
+    Y = rng.normal(size=(12, 16))
+    valid = np.ones((5, 12), dtype=bool)
+    y = rng.normal(size=16)
+    out, Kn, Vn, Yn, vn = O.mha_sparse_kvfill(y, attn, K, V, Y, valid, 7, [1, 3], 0.5)
+    ref, Kr, Vr, _ = O.mha_sparse(y, attn, K, V, 7, [1, 3], 0.5)
+    assert np.array_equal(out, ref) and np.array_equal(Kn, Kr) and np.array_equal(Vn, Vr)
+    assert np.array_equal(Yn[:7], Y[:7]) and vn[[1, 3], 7].all() and not vn[[0, 2, 4], 7].any()
+
+
+def test_kvfill_only_touches_missing_rows_of_selected_heads():
+    """A missing row is recomputed from the kept input of its own token, and only for a
+    selected head; present rows are never rewritten (they keep whatever they hold)."""
+    rng = np.random.default_rng(42)
+    attn = _kv_layer(rng)
+    K = np.full((5, 12, 4), 7.0)
+    V = np.full((5, 12, 4), -7.0)
+    Y = rng.normal(size=(12, 16))
+    valid = np.ones((5, 12), dtype=bool)
+    valid[2, 3] = valid[4, 5] = False
+    y = rng.normal(size=16)
+    _, Kn, Vn, _, vn = O.mha_sparse_kvfill(y, attn, K, V, Y, valid, 6, [2], 0.5)
+    k3 = (np.asarray(attn["Wk"])[8:12] @ Y[3]) + attn["bk"][8:12]
+    assert np.allclose(Kn[2, 3], k3, rtol=1e-14) and vn[2, 3]
+    assert (Kn[4, 5] == 7.0).all() and not vn[4, 5]                  # head 4 not selected: still missing
+    rows = [(h, t) for h in range(5) for t in range(6) if (h, t) != (2, 3)]
+    assert all((Kn[h, t] == 7.0).all() and (Vn[h, t] == -7.0).all() for h, t in rows)
