@@ -219,6 +219,27 @@ dv_status dv_sparse_attn(const dv_attn *a, const float *x, int32_t B, const dv_k
                          const int32_t *heads, int32_t n_heads, float scale, float *out,
                          void *ws, size_t ws_bytes, uint32_t flags, void *stream);
 
+/* ------------------------------------------ sparse attention, missing keys and values
+ * dv_sparse_attn_kvfill: dv_sparse_attn for one sequence (kv->B = 1) with the missing-KV
+ * rule of Section 4.2 ("Approach"). Only selected heads write their key and value of a
+ * token, so a head selected now may lack rows of past tokens; the attention input of
+ * every token is kept, and the missing rows of the selected heads are computed from it
+ * (K[h][t] = Y[t] W^K_h + bk_h, likewise V) before those heads attend.
+ *   x      [d] fp32 device: this token's attention input (normalised, as for dv_sparse_attn).
+ *   Y      [cap][d] fp32 device, in/out: the kept inputs; the call writes Y[pos] = x.
+ *   valid  [H][cap] uint8 device, in/out: 1 where row t of head h holds token t's key
+ *          and value. On return valid[h][0..pos] = 1 for every selected head and
+ *          valid[h][pos] = 0 for the others; rows above pos are not touched. A sequence
+ *          starts with 1 for the rows its prompt filled and 0 elsewhere.
+ *   out, heads, n_heads, scale, ws, flags as for dv_sparse_attn (workspace: the
+ *          dv_sparse_attn_workspace_bytes query with B = 1).
+ * Cost: one launch more than dv_sparse_attn; it reads no weights when no selected head
+ * misses a row, otherwise each selected head's W^K and W^V rows once per 8 missing
+ * positions. Limits: pos <= 32768 (else DV_ERR_UNSUPPORTED). */
+dv_status dv_sparse_attn_kvfill(const dv_attn *a, const float *x, const dv_kv *kv, float *Y, uint8_t *valid,
+                                const int32_t *heads, int32_t n_heads, float scale, float *out, void *ws,
+                                size_t ws_bytes, uint32_t flags, void *stream);
+
 /* ------------------------------------------------------------- decoder layer
  * dv_sparse_block: one decoder layer for one token per sequence (Section 4.3):
  *   S_A  = top-k_heads(SP_A(LN1(y)))

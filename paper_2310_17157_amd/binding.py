@@ -79,6 +79,8 @@ _SIGS = {
     "dv_launch_label": (c_char_p, [c_int32]),
     "dv_abi_version": (c_int32, []),
     "dv_stream_read": (c_int32, [c_void_p, c_size_t, c_void_p, c_void_p]),
+    "dv_sparse_attn_kvfill": (c_int32, [POINTER(CAttn), c_void_p, POINTER(CKV), c_void_p, c_void_p, c_void_p,
+                                        c_int32, c_float, c_void_p, c_void_p, c_size_t, c_uint32, c_void_p]),
     "dv_sparse_decode_workspace_bytes": (c_size_t, [POINTER(CLayer), c_int32, c_int32, c_int32]),
     "dv_sparse_decode": (c_int32, [POINTER(CLayer), c_int32, c_void_p, c_void_p, c_int32, c_int32, c_float,
                                    c_void_p, c_void_p, c_void_p, c_size_t, c_uint32, c_void_p]),
@@ -283,6 +285,12 @@ class KVCache:
         self.K, self.V = K, V
         self._pos = (c_int32 * K.shape[0])(*[int(p) for p in pos])
 
+    def set_pos(self, pos):
+        """Move to new decode positions (the struct handed to the library keeps pointing
+        at the same host array)."""
+        for b, p in enumerate(pos):
+            self._pos[b] = int(p)
+
     def c(self) -> CKV:
         # checked and built once per set of tensors (calls are on the hot path)
         key = tuple(id(t) for t in (self.K, self.V, self._pos,))
@@ -396,6 +404,32 @@ def dv_sparse_attn(attn: Attn, x, kv: KVCache, heads, scale, out=None, ws=None, 
     st = lib.dv_sparse_attn(ctypes.byref(ca), _ptr(x), B, ctypes.byref(ck), _ptr(heads), n_heads, scale,
                             _ptr(out), *_wsarg(ws), flags, _stream(stream))
     _check("dv_sparse_attn", st)
+    return out
+
+
+def dv_sparse_attn_kvfill(attn: Attn, x, kv: KVCache, Y, valid, heads, scale, out=None, ws=None, flags=0,
+                          stream=None):
+    """dv_sparse_attn for one sequence with the missing-KV rule of Section 4.2: Y [cap][d]
+    fp32 keeps every token's attention input, valid [H][cap] uint8 marks the cache rows
+    that hold their token's key and value (both updated in place)."""
+    lib = load()
+    ca, ck = attn.c(), kv.c()
+    _tensor("x", x, _F32, 2, (1, ca.d), dev=False)
+    _tensor("Y", Y, _F32, 2, (ck.cap, ca.d), dev=False)
+    _tensor("valid", valid, (torch.uint8,), 2, (ca.H, ck.cap), dev=False)
+    _tensor("heads", heads, _I32, dev=False)
+    n_heads = heads.shape[-1]
+    if heads.numel() != n_heads:
+        raise ValueError("heads: one sequence's set")
+    _tensor("out", out, _F32, 2, (1, ca.d), optional=True, dev=False)
+    _gpu("arguments", x, Y, valid, heads, out)
+    if out is None:
+        out = torch.empty((1, ca.d), dtype=torch.float32, device=x.device)
+    if ws is None:
+        ws = _workspace(lib.dv_sparse_attn_workspace_bytes(ctypes.byref(ca), ctypes.byref(ck), 1, n_heads), x.device)
+    st = lib.dv_sparse_attn_kvfill(ctypes.byref(ca), _ptr(x), ctypes.byref(ck), _ptr(Y), _ptr(valid), _ptr(heads),
+                                   n_heads, scale, _ptr(out), *_wsarg(ws), flags, _stream(stream))
+    _check("dv_sparse_attn_kvfill", st)
     return out
 
 

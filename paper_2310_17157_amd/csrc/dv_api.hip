@@ -277,13 +277,14 @@ extern "C" size_t dv_sparse_attn_workspace_bytes(const dv_attn* a, const dv_kv* 
 }
 
 static dv_status enqueue_attention(const dv_attn* a, const dv_kv* kv, const AttnWs& o, int n_heads,
-                                   float scale, hipStream_t hs) {
+                                   float scale, hipStream_t hs, uint8_t* valid = nullptr) {
   const int pos = kv->pos[0];
   AttnArgs at{};
   at.H = a->H; at.dh = a->dh; at.cap = kv->cap; at.posb[0] = pos; at.n_heads = n_heads;
   at.chunk = attn_chunk(n_heads, pos + 1, a->dh, kv->ktype);
   at.n_split = (pos + 1 + at.chunk - 1) / at.chunk;
   at.q = o.q; at.heads = o.heads; at.K = kv->K; at.V = kv->V; at.scale = scale; at.part = o.part;
+  at.valid = valid;
   DV_LAUNCH("attn", hs, launch_attn(kv->ktype, at, 1, hs));
   return DV_OK;
 }
@@ -336,6 +337,66 @@ extern "C" dv_status dv_sparse_attn(const dv_attn* a, const float* x, int32_t B,
   DV_LAUNCH("qkv", hs, launch_qkv(a->wtype, kv->ktype, q, hs));
   st = enqueue_attention(a, kv, o, n_heads, scale, hs);
   if (st != DV_OK) return st;
+  AxpyArgs ax{};
+  ax.d = a->d; ax.nrows = n_heads * a->dh; ax.M = a->WoT; ax.m_rows = a->H * a->dh; ax.set = o.heads;
+  ax.dh = a->dh; ax.coef = nullptr; ax.part = o.part; ax.n_split = attn_nsplit(a, kv, n_heads);
+  ax.resid = nullptr; ax.bias = a->bo; ax.out = out; ax.out2 = nullptr; ax.partial = o.axp; ax.cnt = o.axc;
+  return enqueue_axpy("oproj", a->wtype, ax, hs);
+}
+
+// ------------------------------------------- sparse attention, missing keys and values
+static constexpr int kMaxFillPos = 32768;   // the fill launch lists missing positions in LDS
+
+extern "C" dv_status dv_sparse_attn_kvfill(const dv_attn* a, const float* x, const dv_kv* kv, float* Y,
+                                           uint8_t* valid, const int32_t* heads, int32_t n_heads, float scale,
+                                           float* out, void* ws, size_t ws_bytes, uint32_t flags, void* stream) {
+  trace_reset();
+  dv_status st = check_attn(a);
+  if (st != DV_OK) return st;
+  if (x == nullptr || out == nullptr || Y == nullptr || valid == nullptr || (heads == nullptr && n_heads > 0))
+    return DV_ERR_NULL;
+  if (n_heads < 0 || n_heads > a->H) return DV_ERR_SHAPE;
+  if ((st = check_kv(kv, a, 1)) != DV_OK) return st;
+  if (!aligned16(x) || !aligned16(out) || !aligned16(Y)) return DV_ERR_ALIGN;
+  if (flags & ~(uint32_t)(DV_DETERMINISTIC | DV_VALIDATE)) return DV_ERR_ARG;
+  if (!isfinite(scale)) return DV_ERR_ARG;
+  if (a->bo != nullptr && !aligned16(a->bo)) return DV_ERR_ALIGN;
+  if (kv->pos[0] > kMaxFillPos) return DV_ERR_UNSUPPORTED;
+  if (!ws_ok(ws)) return DV_ERR_WORKSPACE;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  Workspace w(ws);
+  AttnWs o;
+  if (attn_ws_layout(a, kv->cap, 1, n_heads, w, &o) > ws_bytes) return DV_ERR_WORKSPACE;
+  if (flags & DV_VALIDATE) {
+    st = validate_sets(heads, 1, n_heads, a->H, o.flag, hs);
+    if (st != DV_OK) return st;
+  }
+  const int pos = kv->pos[0];
+  KvFillArgs f{};
+  f.d = a->d; f.H = a->H; f.dh = a->dh; f.cap = kv->cap; f.pos = pos; f.n_heads = n_heads;
+  f.x = x; f.Y = Y; f.valid = valid; f.heads = heads;
+  f.Wk = a->Wk; f.Wv = a->Wv; f.bk = a->bk; f.bv = a->bv; f.K = kv->K; f.V = kv->V;
+  if (n_heads > 0) {
+    DV_LAUNCH("kv_fill", hs, launch_kv_fill(a->wtype, kv->ktype, f, hs));
+  } else if (hipMemcpyAsync(Y + (size_t)pos * a->d, x, (size_t)a->d * sizeof(float), hipMemcpyDeviceToDevice,
+                            hs) != hipSuccess) {
+    return DV_ERR_HIP;   // (no head selected: nothing to compute, the input is still kept)
+  }
+  QkvArgs q{};
+  q.d = a->d; q.H = a->H; q.dh = a->dh; q.cap = kv->cap; q.pos = pos; q.n_heads = n_heads;
+  q.x = x;
+  q.Wq = a->Wq; q.Wk = a->Wk; q.Wv = a->Wv; q.bq = a->bq; q.bk = a->bk; q.bv = a->bv;
+  q.K = kv->K; q.V = kv->V; q.q = o.q; q.heads_in = heads; q.heads_ws = o.heads;
+  q.clear = o.axc; q.clear_n = kAxpyMaxSpans; q.valid = valid;
+  DV_LAUNCH("qkv", hs, launch_qkv(a->wtype, kv->ktype, q, hs));   // also marks row pos of every head
+  if (n_heads == 0) {
+    AxpyArgs ax{};
+    ax.d = a->d; ax.nrows = 0; ax.M = a->WoT; ax.m_rows = a->H * a->dh; ax.set = o.heads; ax.dh = 0;
+    ax.coef = o.q; ax.bias = a->bo; ax.out = out;
+    DV_LAUNCH("oproj", hs, launch_axpy(a->wtype, ax, hs));
+    return DV_OK;
+  }
+  if ((st = enqueue_attention(a, kv, o, n_heads, scale, hs, valid)) != DV_OK) return st;
   AxpyArgs ax{};
   ax.d = a->d; ax.nrows = n_heads * a->dh; ax.M = a->WoT; ax.m_rows = a->H * a->dh; ax.set = o.heads;
   ax.dh = a->dh; ax.coef = nullptr; ax.part = o.part; ax.n_split = attn_nsplit(a, kv, n_heads);

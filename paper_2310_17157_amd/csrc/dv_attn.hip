@@ -35,6 +35,12 @@ __global__ void __launch_bounds__(NW * 64) k_qkv(QkvArgs a) {
   __syncthreads();
   if (wg == 0 && a.heads_ws != nullptr)
     for (int i = threadIdx.x; i < a.n_heads; i += NT) a.heads_ws[i] = hset[i];
+  if (wg == 0 && a.valid != nullptr)
+    for (int h = threadIdx.x; h < a.H; h += NT) {
+      uint8_t in = 0;
+      for (int i = 0; i < a.n_heads; ++i) in |= hset[i] == h;
+      a.valid[(size_t)h * a.cap + a.pos] = in;
+    }
   const int per_mat = a.n_heads * a.dh, nqkv = 3 * per_mat;
   auto row_ptr = [&](int row) {
     if (row >= nqkv) {   // appended predictor rows
@@ -157,6 +163,8 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   const char* Kb = static_cast<const char*>(a.K) + hoff;
   const char* Vb = static_cast<const char*>(a.V) + hoff;
 
+  if (a.valid != nullptr)   // every row this workgroup attends holds its key and value
+    for (int t = t0 + (int)threadIdx.x; t < tend; t += 256) a.valid[((size_t)b * a.H + head) * a.cap + t] = 1;
   float m = -INFINITY, l = 0.f;
   float o[E];
 #pragma unroll
@@ -332,6 +340,91 @@ static hipError_t launch_attn_t(const AttnArgs& a, int B, hipStream_t st) {
 
 hipError_t launch_attn(int kvtype, const AttnArgs& a, int B, hipStream_t st) {
   return kvtype == DV_F16 ? launch_attn_t<_Float16>(a, B, st) : launch_attn_t<float>(a, B, st);
+}
+
+// ------------------------------------------------------------ missing keys and values
+// One workgroup per (selected head, block of kFillRows rows of [W^K_h; W^V_h]). It lists
+// the head's missing positions (valid == 0 below pos), then streams each of its rows once
+// per group of MT positions: a wavefront holds 64 chunks of the row and dots them with the
+// matching elements of the MT kept inputs (read through L2: every workgroup of the
+// head reads the same few rows of Y). Nothing is read when nothing is missing.
+constexpr int kFillRows = 16;
+
+template <typename T, typename KT, int MT>
+__global__ void __launch_bounds__(256) k_kv_fill(KvFillArgs a) {
+  constexpr int E = Chunk<T>::E;
+  extern __shared__ int flist[];
+  __shared__ int fcnt;
+  const int nrb = (2 * a.dh + kFillRows - 1) / kFillRows;
+  const int j = blockIdx.x / nrb, rb = blockIdx.x - j * nrb;
+  const int head = min(max(a.heads[j], 0), a.H - 1);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (blockIdx.x == 0)
+    for (int e = threadIdx.x; e < a.d; e += 256) a.Y[(size_t)a.pos * a.d + e] = a.x[e];
+  if (threadIdx.x == 0) fcnt = 0;
+  __syncthreads();
+  const uint8_t* vh = a.valid + (size_t)head * a.cap;
+  for (int t = threadIdx.x; t < a.pos; t += 256)
+    if (vh[t] == 0) flist[atomicAdd(&fcnt, 1)] = t;
+  __syncthreads();
+  const int m = fcnt;
+  if (m == 0) return;
+  const int nch = a.d / E;
+  const int r0 = rb * kFillRows, r1 = min(2 * a.dh, r0 + kFillRows);
+  for (int t0 = 0; t0 < m; t0 += MT) {
+    for (int r = r0 + wave; r < r1; r += 4) {
+      const bool isv = r >= a.dh;
+      const int tr = isv ? r - a.dh : r;
+      const T* W = static_cast<const T*>(isv ? a.Wv : a.Wk) + ((size_t)head * a.dh + tr) * a.d;
+      float acc[MT];
+#pragma unroll
+      for (int u = 0; u < MT; ++u) acc[u] = 0.f;
+      for (int c = lane; c < nch; c += 64) {
+        float w[E];
+        unpack<T>(ld_stream(W + (size_t)c * E), w);
+#pragma unroll
+        for (int u = 0; u < MT; ++u) {
+          if (t0 + u < m) {
+            const float* y = a.Y + (size_t)flist[t0 + u] * a.d + (size_t)c * E;
+#pragma unroll
+            for (int e = 0; e < E; e += 4) {
+              const f32x4 yv = *reinterpret_cast<const f32x4*>(y + e);
+              acc[u] = fmaf(w[e], yv[0], acc[u]);
+              acc[u] = fmaf(w[e + 1], yv[1], acc[u]);
+              acc[u] = fmaf(w[e + 2], yv[2], acc[u]);
+              acc[u] = fmaf(w[e + 3], yv[3], acc[u]);
+            }
+          }
+        }
+      }
+      const float* bias = isv ? a.bv : a.bk;
+      const float bb = bias ? bias[(size_t)head * a.dh + tr] : 0.f;
+#pragma unroll
+      for (int u = 0; u < MT; ++u) {
+        const float v = wave_sum(acc[u]);
+        if (lane == 0 && t0 + u < m) {
+          KT* C = static_cast<KT*>(isv ? a.V : a.K);
+          C[((size_t)head * a.cap + flist[t0 + u]) * a.dh + tr] = (KT)(v + bb);
+        }
+      }
+    }
+  }
+}
+
+template <typename T, typename KT>
+static hipError_t launch_kv_fill_t(const KvFillArgs& a, hipStream_t st) {
+  const int nrb = (2 * a.dh + kFillRows - 1) / kFillRows;
+  const size_t lds = (size_t)max(a.pos, 1) * sizeof(int);
+  const hipError_t e = ensure_dyn_lds(reinterpret_cast<const void*>(k_kv_fill<T, KT, 8>), lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((k_kv_fill<T, KT, 8>), dim3(max(1, a.n_heads) * nrb), dim3(256), lds, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_fill(int wtype, int kvtype, const KvFillArgs& a, hipStream_t st) {
+  if (wtype == DV_F16)
+    return kvtype == DV_F16 ? launch_kv_fill_t<_Float16, _Float16>(a, st) : launch_kv_fill_t<_Float16, float>(a, st);
+  return kvtype == DV_F16 ? launch_kv_fill_t<float, _Float16>(a, st) : launch_kv_fill_t<float, float>(a, st);
 }
 
 }  // namespace dv

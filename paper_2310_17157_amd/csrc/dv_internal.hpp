@@ -307,6 +307,7 @@ struct QkvArgs {
   float* q;                         // [n_heads][dh] out
   const int32_t* heads_in;          // [n_heads] the head set
   int32_t* heads_ws;                // optional [n_heads] out: the set, clamped (one workgroup)
+  uint8_t* valid;                   // optional [H][cap]: row pos marked present for the set, absent otherwise
   // Top-k selection run by one extra workgroup of the launch (sel_n == 0: none).
   const float* sel_scores; int sel_n; int sel_k; int32_t* sel_idx; int32_t* sel_idx_out;
   uint32_t* clear; int clear_n;     // counters of a later row-axpy to zero (optional)
@@ -334,8 +335,24 @@ struct AttnArgs {
   // the out-projection's fp16 coefficients C[b][p * dh + t] (p: h's place in the union
   // list ulist[0..*ucount)) instead of a partial; the rest of C is zeroed beforehand.
   _Float16* C; int ldc; const int32_t* ulist; const int32_t* ucount;
+  uint8_t* valid;                   // optional [B][H][cap]: rows attended are marked present
 };
 hipError_t launch_attn(int kvtype, const AttnArgs& a, int B, hipStream_t st);
+
+// Missing keys and values (B = 1): for every selected head, the cache rows t < pos
+// whose valid[h][t] is 0 are computed from the kept inputs Y[t] (K[h][t] = Y[t] . W^K_h
+// rows + bk, likewise V); Y[pos] = x is kept for later tokens. The valid marks are set
+// by the launches that follow (QKV at pos, attention over 0..pos), never here.
+struct KvFillArgs {
+  int d, H, dh, cap, pos, n_heads;
+  const float* x;                   // [d] this token's attention input
+  float* Y;                         // [cap][d] kept attention inputs
+  const uint8_t* valid;             // [H][cap]
+  const int32_t* heads;             // [n_heads]
+  const void* Wk; const void* Wv; const float* bk; const float* bv;
+  void* K; void* V;                 // [H][cap][dh]
+};
+hipError_t launch_kv_fill(int wtype, int kvtype, const KvFillArgs& a, hipStream_t st);
 
 // Gathered row-axpy: out = resid + bias + sum_rows coef[row] * M[rowidx(row)], tiled by
 // 128-byte column tiles; every workgroup sums all selected rows of its tile.
