@@ -50,6 +50,7 @@ Parity pins: every function here is checked in tests/test_oracle_*.py against
 something other than itself (closed forms, brute force on tiny shapes, invariants,
 library routines for special cases, and the values printed in Tables 1-2).
 """
+import math
 from typing import Dict, Optional, Sequence, Tuple
 
 import numpy as np
@@ -114,21 +115,35 @@ def select_threshold(s, t: float) -> np.ndarray:
 
 
 # -------------------------------------------------------------------------- MLP
-def mlp_dense(y, W1T, b1, W2T, b2) -> np.ndarray:
-    """Dense MLP: sigma(y W^1 + b1) (W^2)^T + b2 with sigma = ReLU."""
+_erf = np.vectorize(math.erf, otypes=[F64])
+
+
+def activation(z, act: str = "relu") -> np.ndarray:
+    """sigma of Eq. (1): ReLU (OPT, reading R4) or GeLU, x * Phi(x) with the normal CDF
+    Phi(x) = (1 + erf(x / sqrt 2)) / 2 (the exact form, not a tanh approximation)."""
+    z = _f64(z)
+    if act == "relu":
+        return np.maximum(z, 0.0)
+    if act == "gelu":
+        return 0.5 * z * (1.0 + _erf(z / math.sqrt(2.0)))
+    raise ValueError(act)
+
+
+def mlp_dense(y, W1T, b1, W2T, b2, act: str = "relu") -> np.ndarray:
+    """Dense MLP: sigma(y W^1 + b1) (W^2)^T + b2."""
     y = _f64(y)
     z = y @ _f64(W1T).T
     if b1 is not None:
         z = z + _f64(b1)
-    a = np.maximum(z, 0.0)
+    a = activation(z, act)
     out = a @ _f64(W2T)
     if b2 is not None:
         out = out + _f64(b2)
     return out
 
 
-def mlp_sparse(y, W1T, b1, W2T, b2, S) -> np.ndarray:
-    """Eq. (1): sum over i in S of ReLU(y . W^1_i + b1_i) * W^2_i, plus b2 once.
+def mlp_sparse(y, W1T, b1, W2T, b2, S, act: str = "relu") -> np.ndarray:
+    """Eq. (1): sum over i in S of sigma(y . W^1_i + b1_i) * W^2_i, plus b2 once.
 
     Gather form: one neuron at a time, in the order S lists them.
     y: [d] (one token). Returns [d].
@@ -143,12 +158,12 @@ def mlp_sparse(y, W1T, b1, W2T, b2, S) -> np.ndarray:
         z = float(np.dot(y, _f64(W1T[i])))
         if b1 is not None:
             z += float(b1[i])
-        a = z if z > 0.0 else 0.0
+        a = (z if z > 0.0 else 0.0) if act == "relu" else float(activation(z, act))
         out += a * _f64(W2T[i])
     return out
 
 
-def mlp_sparse_masked(y, W1T, b1, W2T, b2, S) -> np.ndarray:
+def mlp_sparse_masked(y, W1T, b1, W2T, b2, S, act: str = "relu") -> np.ndarray:
     """Eq. (1) in mask form: (ReLU(y W^1 + b1) * 1_S) (W^2)^T + b2.
 
     An independent formulation of mlp_sparse (dense products, then a 0/1 mask).
@@ -159,7 +174,7 @@ def mlp_sparse_masked(y, W1T, b1, W2T, b2, S) -> np.ndarray:
     z = y @ _f64(W1T).T
     if b1 is not None:
         z = z + _f64(b1)
-    a = np.maximum(z, 0.0) * mask
+    a = activation(z, act) * mask
     out = a @ _f64(W2T)
     if b2 is not None:
         out = out + _f64(b2)
@@ -177,6 +192,33 @@ def mlp_activations(y, W1T, b1, S) -> np.ndarray:
             z += float(b1[int(i)])
         out[j] = z if z > 0.0 else 0.0
     return out
+
+
+# ----------------------------------------------------------- 4-bit weights (W4A16)
+Q4_BLOCK = 32   # elements per scale (reading R15)
+
+
+def dequant_q4(packed, scales, d: int) -> np.ndarray:
+    """Rows of 4-bit weights (Section 5.2 "Compatibility with Quantization", W4A16;
+    format of reading R15): element j of a row is scales[j // 32] * (q_j - 8), where q_j
+    is the low 4 bits of byte j // 2 for even j and the high 4 bits for odd j.
+    packed: [rows, d/2] uint8; scales: [rows, d/32] (fp16 values). Returns [rows, d] fp64."""
+    packed = np.asarray(packed, dtype=np.uint8)
+    rows = packed.shape[0]
+    out = np.empty((rows, d), dtype=F64)
+    sc = _f64(scales)
+    for r in range(rows):
+        for j in range(d):
+            byte = int(packed[r, j // 2])
+            q = (byte & 15) if j % 2 == 0 else (byte >> 4)
+            out[r, j] = sc[r, j // Q4_BLOCK] * (q - 8)
+    return out
+
+
+def dequant_q4_rows(packed, scales, d: int, rows) -> np.ndarray:
+    """dequant_q4 of the listed rows only (a gathered set), in list order."""
+    rows = [int(i) for i in rows]
+    return dequant_q4(np.asarray(packed)[rows], np.asarray(scales)[rows], d)
 
 
 # -------------------------------------------------------------------- attention
@@ -419,7 +461,7 @@ def mlp_batch(Y, W1T, b1, W2T, b2, sets, mode: str = "union") -> np.ndarray:
     return np.stack([mlp_sparse(Y[b], W1T, b1, W2T, b2, sets[b]) for b in range(Y.shape[0])])
 
 
-def mlp_union_rows(Y, W1T, b1, W2T, b2, U, rows_per_step: int = 2048) -> np.ndarray:
+def mlp_union_rows(Y, W1T, b1, W2T, b2, U, rows_per_step: int = 2048, act: str = "relu") -> np.ndarray:
     """Eq. (1) on the rows U for every sequence of a batch, as matrix products.
 
     out[b] = b2 + sum_{i in U} ReLU(Y[b] . W^1_i + b1_i) W^2_i, taken over slices of U
@@ -439,7 +481,7 @@ def mlp_union_rows(Y, W1T, b1, W2T, b2, U, rows_per_step: int = 2048) -> np.ndar
         z = Y @ _f64(W1T[rows]).T                 # [B, rows]
         if b1 is not None:
             z = z + _f64(b1)[rows]
-        out += np.maximum(z, 0.0) @ _f64(W2T[rows])
+        out += activation(z, act) @ _f64(W2T[rows])
     return out
 
 

@@ -132,3 +132,19 @@ def zipf_mlp_sets(cfg: Config, seed: int, s: Optional[float] = None) -> np.ndarr
 def to_numpy64(t: torch.Tensor) -> np.ndarray:
     """Exact upcast of stored values (fp16, including subnormals, or fp32) to float64."""
     return t.detach().to("cpu").to(torch.float64).numpy()
+
+
+def quantize_q4(W: torch.Tensor, block: int = 32):
+    """4-bit weights in blocks of `block` elements of a row, for W4A16 inputs: per block
+    an fp16 scale s = max|w| / 7 (1 for an all-zero block) and codes
+    q = clamp(round(w / s), -8, 7) + 8 in [0, 15], two per byte (low nibble first).
+    Returns (packed uint8 [rows, d/2], scales fp16 [rows, d/block]) on W's device."""
+    rows, d = W.shape
+    assert d % block == 0 and block % 2 == 0
+    w = W.float().view(rows, d // block, block)
+    s = (w.abs().amax(dim=-1) / 7.0).half()
+    s = torch.where(s == 0, torch.ones_like(s), s)
+    q = torch.clamp(torch.round(w / s.float()[..., None]), -8, 7).to(torch.int32) + 8
+    q = q.view(rows, d)
+    packed = (q[:, 0::2] | (q[:, 1::2] << 4)).to(torch.uint8)
+    return packed.contiguous(), s.contiguous()

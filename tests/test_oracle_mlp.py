@@ -134,3 +134,59 @@ def test_folded_gaussian_fact_half_of_relu_outputs_are_zero():
     frac0 = np.mean(W1T @ y <= 0)
     sd = np.sqrt(0.25 / N)
     assert abs(frac0 - 0.5) < 5 * sd
+
+
+# ---------------------------------------------------------------- GeLU, W4A16
+def test_gelu_matches_torch_exact_gelu():
+    z = np.linspace(-6, 6, 241)
+    ref = torch.nn.functional.gelu(torch.tensor(z, dtype=torch.float64), approximate="none").numpy()
+    assert np.allclose(O.activation(z, "gelu"), ref, rtol=1e-14, atol=1e-15)
+    assert np.array_equal(O.activation(z, "relu"), np.maximum(z, 0))
+
+
+@pytest.mark.parametrize("act", ["relu", "gelu"])
+def test_gelu_mlp_forms_agree_and_match_torch(act):
+    rng = np.random.default_rng(60)
+    y, W1T, b1, W2T, b2 = _mlp(rng, 24, 40)
+    W1T, W2T = W1T * 50, W2T * 50       # pre-activations of order 1: GeLU away from its linear part
+    S = np.sort(rng.choice(40, 13, replace=False))
+    assert _rel(O.mlp_sparse(y, W1T, b1, W2T, b2, S, act), O.mlp_sparse_masked(y, W1T, b1, W2T, b2, S, act)) < 1e-13
+    assert _rel(O.mlp_sparse(y, W1T, b1, W2T, b2, range(40), act), O.mlp_dense(y, W1T, b1, W2T, b2, act)) < 1e-13
+    f = torch.nn.functional
+    h = f.linear(torch.tensor(y), torch.tensor(W1T), torch.tensor(b1))
+    h = f.gelu(h, approximate="none") if act == "gelu" else f.relu(h)
+    ref = (h @ torch.tensor(W2T) + torch.tensor(b2)).numpy()
+    assert _rel(O.mlp_dense(y, W1T, b1, W2T, b2, act), ref) < 1e-13
+
+
+def test_dequant_q4_hand_values():
+    """Byte 0x80 holds q = 0 (low nibble, even element) and q = 8 (high nibble): -8 s, 0.
+    Byte 0xF3: q = 3 then 15: -5 s, 7 s. The second block of 32 uses its own scale."""
+    packed = np.zeros((1, 32), dtype=np.uint8)       # d = 64: two blocks
+    packed[0, 0] = 0x80
+    packed[0, 1] = 0xF3
+    packed[0, 16] = 0x9A                              # element 32: q = 10, element 33: q = 9
+    packed[0, 2:16] = 0x88
+    packed[0, 17:] = 0x88
+    scales = np.array([[0.5, 2.0]], dtype=np.float16)
+    w = O.dequant_q4(packed, scales, 64)[0]
+    assert w[:4].tolist() == [-4.0, 0.0, -2.5, 3.5]
+    assert w[32:34].tolist() == [4.0, 2.0]
+    assert np.count_nonzero(w) == 5
+
+
+def test_quantizer_and_dequant_round_trip_within_half_a_step():
+    """synth.quantize_q4 (the input format) against the oracle's dequantisation: every
+    weight is reproduced within half its block's step (round to nearest), codes fit 4
+    bits, and the largest magnitude of each block maps to +-7 steps."""
+    from synth import quantize_q4
+    rng = np.random.default_rng(61)
+    W = torch.tensor(rng.normal(0, 0.02, (5, 96)), dtype=torch.float16)
+    packed, scales = quantize_q4(W)
+    assert packed.dtype == torch.uint8 and packed.shape == (5, 48) and scales.shape == (5, 3)
+    deq = O.dequant_q4(packed.numpy(), scales.numpy(), 96)
+    step = np.repeat(scales.numpy().astype(np.float64), 32, axis=1)
+    err = np.abs(deq - W.numpy().astype(np.float64))
+    assert (err <= 0.5 * step * (1 + 1e-3) + 1e-12).all()
+    assert np.allclose(np.abs(deq).reshape(5, 3, 32).max(axis=-1), 7 * scales.numpy().astype(np.float64))
+    assert np.array_equal(O.dequant_q4_rows(packed.numpy(), scales.numpy(), 96, [3, 1]), deq[[3, 1]])
