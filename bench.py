@@ -420,6 +420,8 @@ def bench_b1(args, cfg):
            "stream_ceiling": ceil}
 
     loop = lookahead_loop(args, cfg, layers, stream, scale, b.total)
+    kvfill = kvfill_steps(cfg, layers[0][0], stream, scale)
+    q4 = q4_mlp(args, cfg, layers, stream)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -439,7 +441,7 @@ def bench_b1(args, cfg):
                    "weights": cfg.wdtype, "kv": cfg.kvdtype, "mode": args.mode, "replicas": args.replicas,
                    "parallelism": "none (1 GPU)"},
         "roofline": roofline, "cpu_baseline": cpu, "hbm": hbm, "step_spread": spread, "lookahead_loop": loop,
-        "kernels": kernels,
+        "kvfill": kvfill, "w4a16_mlp": q4, "kernels": kernels,
         "wall_s_timed": round(wall, 4), "ms_per_step_all_launch_events": round(ms_all_events, 5),
     }
 
@@ -601,6 +603,102 @@ def density_sweep(args, cfg, densities=(0.05, 0.1, 0.2, 0.3, 0.4, 0.5, 0.6, 0.7,
             "dense_mlp_us": t_dense_mlp, "dense_mlp_GBps": round(mlp_bytes_dense / t_dense_mlp / 1e3, 1),
             "dense_attn_us": t_dense_attn, "dense_attn_GBps": round(attn_bytes_dense / t_dense_attn / 1e3, 1),
             "summary": cross, "paper": PAPER_KERNEL_CLAIMS, **out}
+
+
+def q4_mlp(args, cfg, layers, stream):
+    """Section 5.2's W4A16 setting: the sparse MLP of each replica with its W1T and W2T
+    rows stored as 4-bit codes in blocks of 32 with an fp16 scale (dv_sparse_mlp_q4,
+    same neuron sets as the block's), per call and per launch, against the fp16 rows."""
+    import torch
+    from paper_2310_17157_amd import binding as Bd
+    from synth import quantize_q4
+    objs = []
+    for t, *_ in layers:
+        P1, S1 = quantize_q4(t["W1T"])
+        P2, S2 = quantize_q4(t["W2T"])
+        objs.append(Bd.MLPQ4(P1, S1, P2, S2, t["b1"], t["b2"]))
+    sets = [L[5].view(-1) for L in layers]          # each replica's neuron set from the timed steps
+    x = layers[0][0]["x"]
+    out = torch.empty_like(x)
+    ws = torch.empty(Bd.load().dv_sparse_mlp_q4_workspace_bytes(__import__("ctypes").byref(objs[0].c()), cfg.k_mlp),
+                     dtype=torch.uint8, device="cuda")
+    n = len(objs)
+
+    def step(i, timers=None):
+        if timers:
+            timers[0].arm()
+        Bd.dv_sparse_mlp_q4(objs[i % n], x, sets[i % n], out=out, ws=ws, stream=stream)
+        if timers:
+            timers[0].disarm()
+
+    for i in range(args.warmup):
+        step(i)
+    ms_call, _, _ = _measure(stream, step, args.steps, 1, every=10 ** 9)
+    _, _, per = _measure(stream, step, args.steps, 1)
+    row = cfg.d // 2 + cfg.d // 16
+    nb = 2 * cfg.k_mlp * row
+    us = {k: statistics.mean(v) * 1e3 for k, v in per.items()}
+    return {"bytes": nb, "fp16_bytes": 2 * cfg.k_mlp * cfg.d * cfg.wbytes, "us_per_call": round(ms_call * 1e3, 2),
+            "launch_avg_us": {k: round(v, 2) for k, v in us.items()},
+            "GBps_launches": round(nb / (sum(us.values()) * 1e-6) / 1e9, 1),
+            "frac_launches": round(nb / (sum(us.values()) * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4)}
+
+
+def kvfill_steps(cfg, t, stream, scale, T=32):
+    """Section 4.2's missing-KV rule over T consecutive tokens with independent uniform
+    head sets (k_heads of H per token): dv_sparse_attn_kvfill per token against
+    dv_sparse_attn on the same sets (which leaves the missing rows missing), and the
+    fill launch alone; missing rows filled per token, counted on the host."""
+    import numpy as np
+    import torch
+    from paper_2310_17157_amd import binding as Bd
+    H, cap, d = cfg.H, cfg.kv_cap, cfg.d
+    attn = Bd.Attn(t["Wq"], t["Wk"], t["Wv"], t["WoT"], H)
+    p0 = cap - T
+    kv = Bd.KVCache(t["K"], t["V"], [p0])
+    Y = torch.randn((cap, d), dtype=torch.float32, device="cuda")
+    valid = torch.zeros((H, cap), dtype=torch.uint8, device="cuda")
+    valid[:, :p0] = 1
+    rng = np.random.default_rng(17)
+    sets = [torch.tensor(np.sort(rng.choice(H, cfg.k_heads, replace=False)).astype(np.int32), device="cuda")
+            for _ in range(T)]
+    last = np.full(H, p0 - 1)
+    filled = []
+    for s_ in range(T):
+        S = sets[s_].cpu().numpy()
+        filled.append(int(sum(p0 + s_ - 1 - last[h] for h in S)))
+        last[S] = p0 + s_
+    ws = torch.empty(Bd.attn_workspace_bytes(attn, kv, 1, cfg.k_heads), dtype=torch.uint8, device="cuda")
+    out = torch.empty((1, d), dtype=torch.float32, device="cuda")
+    x = torch.randn((1, d), device="cuda")
+    res = {}
+    for key in ("kvfill", "plain"):
+        valid[:, p0:] = 0
+        valid[:, :p0] = 1
+        tm = [Bd.LaunchTimer(8, only="kv_fill") for _ in range(T)] if key == "kvfill" else None
+        torch.cuda.synchronize()
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record(stream)
+        for s_ in range(T):
+            kv.set_pos([p0 + s_])
+            if key == "kvfill":
+                tm[s_].arm()
+                Bd.dv_sparse_attn_kvfill(attn, x, kv, Y, valid, sets[s_], scale, out=out, ws=ws, stream=stream)
+                tm[s_].disarm()
+            else:
+                Bd.dv_sparse_attn(attn, x, kv, sets[s_].view(1, -1), scale, out=out, ws=ws, stream=stream)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        res[key] = ev0.elapsed_time(ev1) * 1e3 / T
+        if tm:
+            fill = [ms for tmr in tm for _, ms in tmr.times_ms()]
+            for tmr in tm:
+                tmr.close()
+            res["fill_launch_us"] = round(statistics.mean(fill) * 1e3, 2)
+    kv.set_pos([cap - 1])
+    return {"tokens": T, "k_heads": cfg.k_heads, "heads": H, "missing_rows_filled_per_token": round(statistics.mean(
+            filled[1:]), 2), "us_per_token_kvfill": round(res["kvfill"], 2),
+            "us_per_token_without_fill": round(res["plain"], 2), "fill_launch_us": res["fill_launch_us"]}
 
 
 def cpu_baseline_b32(cfg, th, heads, sets, pos):

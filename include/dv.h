@@ -72,7 +72,10 @@ typedef enum dv_status {
   DV_ERR_ARG = 9          /* an invalid mode or flag value */
 } dv_status;
 
-typedef enum dv_dtype { DV_F32 = 0, DV_F16 = 1 } dv_dtype;
+/* DV_Q4: 4-bit weights (W4A16) in the dv_mlp_q4 layout, for dv_sparse_mlp_q4 only. */
+typedef enum dv_dtype { DV_F32 = 0, DV_F16 = 1, DV_Q4 = 2 } dv_dtype;
+/* sigma of Eq. (1) (Section 2.3 names ReLU and GeLU): dv_mlp.act, dv_mlp_q4.act. */
+enum { DV_ACT_RELU = 0, DV_ACT_GELU = 1 };
 
 /* Selection rule (Section 4.1; Algorithm 1 labels s >= t as positive). */
 enum { DV_SELECT_TOPK = 0, DV_SELECT_THRESHOLD = 1 };
@@ -106,7 +109,7 @@ typedef struct dv_mlp {
   int32_t d;          /* model width */
   int32_t n;          /* neurons N */
   int32_t wtype;      /* dv_dtype of W1T and W2T */
-  int32_t reserved;   /* must be 0 */
+  int32_t act;        /* DV_ACT_RELU (0, OPT) or DV_ACT_GELU (exact, x * Phi(x)) */
   const void *W1T;    /* [n][d]; row i = W^1_i */
   const float *b1;    /* [n] or NULL */
   const void *W2T;    /* [n][d]; row i = W^2_i */
@@ -203,6 +206,30 @@ size_t dv_sparse_mlp_workspace_bytes(const dv_mlp *m, int32_t B, int32_t n_idx, 
 dv_status dv_sparse_mlp(const dv_mlp *m, const float *x, int32_t B, const int32_t *idx,
                         int32_t n_idx, int32_t idx_per_seq, int32_t batch_mode, float *out,
                         void *ws, size_t ws_bytes, uint32_t flags, void *stream);
+
+/* ------------------------------------------------------ 4-bit sparse MLP (W4A16)
+ * dv_sparse_mlp_q4: dv_sparse_mlp for one token (B = 1) with 4-bit weights, the W4A16
+ * setting of Section 5.2 ("Compatibility with Quantization"): out = b2 + sum_{i in S}
+ * sigma(x . W^1_i + b1_i) W^2_i, where element j of a stored row is s_{j/32} (q_j - 8):
+ * 4-bit codes q_j, two per byte (even element in the low nibble), and one fp16 scale per
+ * block of 32 elements. Each selected row is 0.5625 d bytes (d / 2 of codes, d / 16 of
+ * scales) instead of 2 d in fp16. Arithmetic in fp32.
+ *   W1T, W2T  [n][d/2] uint8 device, 16-byte aligned rows (d a multiple of 32).
+ *   S1, S2    [n][d/32] fp16 device: row i's block scales.
+ *   act       DV_ACT_RELU or DV_ACT_GELU.
+ * idx, n_idx, out, ws, flags as for dv_sparse_mlp with B = 1. */
+typedef struct dv_mlp_q4 {
+  int32_t d, n;       /* model width (multiple of 32), neurons */
+  int32_t act;        /* DV_ACT_RELU or DV_ACT_GELU */
+  int32_t reserved;   /* must be 0 */
+  const void *W1T, *S1;
+  const float *b1;    /* [n] or NULL */
+  const void *W2T, *S2;
+  const float *b2;    /* [d] or NULL */
+} dv_mlp_q4;
+size_t dv_sparse_mlp_q4_workspace_bytes(const dv_mlp_q4 *m, int32_t n_idx);
+dv_status dv_sparse_mlp_q4(const dv_mlp_q4 *m, const float *x, const int32_t *idx, int32_t n_idx, float *out,
+                           void *ws, size_t ws_bytes, uint32_t flags, void *stream);
 
 /* ---------------------------------------------------------- sparse attention
  * dv_sparse_attn: out[b] = bo + sum_{i in S_A^b} H_i(x[b]) W^O_i (Eq. (2) with a

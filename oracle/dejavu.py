@@ -205,14 +205,11 @@ def dequant_q4(packed, scales, d: int) -> np.ndarray:
     packed: [rows, d/2] uint8; scales: [rows, d/32] (fp16 values). Returns [rows, d] fp64."""
     packed = np.asarray(packed, dtype=np.uint8)
     rows = packed.shape[0]
-    out = np.empty((rows, d), dtype=F64)
-    sc = _f64(scales)
-    for r in range(rows):
-        for j in range(d):
-            byte = int(packed[r, j // 2])
-            q = (byte & 15) if j % 2 == 0 else (byte >> 4)
-            out[r, j] = sc[r, j // Q4_BLOCK] * (q - 8)
-    return out
+    q = np.empty((rows, d), dtype=F64)
+    q[:, 0::2] = packed & 15          # even elements: low nibbles
+    q[:, 1::2] = packed >> 4          # odd elements: high nibbles
+    s = np.repeat(_f64(scales), Q4_BLOCK, axis=1)    # element j -> scale of block j // 32
+    return s * (q - 8.0)
 
 
 def dequant_q4_rows(packed, scales, d: int, rows) -> np.ndarray:

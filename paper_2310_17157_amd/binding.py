@@ -20,7 +20,8 @@ import torch
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdejavu_hip.so")
 
-DV_F32, DV_F16 = 0, 1
+DV_F32, DV_F16, DV_Q4 = 0, 1, 2
+DV_ACT_RELU, DV_ACT_GELU = 0, 1
 DV_SELECT_TOPK, DV_SELECT_THRESHOLD = 0, 1
 DV_LOOKAHEAD, DV_SEQUENTIAL = 0, 1
 DV_MLP_UNION, DV_MLP_MASKED = 0, 1
@@ -45,8 +46,14 @@ class CPredictor(ctypes.Structure):
 
 
 class CMlp(ctypes.Structure):
-    _fields_ = [("d", c_int32), ("n", c_int32), ("wtype", c_int32), ("reserved", c_int32),
+    _fields_ = [("d", c_int32), ("n", c_int32), ("wtype", c_int32), ("act", c_int32),
                 ("W1T", c_void_p), ("b1", c_void_p), ("W2T", c_void_p), ("b2", c_void_p)]
+
+
+class CMlpQ4(ctypes.Structure):
+    _fields_ = [("d", c_int32), ("n", c_int32), ("act", c_int32), ("reserved", c_int32),
+                ("W1T", c_void_p), ("S1", c_void_p), ("b1", c_void_p),
+                ("W2T", c_void_p), ("S2", c_void_p), ("b2", c_void_p)]
 
 
 class CAttn(ctypes.Structure):
@@ -79,6 +86,9 @@ _SIGS = {
     "dv_launch_label": (c_char_p, [c_int32]),
     "dv_abi_version": (c_int32, []),
     "dv_stream_read": (c_int32, [c_void_p, c_size_t, c_void_p, c_void_p]),
+    "dv_sparse_mlp_q4_workspace_bytes": (c_size_t, [POINTER(CMlpQ4), c_int32]),
+    "dv_sparse_mlp_q4": (c_int32, [POINTER(CMlpQ4), c_void_p, c_void_p, c_int32, c_void_p, c_void_p, c_size_t,
+                                   c_uint32, c_void_p]),
     "dv_sparse_attn_kvfill": (c_int32, [POINTER(CAttn), c_void_p, POINTER(CKV), c_void_p, c_void_p, c_void_p,
                                         c_int32, c_float, c_void_p, c_void_p, c_size_t, c_uint32, c_void_p]),
     "dv_sparse_decode_workspace_bytes": (c_size_t, [POINTER(CLayer), c_int32, c_int32, c_int32]),
@@ -228,10 +238,11 @@ class MLP:
     W2T: torch.Tensor
     b1: Optional[torch.Tensor] = None
     b2: Optional[torch.Tensor] = None
+    act: int = DV_ACT_RELU
 
     def c(self) -> CMlp:
         # checked and built once per set of tensors (calls are on the hot path)
-        key = tuple(id(t) for t in (self.W1T, self.W2T, self.b1, self.b2,))
+        key = tuple(id(t) for t in (self.W1T, self.W2T, self.b1, self.b2,)) + (self.act,)
         if getattr(self, "_ck", None) != key:
             _tensor("MLP.W1T", self.W1T, _STORE, 2, dev=False)
             n, d = self.W1T.shape
@@ -240,7 +251,38 @@ class MLP:
             _tensor("MLP.b1", self.b1, _F32, 1, (n,), optional=True, dev=False)
             _tensor("MLP.b2", self.b2, _F32, 1, (d,), optional=True, dev=False)
             _gpu(type(self).__name__, self.W1T, self.W2T, self.b1, self.b2)
-            self._cs = CMlp(d, n, _wtype(self.W1T), 0, _ptr(self.W1T), _ptr(self.b1), _ptr(self.W2T), _ptr(self.b2))
+            self._cs = CMlp(d, n, _wtype(self.W1T), int(self.act), _ptr(self.W1T), _ptr(self.b1), _ptr(self.W2T),
+                            _ptr(self.b2))
+            self._ck = key
+        return self._cs
+
+
+@dataclass
+class MLPQ4:
+    """4-bit MLP weights (W4A16): W1T, W2T [n][d/2] uint8 codes (even element in the low
+    nibble), S1, S2 [n][d/32] fp16 block scales; element = scale * (code - 8)."""
+    W1T: torch.Tensor
+    S1: torch.Tensor
+    W2T: torch.Tensor
+    S2: torch.Tensor
+    b1: Optional[torch.Tensor] = None
+    b2: Optional[torch.Tensor] = None
+    act: int = DV_ACT_RELU
+
+    def c(self) -> CMlpQ4:
+        key = tuple(id(t) for t in (self.W1T, self.S1, self.W2T, self.S2, self.b1, self.b2)) + (self.act,)
+        if getattr(self, "_ck", None) != key:
+            _tensor("MLPQ4.W1T", self.W1T, (torch.uint8,), 2, dev=False)
+            n, h = self.W1T.shape
+            d = 2 * h
+            _tensor("MLPQ4.W2T", self.W2T, (torch.uint8,), 2, (n, h), dev=False)
+            _tensor("MLPQ4.S1", self.S1, (torch.float16,), 2, (n, d // 32), dev=False)
+            _tensor("MLPQ4.S2", self.S2, (torch.float16,), 2, (n, d // 32), dev=False)
+            _tensor("MLPQ4.b1", self.b1, _F32, 1, (n,), optional=True, dev=False)
+            _tensor("MLPQ4.b2", self.b2, _F32, 1, (d,), optional=True, dev=False)
+            _gpu("MLPQ4", self.W1T, self.S1, self.W2T, self.S2, self.b1, self.b2)
+            self._cs = CMlpQ4(d, n, int(self.act), 0, _ptr(self.W1T), _ptr(self.S1), _ptr(self.b1), _ptr(self.W2T),
+                              _ptr(self.S2), _ptr(self.b2))
             self._ck = key
         return self._cs
 
@@ -404,6 +446,25 @@ def dv_sparse_attn(attn: Attn, x, kv: KVCache, heads, scale, out=None, ws=None, 
     st = lib.dv_sparse_attn(ctypes.byref(ca), _ptr(x), B, ctypes.byref(ck), _ptr(heads), n_heads, scale,
                             _ptr(out), *_wsarg(ws), flags, _stream(stream))
     _check("dv_sparse_attn", st)
+    return out
+
+
+def dv_sparse_mlp_q4(mlp: MLPQ4, x, idx, out=None, ws=None, flags=0, stream=None):
+    """out = MLP_S(x) with 4-bit weights (Section 5.2, W4A16), one token."""
+    lib = load()
+    cm = mlp.c()
+    _tensor("x", x, _F32, 2, (1, cm.d), dev=False)
+    _tensor("idx", idx, _I32, dev=False)
+    n_idx = idx.shape[-1]
+    _tensor("out", out, _F32, 2, (1, cm.d), optional=True, dev=False)
+    _gpu("arguments", x, idx, out)
+    if out is None:
+        out = torch.empty((1, cm.d), dtype=torch.float32, device=x.device)
+    if ws is None:
+        ws = _workspace(lib.dv_sparse_mlp_q4_workspace_bytes(ctypes.byref(cm), n_idx), x.device)
+    st = lib.dv_sparse_mlp_q4(ctypes.byref(cm), _ptr(x), _ptr(idx), n_idx, _ptr(out), *_wsarg(ws), flags,
+                              _stream(stream))
+    _check("dv_sparse_mlp_q4", st)
     return out
 
 

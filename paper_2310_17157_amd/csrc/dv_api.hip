@@ -126,7 +126,7 @@ bool dv::ws_ok(void* ws) { return ws != nullptr && (reinterpret_cast<uintptr_t>(
 dv_status dv::check_mlp(const dv_mlp* m) {
   if (m == nullptr || m->W1T == nullptr || m->W2T == nullptr) return DV_ERR_NULL;
   if (!dtype_ok(m->wtype)) return DV_ERR_DTYPE;
-  if (m->reserved != 0) return DV_ERR_ARG;
+  if (m->act != DV_ACT_RELU && m->act != DV_ACT_GELU) return DV_ERR_ARG;
   if (m->d <= 0 || m->n <= 0) return DV_ERR_SHAPE;
   if (m->d % chunk_elems(m->wtype) != 0) return DV_ERR_ALIGN;
   if (!aligned16(m->W1T) || !aligned16(m->W2T)) return DV_ERR_ALIGN;
@@ -239,6 +239,7 @@ extern "C" dv_status dv_sparse_mlp(const dv_mlp* m, const float* x, int32_t B, c
   Fc1Args f{};
   f.d = m->d; f.k = n_idx; f.n = m->n; f.x = x; f.g = nullptr; f.be = nullptr; f.eps = 0.f;
   f.W1T = m->W1T; f.b1 = m->b1; f.set = idx; f.h = o.h; f.clear = o.axc; f.clear_n = kAxpyMaxSpans;
+  f.act = m->act;
   DV_LAUNCH("fc1", hs, launch_fc1(m->wtype, f, hs));
   AxpyArgs ax{};
   ax.d = m->d; ax.nrows = n_idx; ax.M = m->W2T; ax.m_rows = m->n; ax.set = idx; ax.dh = 0;
@@ -342,6 +343,61 @@ extern "C" dv_status dv_sparse_attn(const dv_attn* a, const float* x, int32_t B,
   ax.dh = a->dh; ax.coef = nullptr; ax.part = o.part; ax.n_split = attn_nsplit(a, kv, n_heads);
   ax.resid = nullptr; ax.bias = a->bo; ax.out = out; ax.out2 = nullptr; ax.partial = o.axp; ax.cnt = o.axc;
   return enqueue_axpy("oproj", a->wtype, ax, hs);
+}
+
+// ------------------------------------------------------------ 4-bit sparse MLP
+static dv_status check_mlp_q4(const dv_mlp_q4* m) {
+  if (m == nullptr || m->W1T == nullptr || m->W2T == nullptr || m->S1 == nullptr || m->S2 == nullptr)
+    return DV_ERR_NULL;
+  if (m->act != DV_ACT_RELU && m->act != DV_ACT_GELU) return DV_ERR_ARG;
+  if (m->reserved != 0) return DV_ERR_ARG;
+  if (m->d <= 0 || m->n <= 0) return DV_ERR_SHAPE;
+  if (m->d % 32 != 0 || !aligned16(m->W1T) || !aligned16(m->W2T)) return DV_ERR_ALIGN;
+  if ((reinterpret_cast<uintptr_t>(m->S1) & 1u) || (reinterpret_cast<uintptr_t>(m->S2) & 1u)) return DV_ERR_ALIGN;
+  if (m->d > kMaxWidth) return DV_ERR_UNSUPPORTED;
+  return DV_OK;
+}
+
+extern "C" size_t dv_sparse_mlp_q4_workspace_bytes(const dv_mlp_q4* m, int32_t n_idx) {
+  if (m == nullptr || m->d <= 0 || m->n <= 0 || n_idx < 0) return 0;
+  Workspace w(nullptr);
+  w.take<float>((size_t)n_idx * sizeof(float));
+  w.take<float>(axpy_partial_bytes(m->d));
+  w.take<uint32_t>(kAxpyMaxSpans * sizeof(uint32_t));
+  w.take<int32_t>(sizeof(int32_t));
+  return w.off;
+}
+
+extern "C" dv_status dv_sparse_mlp_q4(const dv_mlp_q4* m, const float* x, const int32_t* idx, int32_t n_idx,
+                                      float* out, void* ws, size_t ws_bytes, uint32_t flags, void* stream) {
+  trace_reset();
+  dv_status st = check_mlp_q4(m);
+  if (st != DV_OK) return st;
+  if (x == nullptr || out == nullptr || (idx == nullptr && n_idx > 0)) return DV_ERR_NULL;
+  if (n_idx < 0 || n_idx > m->n) return DV_ERR_SHAPE;
+  if (!aligned16(x) || !aligned16(out)) return DV_ERR_ALIGN;
+  if ((m->b1 != nullptr && !aligned16(m->b1)) || (m->b2 != nullptr && !aligned16(m->b2))) return DV_ERR_ALIGN;
+  if (flags & ~(uint32_t)(DV_DETERMINISTIC | DV_VALIDATE)) return DV_ERR_ARG;
+  if (!ws_ok(ws)) return DV_ERR_WORKSPACE;
+  if (dv_sparse_mlp_q4_workspace_bytes(m, n_idx) > ws_bytes) return DV_ERR_WORKSPACE;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  Workspace w(ws);
+  float* h = w.take<float>((size_t)n_idx * sizeof(float));
+  float* axp = w.take<float>(axpy_partial_bytes(m->d));
+  uint32_t* axc = w.take<uint32_t>(kAxpyMaxSpans * sizeof(uint32_t));
+  int32_t* flag = w.take<int32_t>(sizeof(int32_t));
+  if (flags & DV_VALIDATE) {
+    st = validate_sets(idx, 1, n_idx, m->n, flag, hs);
+    if (st != DV_OK) return st;
+  }
+  Fc1Args f{};
+  f.d = m->d; f.k = n_idx; f.n = m->n; f.x = x; f.W1T = m->W1T; f.b1 = m->b1; f.set = idx;
+  f.s1 = static_cast<const _Float16*>(m->S1); f.act = m->act; f.h = h; f.clear = axc; f.clear_n = kAxpyMaxSpans;
+  DV_LAUNCH("fc1", hs, launch_fc1(DV_Q4, f, hs));
+  AxpyArgs ax{};
+  ax.d = m->d; ax.nrows = n_idx; ax.M = m->W2T; ax.m_rows = m->n; ax.set = idx; ax.dh = 0; ax.coef = h;
+  ax.scales = static_cast<const _Float16*>(m->S2); ax.bias = m->b2; ax.out = out; ax.partial = axp; ax.cnt = axc;
+  return enqueue_axpy("fc2", DV_Q4, ax, hs);
 }
 
 // ------------------------------------------- sparse attention, missing keys and values
@@ -560,7 +616,7 @@ extern "C" dv_status dv_sparse_block(const dv_attn* a, const dv_mlp* m, const dv
   // 6. fc1 + ReLU on LN2(y~).
   Fc1Args f{};
   f.d = m->d; f.k = k_mlp; f.n = m->n; f.x = o.ytilde; f.g = g2; f.be = be2; f.eps = eps;
-  f.W1T = m->W1T; f.b1 = m->b1; f.set = o.idx; f.h = o.h;
+  f.W1T = m->W1T; f.b1 = m->b1; f.set = o.idx; f.h = o.h; f.act = m->act;
   f.clear = o.axc + kAxpyMaxSpans; f.clear_n = kAxpyMaxSpans;
   DV_LAUNCH("fc1", hs, launch_fc1(m->wtype, f, hs));
   // 7. fc2 + residual: y^ = y~ + MLP(LN2(y~)).

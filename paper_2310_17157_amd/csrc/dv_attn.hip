@@ -344,13 +344,15 @@ hipError_t launch_attn(int kvtype, const AttnArgs& a, int B, hipStream_t st) {
 
 // ------------------------------------------------------------ missing keys and values
 // One workgroup per (selected head, block of kFillRows rows of [W^K_h; W^V_h]). It lists
-// the head's missing positions (valid == 0 below pos), then streams each of its rows once
-// per group of MT positions: a wavefront holds 64 chunks of the row and dots them with the
-// matching elements of the MT kept inputs (read through L2: every workgroup of the
-// head reads the same few rows of Y). Nothing is read when nothing is missing.
+// the head's missing positions (valid == 0 below pos); each wavefront then takes RPW of
+// the rows at once and, for groups of MT missing positions, walks the rows in 16-byte
+// chunks: the RPW weight chunks and the MT matching slices of the kept inputs (L2 hits:
+// every workgroup of the head reads the same few rows of Y) are loaded together, two
+// steps in flight, with indices clamped so that no load is predicated. Nothing is read
+// when nothing is missing.
 constexpr int kFillRows = 16;
 
-template <typename T, typename KT, int MT>
+template <typename T, typename KT, int RPW, int MT>
 __global__ void __launch_bounds__(256) k_kv_fill(KvFillArgs a) {
   constexpr int E = Chunk<T>::E;
   extern __shared__ int flist[];
@@ -369,40 +371,72 @@ __global__ void __launch_bounds__(256) k_kv_fill(KvFillArgs a) {
   __syncthreads();
   const int m = fcnt;
   if (m == 0) return;
-  const int nch = a.d / E;
-  const int r0 = rb * kFillRows, r1 = min(2 * a.dh, r0 + kFillRows);
+  const int nch = a.d / E, nit = (nch + 63) / 64;
+  // this wavefront's rows (clamped into the block; duplicates are not written)
+  const int r0 = rb * kFillRows + wave * RPW, rend = min(2 * a.dh, (rb + 1) * kFillRows);
+  const T* W[RPW];
+#pragma unroll
+  for (int r = 0; r < RPW; ++r) {
+    const int rr = min(r0 + r, rend - 1);
+    const bool isv = rr >= a.dh;
+    W[r] = static_cast<const T*>(isv ? a.Wv : a.Wk) + ((size_t)head * a.dh + (isv ? rr - a.dh : rr)) * a.d;
+  }
   for (int t0 = 0; t0 < m; t0 += MT) {
-    for (int r = r0 + wave; r < r1; r += 4) {
-      const bool isv = r >= a.dh;
-      const int tr = isv ? r - a.dh : r;
-      const T* W = static_cast<const T*>(isv ? a.Wv : a.Wk) + ((size_t)head * a.dh + tr) * a.d;
-      float acc[MT];
+    const float* Yp[MT];
 #pragma unroll
-      for (int u = 0; u < MT; ++u) acc[u] = 0.f;
-      for (int c = lane; c < nch; c += 64) {
-        float w[E];
-        unpack<T>(ld_stream(W + (size_t)c * E), w);
+    for (int u = 0; u < MT; ++u) Yp[u] = a.Y + (size_t)flist[min(t0 + u, m - 1)] * a.d;
+    float acc[RPW][MT];
 #pragma unroll
-        for (int u = 0; u < MT; ++u) {
-          if (t0 + u < m) {
-            const float* y = a.Y + (size_t)flist[t0 + u] * a.d + (size_t)c * E;
+    for (int r = 0; r < RPW; ++r)
 #pragma unroll
-            for (int e = 0; e < E; e += 4) {
-              const f32x4 yv = *reinterpret_cast<const f32x4*>(y + e);
-              acc[u] = fmaf(w[e], yv[0], acc[u]);
-              acc[u] = fmaf(w[e + 1], yv[1], acc[u]);
-              acc[u] = fmaf(w[e + 2], yv[2], acc[u]);
-              acc[u] = fmaf(w[e + 3], yv[3], acc[u]);
-            }
-          }
-        }
+      for (int u = 0; u < MT; ++u) acc[r][u] = 0.f;
+    struct Step {
+      u32x4 w[RPW];
+      f32x4 y[MT][E / 4];
+    };
+    auto load = [&](Step& st, int it) {
+      const int c = min(it * 64 + lane, nch - 1);
+#pragma unroll
+      for (int r = 0; r < RPW; ++r) st.w[r] = ld_stream(W[r] + (size_t)c * E);
+#pragma unroll
+      for (int u = 0; u < MT; ++u)
+#pragma unroll
+        for (int q = 0; q < E / 4; ++q) st.y[u][q] = *reinterpret_cast<const f32x4*>(Yp[u] + (size_t)c * E + 4 * q);
+    };
+    auto use = [&](const Step& st, int it) {
+      if (it * 64 + lane >= nch) return;
+#pragma unroll
+      for (int r = 0; r < RPW; ++r) {
+        float wv[E];
+        unpack<T>(st.w[r], wv);
+#pragma unroll
+        for (int u = 0; u < MT; ++u)
+#pragma unroll
+          for (int e = 0; e < E; ++e) acc[r][u] = fmaf(wv[e], st.y[u][e >> 2][e & 3], acc[r][u]);
       }
+    };
+    // two steps in flight: the next step's loads go out before this step is used
+    Step sa, sb;
+    load(sa, 0);
+    for (int it = 0; it < nit;) {
+      load(sb, min(it + 1, nit - 1));
+      use(sa, it);
+      if (++it >= nit) break;
+      load(sa, min(it + 1, nit - 1));
+      use(sb, it);
+      ++it;
+    }
+#pragma unroll
+    for (int r = 0; r < RPW; ++r) {
+      const int rr = r0 + r;
+      const bool isv = rr >= a.dh;
+      const int tr = isv ? rr - a.dh : rr;
       const float* bias = isv ? a.bv : a.bk;
-      const float bb = bias ? bias[(size_t)head * a.dh + tr] : 0.f;
+      const float bb = (bias != nullptr && rr < rend) ? bias[(size_t)head * a.dh + tr] : 0.f;
 #pragma unroll
       for (int u = 0; u < MT; ++u) {
-        const float v = wave_sum(acc[u]);
-        if (lane == 0 && t0 + u < m) {
+        const float v = wave_sum(acc[r][u]);
+        if (lane == 0 && rr < rend && t0 + u < m) {
           KT* C = static_cast<KT*>(isv ? a.V : a.K);
           C[((size_t)head * a.cap + flist[t0 + u]) * a.dh + tr] = (KT)(v + bb);
         }
@@ -415,9 +449,10 @@ template <typename T, typename KT>
 static hipError_t launch_kv_fill_t(const KvFillArgs& a, hipStream_t st) {
   const int nrb = (2 * a.dh + kFillRows - 1) / kFillRows;
   const size_t lds = (size_t)max(a.pos, 1) * sizeof(int);
-  const hipError_t e = ensure_dyn_lds(reinterpret_cast<const void*>(k_kv_fill<T, KT, 8>), lds);
+  constexpr int RPW = kFillRows / 4, MT = 4;
+  const hipError_t e = ensure_dyn_lds(reinterpret_cast<const void*>(k_kv_fill<T, KT, RPW, MT>), lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((k_kv_fill<T, KT, 8>), dim3(max(1, a.n_heads) * nrb), dim3(256), lds, st, a);
+  hipLaunchKernelGGL((k_kv_fill<T, KT, RPW, MT>), dim3(max(1, a.n_heads) * nrb), dim3(256), lds, st, a);
   return hipGetLastError();
 }
 

@@ -52,9 +52,13 @@ __global__ void __launch_bounds__(NW * 64) k_axpy(AxpyArgs a) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int S = gridDim.y, sp = blockIdx.y;
   const int r0 = (int)((long)sp * a.nrows / S), r1 = (int)((long)(sp + 1) * a.nrows / S);
+  constexpr bool Q4 = kIsQ4<T>;
   const int nch = a.d / E;
-  const char* Mb = static_cast<const char*>(a.M) + (size_t)min((int)blockIdx.x * 64 + lane, nch - 1) * 16;
-  const size_t rowb = (size_t)a.d * sizeof(T);
+  const int lc = min((int)blockIdx.x * 64 + lane, nch - 1);          // this lane's chunk of a row
+  const char* Mb = static_cast<const char*>(a.M) + (size_t)lc * 16;
+  const size_t rowb = Q4 ? (size_t)a.d / 2 : (size_t)a.d * sizeof(T);
+  const _Float16* Sb = Q4 ? a.scales + lc : nullptr;                  // 4-bit rows: chunk scales
+  const int srow = a.d / 32;
   const int ns = a.n_split;
   const int stride = a.dh + 2;
 
@@ -78,25 +82,31 @@ __global__ void __launch_bounds__(NW * 64) k_axpy(AxpyArgs a) {
     // this wavefront's rows: wave + NW * i, i < nwr; loads past the end are clamped
     // to the last row (and weighted by zero), so every batch issues U loads
     const int nwr = nb > wave ? (nb - wave + NW - 1) / NW : 0;
-    auto load = [&](u32x4 (&w)[U], int i0) {
+    struct Batch {
+      u32x4 w[U];
+      _Float16 s[Q4 ? U : 1];
+    };
+    auto load = [&](Batch& b, int i0) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int i = min(wave + NW * (i0 + u), nb - 1);
-        w[u] = ld_stream(Mb + (size_t)ri[i] * rowb);
+        b.w[u] = ld_stream(Mb + (size_t)ri[i] * rowb);
+        if constexpr (Q4) b.s[u] = Sb[(size_t)ri[i] * srow];
       }
     };
-    auto consume = [&](const u32x4 (&w)[U], int i0) {
+    auto consume = [&](const Batch& b, int i0) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int i = i0 + u;
-        const float f = i < nwr ? cf[wave + NW * i] : 0.f;
+        float f = i < nwr ? cf[wave + NW * i] : 0.f;
+        if constexpr (Q4) f *= (float)b.s[u];
         float v[E];
-        unpack<T>(w[u], v);
+        unpack<T>(b.w[u], v);
 #pragma unroll
         for (int e = 0; e < E; ++e) acc[e] = fmaf(f, v[e], acc[e]);
       }
     };
-    u32x4 wa[U], wb[U];
+    Batch wa, wb;
     if (nwr > 0) load(wa, 0);
     // ---- coefficients, while those loads are in flight
     if (!HEADS) {
@@ -224,23 +234,29 @@ static int axpy_row_splits(int d, int E, int nrows) {
   return max(1, min(S, kAxpyMaxRowSplit));
 }
 
-template <typename T, bool HEADS>
+template <typename T, bool HEADS, int NW = kAxNW, int U = kAxU>
 static hipError_t launch_axpy_t(AxpyArgs a, hipStream_t st) {
   constexpr int E = Chunk<T>::E;
   const int spans = (a.d / E + 63) / 64;
   const int S = a.partial != nullptr ? axpy_row_splits(a.d, E, a.nrows) : 1;
   if (spans > kAxpyMaxSpans) a.cnt = nullptr;   // no counter per span: the split sum is a launch
+  // 4-bit rows: a span is 2048 columns, too wide for one workgroup to add all its splits
+  // in its tail (each thread would wait for 8 rounds of loads); the sum is a launch
+  if (kIsQ4<T>) a.cnt = nullptr;
   // LDS: (coefficient, row index) pairs of a batch of the split's rows and the
   // wavefront sums.
   const int rpb = min(kAxRowsLds, max(1, (a.nrows + S - 1) / S));
   a.rows_per_batch = rpb;
-  const size_t lds = (size_t)rpb * 8 + (size_t)kAxNW * 64 * E * 4;
-  hipLaunchKernelGGL((k_axpy<T, kAxNW, kAxU, HEADS>), dim3(spans, S), dim3(kAxNW * 64), lds, st, a);
+  const size_t lds = (size_t)rpb * 8 + (size_t)NW * 64 * E * 4;
+  hipLaunchKernelGGL((k_axpy<T, NW, U, HEADS>), dim3(spans, S), dim3(NW * 64), lds, st, a);
   if (S > 1 && a.cnt == nullptr) hipLaunchKernelGGL(k_axpy_sum, dim3((a.d / 4 + 255) / 256), dim3(256), 0, st, a, S);
   return hipGetLastError();
 }
 
 hipError_t launch_axpy(int wtype, const AxpyArgs& a, hipStream_t st) {
+  // 4-bit rows: 32 columns per lane, so four wavefronts (their 2048-column sums fit in
+  // 32 KB of LDS) with batches of 4 rows
+  if (wtype == DV_Q4) return a.dh > 0 ? hipErrorInvalidValue : launch_axpy_t<q4_t, false, 4, 4>(a, st);
   if (a.dh > 0)
     return wtype == DV_F16 ? launch_axpy_t<_Float16, true>(a, st) : launch_axpy_t<float, true>(a, st);
   return wtype == DV_F16 ? launch_axpy_t<_Float16, false>(a, st) : launch_axpy_t<float, false>(a, st);

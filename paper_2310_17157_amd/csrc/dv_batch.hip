@@ -725,7 +725,7 @@ __global__ void __launch_bounds__(16 * NB) k_fc1_finish(Fc1FinishArgs a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         float x = v[i] + bias;
-        x = x > 0.f ? x : 0.f;
+        x = act_apply(x, a.act);
         if (b0 + i >= a.B || !((mk >> (b0 + i)) & 1u)) x = 0.f;
         v[i] = x;
       }

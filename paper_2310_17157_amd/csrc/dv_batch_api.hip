@@ -75,6 +75,7 @@ static dv_status bmlp_run(const dv_mlp* m, const BMlp& o, int B, const int32_t* 
   Fc1FinishArgs f{};
   f.P = o.P; f.S = o.S; f.nrows_pad = o.nrows_pad; f.list = list; f.list_count = list_count;
   f.list_max = list_max; f.list_range = m->n; f.b1 = m->b1; f.mask = (per_seq && masked) ? o.mask : nullptr; f.B = B;
+  f.act = m->act;
   f.C = o.C; f.ldc = o.ldc;
   DV_LAUNCH("fc1_finish", hs, launch_fc1_finish(NB, f, hs));
   McolsArgs c{};

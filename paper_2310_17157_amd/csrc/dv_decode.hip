@@ -141,7 +141,7 @@ dv_status enqueue_layer(const dv_layer& L, const dv_layer* next, const float* y,
   DV_LAUNCH("oproj", st, launch_axpy(a.wtype, ax, st));
   Fc1Args f{};
   f.d = m.d; f.k = km; f.n = m.n; f.x = o.ytilde; f.g = L.ln.g2; f.be = L.ln.be2; f.eps = L.ln.eps;
-  f.W1T = m.W1T; f.b1 = m.b1; f.set = o.idx; f.h = o.h;
+  f.W1T = m.W1T; f.b1 = m.b1; f.set = o.idx; f.h = o.h; f.act = m.act;
   f.clear = o.axc + kAxpyMaxSpans; f.clear_n = kAxpyMaxSpans;
   DV_LAUNCH("fc1", st, launch_fc1(m.wtype, f, st));
   AxpyArgs ay{};

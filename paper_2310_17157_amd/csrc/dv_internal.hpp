@@ -18,10 +18,25 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
+// 4-bit weights (W4A16): a 16-byte chunk holds 32 elements, two per byte (low nibble
+// first), element = scale * (code - 8), one fp16 scale per chunk kept in a separate
+// array (scale of chunk c of a row: scales[row][c]).
+struct q4_t {};
+
 // Elements per 16-byte chunk for a storage type.
 template <typename T> struct Chunk;
 template <> struct Chunk<float> { static constexpr int E = 4; };
 template <> struct Chunk<_Float16> { static constexpr int E = 8; };
+template <> struct Chunk<q4_t> { static constexpr int E = 32; };
+template <typename T> inline constexpr bool kIsQ4 = false;
+template <> inline constexpr bool kIsQ4<q4_t> = true;
+
+// Activation of the MLP (sigma of Eq. (1)).
+enum { kActRelu = 0, kActGelu = 1 };
+__device__ __forceinline__ float act_apply(float v, int act) {
+  if (act == kActGelu) return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f));
+  return v > 0.f ? v : 0.f;
+}
 
 // ---------------------------------------------------------------- loads
 // Weights are streamed once per call: non-temporal 16-byte loads.
@@ -47,6 +62,16 @@ __device__ __forceinline__ void unpack<_Float16>(u32x4 w, float* v) {
   for (int i = 0; i < 8; ++i) v[i] = (float)h[i];
 }
 
+// A 4-bit chunk as 32 floats code - 8 (the caller applies the chunk's scale).
+template <>
+__device__ __forceinline__ void unpack<q4_t>(u32x4 w, float* v) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[8 * i + k] = (float)((int)((w[i] >> (4 * k)) & 15u) - 8);
+  }
+}
+
 // Store E floats as one chunk of storage type T (round to nearest even for fp16).
 template <typename T>
 __device__ __forceinline__ void store_elem(T* p, float v) { *p = (T)v; }
@@ -64,6 +89,11 @@ __device__ __forceinline__ int xs_index<float>(int e, int) { return e; }
 template <>
 __device__ __forceinline__ int xs_index<_Float16>(int e, int d) {
   return ((e >> 2) & 1) * (d >> 1) + ((e >> 3) << 2) + (e & 3);
+}
+// 4-bit rows: eight planes (elements 4p..4p+3 of every 32-element chunk in plane p).
+template <>
+__device__ __forceinline__ int xs_index<q4_t>(int e, int d) {
+  return ((e >> 2) & 7) * (d >> 3) + ((e >> 5) << 2) + (e & 3);
 }
 
 template <typename T>
@@ -92,6 +122,22 @@ __device__ __forceinline__ float dot_chunk<_Float16>(u32x4 w, const float* xs, i
   acc = fmaf((float)h[6], xb[2], acc);
   acc = fmaf((float)h[7], xb[3], acc);
   return acc;
+}
+
+// Dot of a 4-bit chunk (scale sc) with its 32 staged inputs: sc * sum (code - 8) x.
+__device__ __forceinline__ float dot_chunk_q4(u32x4 w, float sc, const float* xs, int d, int c, float acc) {
+  float t = 0.f;
+  const int plane = d >> 3;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const f32x4 xa = *reinterpret_cast<const f32x4*>(xs + (2 * i) * plane + 4 * c);
+    const f32x4 xb = *reinterpret_cast<const f32x4*>(xs + (2 * i + 1) * plane + 4 * c);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) t = fmaf((float)((int)((w[i] >> (4 * k)) & 15u) - 8), xa[k], t);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) t = fmaf((float)((int)((w[i] >> (4 * k + 16)) & 15u) - 8), xb[k], t);
+  }
+  return fmaf(sc, t, acc);
 }
 
 // ------------------------------------------------------------ reductions
@@ -363,6 +409,7 @@ struct AxpyArgs {
   const int32_t* set; int dh;       // dh = 0: neuron rows
   // Coefficients: coef[row] (neurons), or from attention partials (heads).
   const float* coef;
+  const _Float16* scales;           // 4-bit rows only: [m_rows][d / 32] chunk scales
   const float* part; int n_split;   // attention partials when coef == NULL
   const float* resid; const float* bias;   // optional, [d]
   float* out;                        // [d]
@@ -399,6 +446,8 @@ struct Fc1Args {
   int d, k, n;                      // width, selected neurons, neurons in W1T
   const float* x; const float* g; const float* be; float eps;    // LN (g NULL: none)
   const void* W1T; const float* b1; const int32_t* set;
+  const _Float16* s1;               // 4-bit rows only: [n][d / 32] chunk scales
+  int act;                          // kActRelu / kActGelu
   float* h;
   uint32_t* clear; int clear_n;     // counters of a later row-axpy to zero (optional)
 };
@@ -460,7 +509,7 @@ hipError_t launch_mcols(int NB, const McolsArgs& a, hipStream_t st);
 struct Fc1FinishArgs {
   const float* P; int S, nrows_pad;
   const int32_t* list; const int32_t* list_count; int list_max; int list_range;
-  const float* b1; const uint32_t* mask; int B;
+  const float* b1; const uint32_t* mask; int B; int act;
   _Float16* C; int ldc;
 };
 hipError_t launch_fc1_finish(int NB, const Fc1FinishArgs& a, hipStream_t st);

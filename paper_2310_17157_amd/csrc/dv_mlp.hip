@@ -18,8 +18,13 @@ __global__ void __launch_bounds__(NW * 64) k_fc1(Fc1Args a) {
   float* part = red + NW;
   clear_counters(a.clear, a.clear_n);
   auto row_ptr = [&](int s) {
-    return static_cast<const T*>(a.W1T) + (size_t)min(max(a.set[s], 0), a.n - 1) * a.d;
+    const size_t row = (size_t)min(max(a.set[s], 0), a.n - 1);
+    if constexpr (kIsQ4<T>)
+      return static_cast<const char*>(a.W1T) + row * (a.d / 2);
+    else
+      return static_cast<const T*>(a.W1T) + row * a.d;
   };
+  auto scale_ptr = [&](int s) { return a.s1 + (size_t)min(max(a.set[s], 0), a.n - 1) * (a.d / 32); };
   // The epilogue's bias reads: the neuron index of row r0 + tid is read first of all
   // loads (it is not waited for until the end), its bias once the stream is done.
   const int r0 = rowdot_split(blockIdx.x, a.k, gridDim.x), r1 = rowdot_split(blockIdx.x + 1, a.k, gridDim.x);
@@ -37,10 +42,10 @@ __global__ void __launch_bounds__(NW * 64) k_fc1(Fc1Args a) {
     } else if (a.b1) {
       v += a.b1[min(max(a.set[s], 0), a.n - 1)];
     }
-    a.h[s] = v > 0.f ? v : 0.f;
+    a.h[s] = act_apply(v, a.act);
   };
   rowdot_flat<T, NW, U, KX, LN>(row_ptr, epi, a.k, a.d, a.x, a.g, a.be, a.eps, xs, red, part, nullptr, blockIdx.x,
-                                   gridDim.x, tail);
+                                gridDim.x, tail, scale_ptr);
 }
 
 template <typename T, int KX>
@@ -73,6 +78,7 @@ static hipError_t launch_fc1_k(const Fc1Args& a, hipStream_t st) {
 }
 
 hipError_t launch_fc1(int wtype, const Fc1Args& a, hipStream_t st) {
+  if (wtype == DV_Q4) return launch_fc1_k<q4_t>(a, st);
   return wtype == DV_F16 ? launch_fc1_k<_Float16>(a, st) : launch_fc1_k<float>(a, st);
 }
 

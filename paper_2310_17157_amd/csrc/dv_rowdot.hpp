@@ -31,6 +31,10 @@ constexpr int kRowdotPre = 4;
 struct NoTail {
   __device__ void operator()() const {}
 };
+// Chunk-scale rows of 4-bit weights (unused for fp16 / fp32 rows).
+struct NoScales {
+  __device__ const _Float16* operator()(int) const { return nullptr; }
+};
 
 // i * n / G rounded down: the boundary of part i of n rows split G ways (in 32 bits
 // where the product fits, avoiding the long 64-bit division sequence).
@@ -38,10 +42,14 @@ __device__ __forceinline__ int rowdot_split(int i, int n, int G) {
   if (n < (1 << 23) && i <= 256) return (int)((unsigned)(i * n) / (unsigned)G);
   return (int)((long)i * n / G);
 }
-template <typename T, int NW, int U, int KX, bool LN, class RowPtr, class Epi, class Tail = NoTail>
+// For 4-bit rows (T = q4_t) scale_ptr(row) gives the row's chunk scales; each weight
+// load is paired with the load of its chunk's scale.
+template <typename T, int NW, int U, int KX, bool LN, class RowPtr, class Epi, class Tail = NoTail,
+          class ScalePtr = NoScales>
 __device__ __forceinline__ void rowdot_flat(RowPtr row_ptr, Epi epi, int nrows, int d, const float* x,
                                             const float* g, const float* be, float eps, float* xs, float* red,
-                                            float* part, float* xhat_out, int wg, int G, Tail tail = Tail()) {
+                                            float* part, float* xhat_out, int wg, int G, Tail tail = Tail(),
+                                            ScalePtr scale_ptr = ScalePtr()) {
   constexpr int NT = NW * 64;
   constexpr int E = Chunk<T>::E;
   // the input's reads go out first of all, ahead of the partition arithmetic
@@ -69,14 +77,22 @@ __device__ __forceinline__ void rowdot_flat(RowPtr row_ptr, Epi epi, int nrows, 
   // stream enters a new row, not per load.
   int lrow = -1;
   const char* lptr = nullptr;
+  const _Float16* sptr = nullptr;   // 4-bit rows: the row's chunk scales
+  constexpr bool Q4 = kIsQ4<T>;
+  struct Batch {
+    u32x4 w[U];
+    _Float16 s[Q4 ? U : 1];
+  };
+  auto set_row = [&](int rr) {
+    lrow = rr;
+    lptr = any ? reinterpret_cast<const char*>(row_ptr(r0 + rr)) : reinterpret_cast<const char*>(x);
+    if constexpr (Q4) sptr = any ? scale_ptr(r0 + rr) : reinterpret_cast<const _Float16*>(x);
+  };
   // loads u in [u0, u1) of the batch of U slots starting at sb (u0, u1 compile-time)
-  auto load_part = [&](u32x4 (&w)[U], int sb, int u0, int u1) {
+  auto load_part = [&](Batch& b, int sb, int u0, int u1) {
     const int sc0 = max(min(sb + u0, shi), 0);
     int rr = sc0 / ipr, j = sc0 - rr * ipr;
-    if (rr != lrow) {
-      lrow = rr;
-      lptr = any ? reinterpret_cast<const char*>(row_ptr(r0 + rr)) : reinterpret_cast<const char*>(x);
-    }
+    if (rr != lrow) set_row(rr);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       if (u < u0 || u >= u1) continue;
@@ -84,15 +100,15 @@ __device__ __forceinline__ void rowdot_flat(RowPtr row_ptr, Epi epi, int nrows, 
         if (++j == ipr) {
           j = 0;
           ++rr;
-          lrow = rr;
-          lptr = reinterpret_cast<const char*>(row_ptr(r0 + rr));
+          set_row(rr);
         }
       }
       const int c = min(j * 64 + lane, nch - 1);
-      w[u] = ld_stream(lptr + (size_t)c * 16);
+      b.w[u] = ld_stream(lptr + (size_t)c * 16);
+      if constexpr (Q4) b.s[u] = sptr[c];
     }
   };
-  auto load = [&](u32x4 (&w)[U], int sb) { load_part(w, sb, 0, U); };
+  auto load = [&](Batch& b, int sb) { load_part(b, sb, 0, U); };
   int cur = active ? s0 / ipr : 0;        // relative row being accumulated
   const int first = cur;
   float acc0 = 0.f, acc1 = 0.f;
@@ -102,7 +118,7 @@ __device__ __forceinline__ void rowdot_flat(RowPtr row_ptr, Epi epi, int nrows, 
     acc0 = 0.f;
     acc1 = 0.f;
   };
-  auto consume = [&](const u32x4 (&w)[U], int sb) {
+  auto consume = [&](const Batch& b, int sb) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int s = sb + u;
@@ -114,10 +130,11 @@ __device__ __forceinline__ void rowdot_flat(RowPtr row_ptr, Epi epi, int nrows, 
       }
       const int c = (s - rr * ipr) * 64 + lane;
       if (c < nch) {
-        if (u & 1)
-          acc1 = dot_chunk<T>(w[u], xs, d, c, acc1);
+        float& acc = (u & 1) ? acc1 : acc0;
+        if constexpr (Q4)
+          acc = dot_chunk_q4(b.w[u], (float)b.s[u], xs, d, c, acc);
         else
-          acc0 = dot_chunk<T>(w[u], xs, d, c, acc0);
+          acc = dot_chunk<T>(b.w[u], xs, d, c, acc);
       }
     }
   };
@@ -126,14 +143,14 @@ __device__ __forceinline__ void rowdot_flat(RowPtr row_ptr, Epi epi, int nrows, 
   // batch follows once the input is staged, so that the staging reads do not queue
   // behind a full batch from every wavefront of the grid.
   constexpr int PRE = kRowdotPre < U ? kRowdotPre : U;
-  u32x4 wa[U];
+  Batch wa;
   if (PRE > 0) load_part(wa, s0, 0, PRE);
   st.finish(d, be != nullptr, eps, xs, red);
   if (PRE < U) load_part(wa, s0, PRE, U);
   if (xhat_out != nullptr && wg == 0)
     for (int e = threadIdx.x; e < d; e += NT) xhat_out[e] = xs[xs_index<T>(e, d)];
   if (active) {
-    u32x4 wb[U];
+    Batch wb;
     for (int sb = s0;;) {
       load(wb, sb + U);
       consume(wa, sb);

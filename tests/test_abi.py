@@ -67,6 +67,9 @@ def test_sparse_mlp_validation(lib):
     assert _call_mlp(lib, _mlp(), n_idx=129) == 2                     # k > n
     assert _call_mlp(lib, _mlp(), Bn=0) == 2
     assert _call_mlp(lib, _mlp(), per_seq=2) == 9
+    bad_act = _mlp()
+    bad_act.act = 2
+    assert _call_mlp(lib, bad_act) == 9                                # unknown activation
     assert _call_mlp(lib, _mlp(), mode=5) == 9
     assert _call_mlp(lib, _mlp(), flags=1 << 7) == 9
     assert _call_mlp(lib, _mlp(), ws=None) == 5
