@@ -7,11 +7,18 @@
  * decode-time hot path on one GPU:
  *   - the low-rank sparsity predictors (two thin GEMVs, then top-k or threshold
  *     selection): dv_predict_mlp, dv_predict_heads;
- *   - the sparsified MLP of Eq. (1): dv_sparse_mlp;
+ *   - the sparsified MLP of Eq. (1): dv_sparse_mlp (fp16/fp32 weights, one token
+ *     or a batch of up to 32), dv_sparse_mlp_q4 (4-bit weights, Section 5.2);
  *   - the sparsified multi-head attention of Eq. (2) over a KV cache:
- *     dv_sparse_attn;
+ *     dv_sparse_attn, and dv_sparse_attn_kvfill with the missing-KV rule of
+ *     Section 4.2;
  *   - one whole decoder layer with predictors, layer norms and residuals
- *     (Section 4.3): dv_sparse_block.
+ *     (Section 4.3): dv_sparse_block, and dv_sparse_block_noalloc for callers
+ *     that cannot allocate a workspace;
+ *   - several layers of one token with the cross-layer look-ahead of Section 4.3:
+ *     dv_sparse_decode.
+ * Aids: dv_set_launch_events / dv_launch_label (per-launch timing) and
+ * dv_stream_read (a plain streaming read, the measured bandwidth ceiling).
  *
  * Conventions shared by every entry point
  *   Memory.   Every array pointer is a DEVICE pointer owned by the caller, except
@@ -194,8 +201,8 @@ dv_status dv_predict_heads(const dv_predictor *p, const float *x, int32_t B, int
                            float *scores, void *ws, size_t ws_bytes, uint32_t flags, void *stream);
 
 /* --------------------------------------------------------------- sparse MLP
- * dv_sparse_mlp: out[b] = MLP_S(x[b]) = b2 + sum_{i in S} ReLU(x[b] . W^1_i + b1_i) W^2_i
- * (Eq. (1)), without any residual.
+ * dv_sparse_mlp: out[b] = MLP_S(x[b]) = b2 + sum_{i in S} sigma(x[b] . W^1_i + b1_i) W^2_i
+ * (Eq. (1); sigma = ReLU or GeLU by m->act), without any residual.
  *   idx          device int32: idx_per_seq == 0: one set idx[n_idx] shared by all B
  *                sequences; idx_per_seq == 1: idx[B][n_idx], one set per sequence.
  *   batch_mode   with per-sequence sets and B > 1: DV_MLP_UNION or DV_MLP_MASKED.
@@ -261,7 +268,7 @@ dv_status dv_sparse_attn(const dv_attn *a, const float *x, int32_t B, const dv_k
  *   out, heads, n_heads, scale, ws, flags as for dv_sparse_attn (workspace: the
  *          dv_sparse_attn_workspace_bytes query with B = 1).
  * Cost: one launch more than dv_sparse_attn; it reads no weights when no selected head
- * misses a row, otherwise each selected head's W^K and W^V rows once per 8 missing
+ * misses a row, otherwise each selected head's W^K and W^V rows once per 4 missing
  * positions. Limits: pos <= 32768 (else DV_ERR_UNSUPPORTED). */
 dv_status dv_sparse_attn_kvfill(const dv_attn *a, const float *x, const dv_kv *kv, float *Y, uint8_t *valid,
                                 const int32_t *heads, int32_t n_heads, float scale, float *out, void *ws,

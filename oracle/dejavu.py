@@ -33,7 +33,8 @@ Readings where the paper is silent or loose (each is also listed in the design n
       (b1 per neuron before sigma; b2, bo once per output).
   R3  X holds the past tokens and the current one: attention covers cache rows
       0..pos-1 and the fresh key/value at pos.
-  R4  sigma is ReLU (OPT).
+  R4  sigma is ReLU (OPT) by default; GeLU (BLOOM) is the other choice Section 2.3
+      names (see R16).
   R5  The predictor is the linear low-rank map s = (x A) B with A = AT^T (d x r),
       B = BT^T (r x n): no hidden activation, no bias.
   R6  The rule from scores to a set: top-k of the raw scores (ties: lower index
@@ -45,6 +46,16 @@ Readings where the paper is silent or loose (each is also listed in the design n
   R9  Batch > 1: the MLP runs on the union U of the per-sequence sets for every
       sequence ("union"), or on each sequence's own set ("masked"); attention uses
       each sequence's own head set and its own position.
+  R15 4-bit weights (Section 5.2, W4A16; the paper fixes no format): each row in
+      blocks of 32 elements with one fp16 scale per block, element = scale * (q - 8)
+      for a 4-bit code q, two codes per byte, the even element in the low nibble.
+  R16 GeLU is the exact form x * Phi(x) with the normal CDF written through erf.
+  R17 Cross-layer look-ahead (Section 4.3): the sets of layer l+1 come from layer
+      l+1's own predictors (they score its heads and neurons) applied to layer l's
+      normalised input LN1^l(y_l); layer 0's sets from its predictors on LN1^0(y_0).
+  R18 Missing keys and values (Section 4.2): the kept per-token input is the
+      attention block's normalised input (what the keys and values are computed
+      from); a head selected now gets its missing rows from it before it attends.
 
 Parity pins: every function here is checked in tests/test_oracle_*.py against
 something other than itself (closed forms, brute force on tiny shapes, invariants,
@@ -393,7 +404,7 @@ def lookahead_layers(y, layers: Sequence[Dict], scale: float, k_heads: int, k_ml
         S^{l+1} = (top-k_heads(SP_A^{l+1}(x_l)), top-k_mlp(SP_M^{l+1}(x_l))), x_l = LN1^l(y_l)
         y_{l+1} = sparse_block_l(y_l; S^l)
     (the paper writes the predictor that produces S^{l+1} from y_l as SP^l; here it is
-    stored with layer l+1, whose heads and neurons it scores, reading R10). S0, if given,
+    stored with layer l+1, whose heads and neurons it scores, reading R17). S0, if given,
     replaces the prediction of S^0. layers[l] holds attn, mlp, K, V (the layer's cache
     of this sequence), pos, pred_h and pred_m ({AT, BT}) and ln.
     Returns {out, y: [y_0..y_L], S_A, S_M (per layer), K_new, V_new (per layer)}.
