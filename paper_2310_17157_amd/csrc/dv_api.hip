@@ -254,13 +254,10 @@ struct AttnWs {
   int32_t* heads; float* q; float* part; float* axp; uint32_t* axc; int32_t* flag;
 };
 
-// Upper bound of split-KV chunks per head.
-static int max_split(int) { return kAttnMaxSplit; }
-
-static size_t attn_ws_layout(const dv_attn* a, int cap, int B, int n_heads, Workspace& w, AttnWs* o) {
+static size_t attn_ws_layout(const dv_attn* a, int B, int n_heads, Workspace& w, AttnWs* o) {
   o->heads = w.take<int32_t>((size_t)B * n_heads * sizeof(int32_t));
   o->q = w.take<float>((size_t)B * n_heads * a->dh * sizeof(float));
-  o->part = w.take<float>((size_t)B * n_heads * max_split(cap) * (a->dh + 2) * sizeof(float));
+  o->part = w.take<float>((size_t)B * n_heads * kAttnMaxSplit * (a->dh + 2) * sizeof(float));
   o->axp = w.take<float>(axpy_partial_bytes(a->d));
   o->axc = w.take<uint32_t>(kAxpyMaxSpans * sizeof(uint32_t));
   o->flag = w.take<int32_t>(sizeof(int32_t));
@@ -274,7 +271,7 @@ extern "C" size_t dv_sparse_attn_workspace_bytes(const dv_attn* a, const dv_kv* 
   if (B > 1) return batch_attn_ws(a, B, n_heads);
   Workspace w(nullptr);
   AttnWs o;
-  return attn_ws_layout(a, kv->cap, B, n_heads, w, &o);
+  return attn_ws_layout(a, B, n_heads, w, &o);
 }
 
 static dv_status enqueue_attention(const dv_attn* a, const dv_kv* kv, const AttnWs& o, int n_heads,
@@ -316,7 +313,7 @@ extern "C" dv_status dv_sparse_attn(const dv_attn* a, const float* x, int32_t B,
   if (B > 1) return batch_attn(a, x, B, kv, heads, n_heads, scale, out, ws, ws_bytes, flags, hs);
   Workspace w(ws);
   AttnWs o;
-  if (attn_ws_layout(a, kv->cap, B, n_heads, w, &o) > ws_bytes) return DV_ERR_WORKSPACE;
+  if (attn_ws_layout(a, B, n_heads, w, &o) > ws_bytes) return DV_ERR_WORKSPACE;
   if (flags & DV_VALIDATE) {
     st = validate_sets(heads, 1, n_heads, a->H, o.flag, hs);
     if (st != DV_OK) return st;
@@ -422,7 +419,7 @@ extern "C" dv_status dv_sparse_attn_kvfill(const dv_attn* a, const float* x, con
   hipStream_t hs = static_cast<hipStream_t>(stream);
   Workspace w(ws);
   AttnWs o;
-  if (attn_ws_layout(a, kv->cap, 1, n_heads, w, &o) > ws_bytes) return DV_ERR_WORKSPACE;
+  if (attn_ws_layout(a, 1, n_heads, w, &o) > ws_bytes) return DV_ERR_WORKSPACE;
   if (flags & DV_VALIDATE) {
     st = validate_sets(heads, 1, n_heads, a->H, o.flag, hs);
     if (st != DV_OK) return st;
@@ -466,9 +463,8 @@ struct BlockWs {
   float* q; float* part; float* ytilde; float* xhat; float* h; float* axp; uint32_t* axc; int32_t* flag;
 };
 
-static size_t block_ws_layout(const dv_attn* a, const dv_mlp* m, const dv_predictor* pa,
-                              const dv_predictor* pm, int cap, int B, int kh, int km, Workspace& w,
-                              BlockWs* o) {
+static size_t block_ws_layout(const dv_attn* a, const dv_predictor* pa, const dv_predictor* pm, int B, int kh,
+                              int km, Workspace& w, BlockWs* o) {
   o->hid_h = w.take<float>((size_t)B * pa->r * sizeof(float));
   o->hid_m = w.take<float>((size_t)B * pm->r * sizeof(float));
   o->s_h = w.take<float>((size_t)B * pa->n_out * sizeof(float));
@@ -476,7 +472,7 @@ static size_t block_ws_layout(const dv_attn* a, const dv_mlp* m, const dv_predic
   o->heads = w.take<int32_t>((size_t)B * kh * sizeof(int32_t));
   o->idx = w.take<int32_t>((size_t)B * km * sizeof(int32_t));
   o->q = w.take<float>((size_t)B * kh * a->dh * sizeof(float));
-  o->part = w.take<float>((size_t)B * kh * max_split(cap) * (a->dh + 2) * sizeof(float));
+  o->part = w.take<float>((size_t)B * kh * kAttnMaxSplit * (a->dh + 2) * sizeof(float));
   o->ytilde = w.take<float>((size_t)B * a->d * sizeof(float));
   o->xhat = w.take<float>((size_t)B * a->d * sizeof(float));
   o->h = w.take<float>((size_t)B * km * sizeof(float));
@@ -496,7 +492,7 @@ extern "C" size_t dv_sparse_block_workspace_bytes(const dv_attn* a, const dv_mlp
   if (B > 1) return batch_block_ws(a, m, pa, pm, B, k_heads, k_mlp);
   Workspace w(nullptr);
   BlockWs o;
-  return block_ws_layout(a, m, pa, pm, kv->cap, B, k_heads, k_mlp, w, &o);
+  return block_ws_layout(a, pa, pm, B, k_heads, k_mlp, w, &o);
 }
 
 dv_status dv::check_predictor_for(const dv_predictor* p, int d, int n_out) {
@@ -546,7 +542,7 @@ extern "C" dv_status dv_sparse_block(const dv_attn* a, const dv_mlp* m, const dv
   if (!ws_ok(ws)) return DV_ERR_WORKSPACE;
   Workspace w(ws);
   BlockWs o;
-  if (block_ws_layout(a, m, pa, pm, kv->cap, B, k_heads, k_mlp, w, &o) > ws_bytes) return DV_ERR_WORKSPACE;
+  if (block_ws_layout(a, pa, pm, B, k_heads, k_mlp, w, &o) > ws_bytes) return DV_ERR_WORKSPACE;
   hipStream_t hs = static_cast<hipStream_t>(stream);
 
   const float* g1 = ln ? ln->g1 : nullptr;

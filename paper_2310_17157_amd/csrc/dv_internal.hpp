@@ -235,12 +235,12 @@ struct StageX {
       float s = 0.f;
 #pragma unroll
       for (int k = 0; k < K; ++k)
-        if (threadIdx.x + k * NT < n4) s += (v[k][0] + v[k][1]) + (v[k][2] + v[k][3]);
+        if ((int)threadIdx.x + k * NT < n4) s += (v[k][0] + v[k][1]) + (v[k][2] + v[k][3]);
       const float mean = block_sum<NT>(s, red) / (float)d;
       float q = 0.f;
 #pragma unroll
       for (int k = 0; k < K; ++k) {
-        if (threadIdx.x + k * NT < n4) {
+        if ((int)threadIdx.x + k * NT < n4) {
           const float a0 = v[k][0] - mean, a1 = v[k][1] - mean, a2 = v[k][2] - mean, a3 = v[k][3] - mean;
           q += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
         }
