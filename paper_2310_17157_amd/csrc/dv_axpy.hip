@@ -18,7 +18,12 @@
 // invalidates a whole L2: partials are written and read with agent-scope (coherent,
 // L2-bypassing) atomic stores and loads, each workgroup waits for its stores to be
 // acknowledged before it increments its span's counter, and the workgroup that
-// draws the last ticket reads every split after that.
+// draws the last ticket reads every split after that. The HIP memory model alone does
+// not order relaxed atomics on different addresses; the protocol rests on gfx950
+// compiling agent-scope stores and loads to sc1 accesses (write-through to, and reads
+// from, the memory side shared by all XCDs), on s_waitcnt returning only once those
+// stores are acknowledged, and on the barrier that follows (also a compiler barrier)
+// keeping the ticket below every wavefront's wait.
 //
 // For the attention the coefficients H_i(y)[t] are combined first, in the prologue,
 // from the split-KV partials (max logit, sum of exponentials and unnormalised value
