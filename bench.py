@@ -814,9 +814,9 @@ def bench_batch(args, cfg):
 def default_replicas(cfg):
     """Layer copies the steps cycle through: enough that what one step reads is not still
     in the 256 MB Infinity Cache when the same copy comes round again. At batch 1 the
-    selected keys and values
-    (33.5 MB per copy at the OPT-175B shape) stay in the cache across calls: 10 copies hold
-    335 MB of them (with 4, the attention launch measured 8.4 us against 9.5 us)."""
+    selected keys and values of a copy (33.5 MB at the OPT-175B shape) would otherwise
+    stay in the cache across calls: 10 copies hold 335 MB of them (with 4, the attention
+    launch measured 8.4 us against 9.5 us)."""
     return 10 if cfg.B == 1 else 4
 
 
