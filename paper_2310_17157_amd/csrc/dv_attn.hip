@@ -271,12 +271,11 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
       L += sm_l[w] * f[w];
     }
     const float rl = 1.f / L;
-    _Float16* o = a.C + (size_t)b * a.ldc + (size_t)up * a.dh;
     for (int t = threadIdx.x; t < a.dh; t += 256) {
       float acc = 0.f;
 #pragma unroll
       for (int w = 0; w < NW; ++w) acc += sm_o[w][t] * f[w];
-      o[t] = (_Float16)(acc * rl);
+      a.C[coef_index(b, up * a.dh + t, a.cnb)] = (_Float16)(acc * rl);
     }
     return;
   }

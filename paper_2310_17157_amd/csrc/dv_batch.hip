@@ -14,7 +14,7 @@
 //                 rows whose contraction index is contiguous in memory (fc1, Q/K/V,
 //                 predictor factors). A workgroup stages one K-split of x-hat in LDS;
 //                 each wavefront streams 16-row tiles straight into MFMA operands.
-//   k_mfma_cols   P2[s][b][n] = sum_{u in split s} C[b][u] M[row(u)][n]: gathered rows
+//   k_mfma_cols   P2[s][b][n] = sum_{u in split s} C(b, u) M[row(u)][n]: gathered rows
 //                 contracted over the row index (fc2, out-projection). Row tiles are
 //                 written to a per-wavefront LDS tile (XOR-swizzled) and read back
 //                 column-wise with the LDS transpose read into the B operand.
@@ -557,7 +557,7 @@ __device__ __forceinline__ void mc_load(ColsStep<NB, U>& st, const int (&ix)[U][
       st.w[u][i] = ld_stream(Mb + (size_t)ix[u][i] * rowb);
     }
 #pragma unroll
-    for (int j = 0; j < NB / 16; ++j) st.h[u][j] = ld_plain(a.C + (size_t)(lr + 16 * j) * a.ldc + 32 * q + 8 * lg);
+    for (int j = 0; j < NB / 16; ++j) st.h[u][j] = ld_plain(a.C + coef_index(lr + 16 * j, 32 * q + 8 * lg, NB));
   }
 }
 
@@ -745,7 +745,7 @@ __device__ __forceinline__ float sum_splits(const float* __restrict__ P, int S, 
   return v;
 }
 
-// fc1: C[b][u] = fp16(ReLU(sum_s P[s][u][b] + b1[list[u]])) for b < B and u < n (and,
+// fc1: C(b, u) = fp16(ReLU(sum_s P[s][u][b] + b1[list[u]])) for b < B and u < n (and,
 // with a mask, only where bit b of mask[u] is set); zero elsewhere up to a multiple
 // of 64 rows. One workgroup per 64 rows.
 template <int NB>
@@ -777,7 +777,7 @@ __global__ void __launch_bounds__(16 * NB) k_fc1_finish(Fc1FinishArgs a) {
   __syncthreads();
   for (int e = threadIdx.x; e < 64 * NB; e += 16 * NB) {
     const int b = e >> 6, ul = e & 63;
-    a.C[(size_t)b * a.ldc + u0 + ul] = (_Float16)t[ul][b];
+    a.C[coef_index(b, u0 + ul, NB)] = (_Float16)t[ul][b];
   }
 }
 
@@ -903,9 +903,10 @@ hipError_t launch_qkv_finish(int NB, int kvtype, const QkvFinishArgs& a, hipStre
   return hipGetLastError();
 }
 
-// Attention outputs as out-projection coefficients: C[b][p*dh + t] = H_h(x_b)[t] for
+// Attention outputs as out-projection coefficients: C(b, p*dh + t) = H_h(x_b)[t] for
 // the union head h = list[p] if h is in sequence b's set (combining its split-KV
-// partials), else 0; rows up to ldc are covered (zero beyond the union).
+// partials), else 0; rows up to ldc are covered (zero beyond the union). C is in the
+// layout of coef_index with gridDim.y (the padded token count) tokens.
 __global__ void __launch_bounds__(256) k_attn_finish(AttnFinishArgs a) {
   __shared__ float fac[kAttnMaxSplit];
   __shared__ int jsel;
@@ -913,7 +914,6 @@ __global__ void __launch_bounds__(256) k_attn_finish(AttnFinishArgs a) {
   const int nu = *a.hcount;
   const int r0 = p * a.dh;
   if (r0 >= a.ldc) return;
-  _Float16* o = a.C + (size_t)b * a.ldc + r0;
   const int rows = min(a.dh, a.ldc - r0);
   if (threadIdx.x == 0) {
     int jj = -1;
@@ -950,7 +950,7 @@ __global__ void __launch_bounds__(256) k_attn_finish(AttnFinishArgs a) {
       const float* P = a.part + ((size_t)b * a.n_heads + jj) * a.n_split * (a.dh + 2) + 2 + t;
       for (int c = 0; c < a.n_split; ++c) v += P[(size_t)c * (a.dh + 2)] * fac[c];
     }
-    o[t] = (_Float16)v;
+    a.C[coef_index(b, r0 + t, gridDim.y)] = (_Float16)v;
   }
 }
 

@@ -180,7 +180,7 @@ static dv_status battn_run(const dv_attn* a, const dv_kv* kv, const BAttn& o, in
   const bool direct = at.n_split == 1;
   if (direct) {
     qf.zero = o.C; qf.zero_n = NB * o.ldc;
-    at.C = o.C; at.ldc = o.ldc; at.ulist = o.Uh; at.ucount = o.hcnt;
+    at.C = o.C; at.ldc = o.ldc; at.cnb = NB; at.ulist = o.Uh; at.ucount = o.hcnt;
   }
   DV_LAUNCH("qkv_finish", hs, launch_qkv_finish(NB, kv->ktype, qf, hs));
   DV_LAUNCH("attn", hs, launch_attn(kv->ktype, at, B, hs));

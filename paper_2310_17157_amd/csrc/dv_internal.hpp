@@ -378,9 +378,9 @@ struct AttnArgs {
   float scale;
   float* part;                      // [B][n_heads][n_split][dh + 2]
   // One chunk per head (n_split == 1) and C set: the output H_h(x_b) goes straight to
-  // the out-projection's fp16 coefficients C[b][p * dh + t] (p: h's place in the union
+  // the out-projection's fp16 coefficients C(b, p * dh + t) (p: h's place in the union
   // list ulist[0..*ucount)) instead of a partial; the rest of C is zeroed beforehand.
-  _Float16* C; int ldc; const int32_t* ulist; const int32_t* ucount;
+  _Float16* C; int ldc; int cnb; const int32_t* ulist; const int32_t* ucount;   // C: coef_index layout, cnb tokens
   uint8_t* valid;                   // optional [B][H][cap]: rows attended are marked present
 };
 hipError_t launch_attn(int kvtype, const AttnArgs& a, int B, hipStream_t st);
@@ -491,8 +491,9 @@ void mrows_split(int Kpad, int NB, int* S, int* Ks);
 hipError_t launch_mrows(int NB, const MrowsArgs& a, hipStream_t st);
 
 // Token-batch coefficients times gathered rows, contracted over the rows:
-// P[s][b][c] = sum_{u in split s} C[b][u] M[row(u)][c], row(u) = list[u] (dh == 0) or
-// list[u / dh] * dh + u % dh. C is fp16 [NB][ldc], zero beyond the rows in use.
+// P[s][b][c] = sum_{u in split s} C(b, u) M[row(u)][c], row(u) = list[u] (dh == 0) or
+// list[u / dh] * dh + u % dh. C is fp16, NB tokens x ldc rows (ldc a multiple of 32) in the
+// blocked layout of coef_index, zero beyond the rows in use.
 struct McolsArgs {
   int d;
   const void* M;
@@ -505,7 +506,16 @@ struct McolsArgs {
 int mcols_split(int d, int nmax);
 hipError_t launch_mcols(int NB, const McolsArgs& a, hipStream_t st);
 
-// C[b][u] = fp16(ReLU(sum_s P[s][u][b] + b1[list[u]])), masked by membership bits.
+// Coefficient matrices of the contraction over gathered rows (k_mfma_cols' C): blocks of 32
+// rows, each NB tokens x 32 rows row-major, so that the 32 rows one k-step contracts are
+// one contiguous NB * 64-byte piece (a wavefront's coefficient load then covers whole
+// 128-byte lines instead of 64-byte pieces of 16 token rows).
+__host__ __device__ __forceinline__ size_t coef_index(int b, int u, int nb) {
+  return ((size_t)(u >> 5) * nb + b) * 32 + (u & 31);
+}
+
+// C(b, u) = fp16(sigma(sum_s P[s][u][b] + b1[list[u]])), masked by membership bits
+// (C in the layout of coef_index).
 struct Fc1FinishArgs {
   const float* P; int S, nrows_pad;
   const int32_t* list; const int32_t* list_count; int list_max; int list_range;
@@ -537,7 +547,7 @@ struct QkvFinishArgs {
 };
 hipError_t launch_qkv_finish(int NB, int kvtype, const QkvFinishArgs& a, hipStream_t st);
 
-// Out-projection coefficients C[b][p*dh + t] from the split-KV partials.
+// Out-projection coefficients C(b, p*dh + t) (coef_index layout) from the split-KV partials.
 struct AttnFinishArgs {
   const float* part; int n_split, n_heads, dh, B;
   const int32_t* heads; const int32_t* list; const int32_t* hcount;
