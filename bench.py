@@ -16,7 +16,7 @@ Inputs are seeded synthetic layers already resident in HBM; R independent layer
 replicas are cycled so that nothing a step reads is served from the 256 MB Infinity
 Cache (default R = 10 at batch 1, whose selected keys and values are 33.5 MB per
 replica; 4 at batch 32, which reads 675 MB of keys and values per step). Prints ONE JSON line: the value, the roofline of the dominant kernel from HIP
-events recorded around each of its launches on the library's stream, and the fp64
+events stamped by its launches' own dispatches on the library's stream, and the fp64
 oracle timed on this host's cores on a bounded sample.
 """
 import argparse
@@ -33,7 +33,7 @@ METRIC = "µs/layer/token sparse block at OPT-175B shape, batch 1; achieved HBM 
 METRIC_B32 = ("µs/layer/token sparse attention + union MLP at OPT-175B shape, batch 32 (sets given); "
               "achieved HBM GB/s vs peak")
 PEAK_HBM_GBPS = 8000.0
-ROOFLINE_EVERY = 8   # timed steps per event-bracketed launch of the dominant kernel
+ROOFLINE_EVERY = 8   # timed steps per event-timed launch of the dominant kernel
 
 
 def kernel_bytes(cfg, pos):
@@ -374,13 +374,13 @@ def bench_b1(args, cfg):
         step(i)
     torch.cuda.synchronize()
 
-    # Diagnostic pass: every launch bracketed by events (the events themselves add
-    # a few microseconds per launch, so this pass is not the reported step time).
+    # Diagnostic pass: every launch timed with events (each timed launch leaves the
+    # GPU idle for a few microseconds, so this pass is not the reported step time).
     ms_all_events, _, per_kernel = _measure(stream, step, args.steps, 1)
     kb = kernel_bytes(cfg, pos)
     dom = max((l for l in per_kernel if l in kb), key=lambda l: statistics.mean(per_kernel[l]))
-    # Timed region: events around the dominant kernel's launch on every
-    # ROOFLINE_EVERY-th step (each event record idles the GPU for a few microseconds).
+    # Timed region: events on the dominant kernel's launch on every
+    # ROOFLINE_EVERY-th step (each timed launch idles the GPU for a few microseconds).
     ms_per_step, wall, per_dom = _measure(stream, step, args.steps, 1, only=dom, every=ROOFLINE_EVERY)
     # Each block kernel timed the same way in a pass of its own (launch averages for
     # the block roofline).

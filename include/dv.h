@@ -160,12 +160,14 @@ const char *dv_status_string(int32_t status);
 int32_t dv_abi_version(void);
 
 /* Per-launch timing (tracing aid). While armed on the calling thread, every entry point
- * called on that thread records, on its stream, events[2*i] just before and
- * events[2*i+1] just after its i-th timed kernel launch (for i < n_pairs), where events
- * are hipEvent_t handles created by the caller. A launch is timed if `only` is NULL or
- * equals its label. The number of launches of the latest call is stored in
- * *n_launched; dv_launch_label(i) names its i-th launch. Pass events == NULL to
- * disarm. Returns DV_ERR_SHAPE if n_pairs < 0. */
+ * called on that thread times its launches (for the i-th timed launch, i < n_pairs):
+ * events[2*i] takes the start time of the launch's first kernel and events[2*i+1] the
+ * end time of its last kernel, both stamped by those kernels' own dispatches
+ * (hipExtLaunchKernel) on the entry point's stream; a launch that runs no kernel
+ * records the two events back to back. Events are hipEvent_t handles created by the
+ * caller. A launch is timed if `only` is NULL or equals its label. The number of
+ * launches of the latest call is stored in *n_launched; dv_launch_label(i) names its
+ * i-th launch. Pass events == NULL to disarm. Returns DV_ERR_SHAPE if n_pairs < 0. */
 dv_status dv_set_launch_events(void **events, int32_t n_pairs, int32_t *n_launched, const char *only);
 const char *dv_launch_label(int32_t i);
 

@@ -631,12 +631,13 @@ _HIP_EVENT_DISABLE_SYSTEM_FENCE = 0x20000000   # hipEventDisableSystemFence
 
 
 class LaunchTimer:
-    """HIP events around each kernel launch of the library's entry points.
+    """Per-launch times of the library's entry points from HIP events.
 
     Arms dv_set_launch_events with `n_pairs` event pairs created through the HIP
     runtime; after a call (and a synchronisation) `times_ms()` returns
-    [(label, milliseconds)] for each launch of that call. Events are recorded on
-    the stream the library launched on.
+    [(label, milliseconds)] for each launch of that call: from the start of the
+    launch's first kernel to the end of its last, as stamped by the kernels'
+    own dispatches on the stream the library launched on.
     """
 
     def __init__(self, n_pairs: int = 16, only: Optional[str] = None):

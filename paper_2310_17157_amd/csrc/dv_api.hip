@@ -73,6 +73,7 @@ struct Trace {
   int count = 0;                // launches of the current call
   int timed = 0;                // event pairs used by the current call
   bool open = false;            // the current launch records events
+  bool started = false;         // its start event went to a kernel
   const char* labels[64] = {};
 };
 thread_local Trace g_trace;
@@ -87,13 +88,25 @@ void trace_begin(const char* label, hipStream_t st) {
   Trace& t = g_trace;
   if (t.count < 64) t.labels[t.count] = label;
   t.open = t.events != nullptr && t.timed < t.n_pairs && (t.only == nullptr || strcmp(t.only, label) == 0);
-  if (t.open) (void)hipEventRecord(static_cast<hipEvent_t>(t.events[2 * t.timed]), st);
+  t.started = false;
+  (void)st;
+}
+
+void trace_take(hipEvent_t* start, hipEvent_t* stop) {
+  Trace& t = g_trace;
+  if (!t.open) return;
+  if (!t.started) *start = static_cast<hipEvent_t>(t.events[2 * t.timed]);
+  *stop = static_cast<hipEvent_t>(t.events[2 * t.timed + 1]);
+  t.started = true;
 }
 
 void trace_end(hipStream_t st) {
   Trace& t = g_trace;
   if (t.open) {
-    (void)hipEventRecord(static_cast<hipEvent_t>(t.events[2 * t.timed + 1]), st);
+    if (!t.started) {   // no kernel ran: an empty interval, so both events are set
+      (void)hipEventRecord(static_cast<hipEvent_t>(t.events[2 * t.timed]), st);
+      (void)hipEventRecord(static_cast<hipEvent_t>(t.events[2 * t.timed + 1]), st);
+    }
     ++t.timed;
     t.open = false;
   }

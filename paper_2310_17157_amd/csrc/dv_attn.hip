@@ -103,11 +103,11 @@ static hipError_t launch_qkv_t(const QkvArgs& a, hipStream_t st) {
   if (a.g != nullptr) {
     const hipError_t e = ensure_dyn_lds(reinterpret_cast<const void*>(k_qkv<T, KT, NW, U, KX, true>), lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((k_qkv<T, KT, NW, U, KX, true>), grid, dim3(NW * 64), lds, st, a);
+    launch_k((k_qkv<T, KT, NW, U, KX, true>), grid, dim3(NW * 64), lds, st, a);
   } else {
     const hipError_t e = ensure_dyn_lds(reinterpret_cast<const void*>(k_qkv<T, KT, NW, U, KX, false>), lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((k_qkv<T, KT, NW, U, KX, false>), grid, dim3(NW * 64), lds, st, a);
+    launch_k((k_qkv<T, KT, NW, U, KX, false>), grid, dim3(NW * 64), lds, st, a);
   }
   return hipGetLastError();
 }
@@ -326,7 +326,7 @@ int attn_chunk(int n_heads, int attended, int dh, int kvtype) {
 template <typename KT, int LPP>
 static hipError_t launch_attn_l(const AttnArgs& a, int B, hipStream_t st) {
   dim3 grid(a.n_split, a.n_heads, B);
-  hipLaunchKernelGGL((k_attn<KT, LPP, kAttnNStep>), grid, dim3(256), 0, st, a);
+  launch_k((k_attn<KT, LPP, kAttnNStep>), grid, dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
@@ -453,7 +453,7 @@ static hipError_t launch_kv_fill_t(const KvFillArgs& a, hipStream_t st) {
   constexpr int RPW = kFillRows / 4, MT = 4;
   const hipError_t e = ensure_dyn_lds(reinterpret_cast<const void*>(k_kv_fill<T, KT, RPW, MT>), lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((k_kv_fill<T, KT, RPW, MT>), dim3(max(1, a.n_heads) * nrb), dim3(256), lds, st, a);
+  launch_k((k_kv_fill<T, KT, RPW, MT>), dim3(max(1, a.n_heads) * nrb), dim3(256), lds, st, a);
   return hipGetLastError();
 }
 

@@ -253,8 +253,8 @@ static hipError_t launch_axpy_t(AxpyArgs a, hipStream_t st) {
   const int rpb = min(kAxRowsLds, max(1, (a.nrows + S - 1) / S));
   a.rows_per_batch = rpb;
   const size_t lds = (size_t)rpb * 8 + (size_t)NW * 64 * E * 4;
-  hipLaunchKernelGGL((k_axpy<T, NW, U, HEADS>), dim3(spans, S), dim3(NW * 64), lds, st, a);
-  if (S > 1 && a.cnt == nullptr) hipLaunchKernelGGL(k_axpy_sum, dim3((a.d / 4 + 255) / 256), dim3(256), 0, st, a, S);
+  launch_k((k_axpy<T, NW, U, HEADS>), dim3(spans, S), dim3(NW * 64), lds, st, a);
+  if (S > 1 && a.cnt == nullptr) launch_k(k_axpy_sum, dim3((a.d / 4 + 255) / 256), dim3(256), 0, st, a, S);
   return hipGetLastError();
 }
 

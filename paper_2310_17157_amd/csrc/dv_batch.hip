@@ -153,9 +153,9 @@ hipError_t launch_union(const int32_t* sets, int B, int k, int n, int32_t* U, in
   const hipError_t e = ensure_dyn_lds(kern, lds);
   if (e != hipSuccess) return e;
   if (mask != nullptr)
-    hipLaunchKernelGGL(k_union<true>, dim3(nc), dim3(kUnionNT), lds, st, sets, B, k, n, U, count, mask);
+    launch_k(k_union<true>, dim3(nc), dim3(kUnionNT), lds, st, sets, B, k, n, U, count, mask);
   else
-    hipLaunchKernelGGL(k_union<false>, dim3(nc), dim3(kUnionNT), lds, st, sets, B, k, n, U, count, mask);
+    launch_k(k_union<false>, dim3(nc), dim3(kUnionNT), lds, st, sets, B, k, n, U, count, mask);
   return hipGetLastError();
 }
 
@@ -232,7 +232,7 @@ __global__ void __launch_bounds__(1024) k_cast_union(const float* __restrict__ x
 
 hipError_t launch_ln_cast(const float* x, int B, int NB, int d, int Kpad, const float* g, const float* be, float eps,
                           _Float16* X16, hipStream_t st) {
-  hipLaunchKernelGGL(k_ln_cast, dim3(NB), dim3(1024), 0, st, x, B, d, Kpad, g, be, eps, X16);
+  launch_k(k_ln_cast, dim3(NB), dim3(1024), 0, st, x, B, d, Kpad, g, be, eps, X16);
   return hipGetLastError();
 }
 
@@ -247,10 +247,10 @@ hipError_t launch_cast_union(const float* x, int B, int NB, int d, int Kpad, con
   const hipError_t e = ensure_dyn_lds(kern, lds);
   if (e != hipSuccess) return e;
   if (mask != nullptr)
-    hipLaunchKernelGGL(k_cast_union<true>, dim3(NB + nc), dim3(1024), lds, st, x, B, d, Kpad, g, be, eps, X16, NB,
+    launch_k(k_cast_union<true>, dim3(NB + nc), dim3(1024), lds, st, x, B, d, Kpad, g, be, eps, X16, NB,
                        sets, k, n, U, count, mask, nc);
   else
-    hipLaunchKernelGGL(k_cast_union<false>, dim3(NB + nc), dim3(1024), lds, st, x, B, d, Kpad, g, be, eps, X16, NB,
+    launch_k(k_cast_union<false>, dim3(NB + nc), dim3(1024), lds, st, x, B, d, Kpad, g, be, eps, X16, NB,
                        sets, k, n, U, count, mask, nc);
   return hipGetLastError();
 }
@@ -479,7 +479,7 @@ static hipError_t launch_mrows_t(MrowsArgs a, hipStream_t st) {
   const hipError_t e = ensure_dyn_lds(reinterpret_cast<const void*>(kern), lds);
   if (e != hipSuccess) return e;
   const int G = max(1, device_cu_count() / a.S);
-  hipLaunchKernelGGL(kern, dim3(G * a.S), dim3(kMrNW * 64), lds, st, a);
+  launch_k(kern, dim3(G * a.S), dim3(kMrNW * 64), lds, st, a);
   return hipGetLastError();
 }
 
@@ -706,9 +706,9 @@ static hipError_t launch_mcols_t(const McolsArgs& a, hipStream_t st) {
   const size_t lds = (size_t)kMcNW * 32 * 64 * 2 + (kMcWide ? 0 : (size_t)kMcNW * NB * 64 * 4);
   dim3 grid(kMcWide ? (a.d + 64 * kMcNW - 1) / (64 * kMcNW) : (a.d + 63) / 64, a.S);
   if (a.dh > 0)
-    hipLaunchKernelGGL((k_mfma_cols<NB, kMcNW, kMcU, true, kMcWide>), grid, dim3(kMcNW * 64), lds, st, a);
+    launch_k((k_mfma_cols<NB, kMcNW, kMcU, true, kMcWide>), grid, dim3(kMcNW * 64), lds, st, a);
   else
-    hipLaunchKernelGGL((k_mfma_cols<NB, kMcNW, kMcU, false, kMcWide>), grid, dim3(kMcNW * 64), lds, st, a);
+    launch_k((k_mfma_cols<NB, kMcNW, kMcU, false, kMcWide>), grid, dim3(kMcNW * 64), lds, st, a);
   return hipGetLastError();
 }
 
@@ -785,9 +785,9 @@ __global__ void __launch_bounds__(16 * NB) k_fc1_finish(Fc1FinishArgs a) {
 hipError_t launch_fc1_finish(int NB, const Fc1FinishArgs& a, hipStream_t st) {
   const int blocks = max(1, (a.list_max + 63) / 64);
   if (NB <= 16)
-    hipLaunchKernelGGL(k_fc1_finish<16>, dim3(blocks), dim3(16 * 16), 0, st, a);
+    launch_k(k_fc1_finish<16>, dim3(blocks), dim3(16 * 16), 0, st, a);
   else
-    hipLaunchKernelGGL(k_fc1_finish<32>, dim3(blocks), dim3(16 * 32), 0, st, a);
+    launch_k(k_fc1_finish<32>, dim3(blocks), dim3(16 * 32), 0, st, a);
   return hipGetLastError();
 }
 
@@ -806,7 +806,7 @@ __global__ void __launch_bounds__(256) k_cols_finish(ColsFinishArgs a) {
 
 hipError_t launch_cols_finish(const ColsFinishArgs& a, hipStream_t st) {
   const long quads = ((long)a.B * a.d / 4 + 255) / 256;
-  hipLaunchKernelGGL(k_cols_finish, dim3((unsigned)max(1L, quads)), dim3(256), 0, st, a);
+  launch_k(k_cols_finish, dim3((unsigned)max(1L, quads)), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
@@ -828,9 +828,9 @@ hipError_t launch_sum_cast(int NB, const float* P, int S, int nrows_pad, int row
                            hipStream_t st) {
   const int blocks = min((NB * ldc + 255) / 256, 4 * device_cu_count());
   if (NB <= 16)
-    hipLaunchKernelGGL(k_sum_cast<16>, dim3(blocks), dim3(256), 0, st, P, S, nrows_pad, row0, r, B, C, ldc);
+    launch_k(k_sum_cast<16>, dim3(blocks), dim3(256), 0, st, P, S, nrows_pad, row0, r, B, C, ldc);
   else
-    hipLaunchKernelGGL(k_sum_cast<32>, dim3(blocks), dim3(256), 0, st, P, S, nrows_pad, row0, r, B, C, ldc);
+    launch_k(k_sum_cast<32>, dim3(blocks), dim3(256), 0, st, P, S, nrows_pad, row0, r, B, C, ldc);
   return hipGetLastError();
 }
 
@@ -895,11 +895,11 @@ hipError_t launch_qkv_finish(int NB, int kvtype, const QkvFinishArgs& a, hipStre
   dim3 grid(a.H, 3);
   const size_t lds = (size_t)a.dh * (NB + 1) * sizeof(float);
   if (NB <= 16) {
-    if (kvtype == DV_F16) hipLaunchKernelGGL((k_qkv_finish<16, _Float16>), grid, dim3(1024), lds, st, a);
-    else hipLaunchKernelGGL((k_qkv_finish<16, float>), grid, dim3(1024), lds, st, a);
+    if (kvtype == DV_F16) launch_k((k_qkv_finish<16, _Float16>), grid, dim3(1024), lds, st, a);
+    else launch_k((k_qkv_finish<16, float>), grid, dim3(1024), lds, st, a);
   } else {
-    if (kvtype == DV_F16) hipLaunchKernelGGL((k_qkv_finish<32, _Float16>), grid, dim3(1024), lds, st, a);
-    else hipLaunchKernelGGL((k_qkv_finish<32, float>), grid, dim3(1024), lds, st, a);
+    if (kvtype == DV_F16) launch_k((k_qkv_finish<32, _Float16>), grid, dim3(1024), lds, st, a);
+    else launch_k((k_qkv_finish<32, float>), grid, dim3(1024), lds, st, a);
   }
   return hipGetLastError();
 }
@@ -957,7 +957,7 @@ __global__ void __launch_bounds__(256) k_attn_finish(AttnFinishArgs a) {
 
 hipError_t launch_attn_finish(int NB, const AttnFinishArgs& a, hipStream_t st) {
   dim3 grid((a.ldc + a.dh - 1) / a.dh, NB);
-  hipLaunchKernelGGL(k_attn_finish, grid, dim3(256), 0, st, a);
+  launch_k(k_attn_finish, grid, dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

@@ -4,9 +4,12 @@
 // argument structures and the host-side launchers.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
+
+#include <tuple>
 
 #include "dv.h"
 
@@ -298,6 +301,29 @@ int device_cu_count();   // cached per device
 void trace_reset();
 void trace_begin(const char* label, hipStream_t st);
 void trace_end(hipStream_t st);
+// Events for the next kernel of an armed launch (both NULL when none is armed): the
+// first kernel of the launch takes the start event, every kernel the end event.
+void trace_take(hipEvent_t* start, hipEvent_t* stop);
+
+// Every kernel goes through here. With events armed they are stamped by the kernel's
+// own dispatch (hipExtLaunchKernel: its start and end times), not by separate marker
+// commands around it, whose completion adds the queue's dispatch latency to the
+// interval. Errors are left for hipGetLastError, as with a <<<>>> launch.
+template <typename... P, typename... A>
+inline void launch_k(void (*kern)(P...), dim3 grid, dim3 block, size_t lds, hipStream_t st, A... args) {
+  static_assert(sizeof...(P) == sizeof...(A), "kernel argument count");
+  std::tuple<P...> vals(static_cast<P>(args)...);
+  void* argv[sizeof...(P) + 1];
+  std::apply([&argv](auto&... v) {
+    int i = 0;
+    ((argv[i++] = static_cast<void*>(&v)), ...);
+  }, vals);
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  trace_take(&e0, &e1);
+  const void* f = reinterpret_cast<const void*>(kern);
+  if (e1 != nullptr) (void)hipExtLaunchKernel(f, grid, block, argv, lds, st, e0, e1, 0);
+  else (void)hipLaunchKernel(f, grid, block, argv, lds, st);
+}
 
 #define DV_LAUNCH(label, stream, expr)              \
   do {                                              \

@@ -61,9 +61,9 @@ static hipError_t launch_fc1_t(const Fc1Args& a, hipStream_t st) {
   const hipError_t e = ensure_dyn_lds(kern, lds);
   if (e != hipSuccess) return e;
   if (a.g != nullptr)
-    hipLaunchKernelGGL((k_fc1<T, NW, U, KX, true>), dim3(blocks), dim3(NW * 64), lds, st, a);
+    launch_k((k_fc1<T, NW, U, KX, true>), dim3(blocks), dim3(NW * 64), lds, st, a);
   else
-    hipLaunchKernelGGL((k_fc1<T, NW, U, KX, false>), dim3(blocks), dim3(NW * 64), lds, st, a);
+    launch_k((k_fc1<T, NW, U, KX, false>), dim3(blocks), dim3(NW * 64), lds, st, a);
   return hipGetLastError();
 }
 

@@ -45,9 +45,9 @@ static hipError_t launch_pred_hidden_t(const PredHidArgs& a, hipStream_t st) {
   const hipError_t e = ensure_dyn_lds(kern, lds);
   if (e != hipSuccess) return e;
   if (a.g != nullptr)
-    hipLaunchKernelGGL((k_pred_hidden<T, NW, U, KX, true>), grid, dim3(NW * 64), lds, st, a);
+    launch_k((k_pred_hidden<T, NW, U, KX, true>), grid, dim3(NW * 64), lds, st, a);
   else
-    hipLaunchKernelGGL((k_pred_hidden<T, NW, U, KX, false>), grid, dim3(NW * 64), lds, st, a);
+    launch_k((k_pred_hidden<T, NW, U, KX, false>), grid, dim3(NW * 64), lds, st, a);
   return hipGetLastError();
 }
 
@@ -238,7 +238,7 @@ template <typename T, int NW, int G, int RU, int NR, bool EARLY>
 static hipError_t launch_scores_k(const PredScoreArgs& a, dim3 grid, size_t lds, hipStream_t st) {
   const hipError_t e = ensure_dyn_lds(reinterpret_cast<const void*>(k_pred_scores<T, NW, G, RU, NR, EARLY>), lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((k_pred_scores<T, NW, G, RU, NR, EARLY>), grid, dim3(NW * 64), lds, st, a);
+  launch_k((k_pred_scores<T, NW, G, RU, NR, EARLY>), grid, dim3(NW * 64), lds, st, a);
   return hipGetLastError();
 }
 
@@ -291,7 +291,7 @@ __global__ void __launch_bounds__(1024) k_select(const float* s, int n, int mode
 
 hipError_t launch_select(const float* scores, int B, int n, int mode, int k, float thresh,
                          int32_t* idx, int cap, int32_t* count, int32_t* idx2, hipStream_t st) {
-  hipLaunchKernelGGL(k_select, dim3(B), dim3(1024), 0, st, scores, n, mode, k, thresh, idx, cap, count, idx2);
+  launch_k(k_select, dim3(B), dim3(1024), 0, st, scores, n, mode, k, thresh, idx, cap, count, idx2);
   return hipGetLastError();
 }
 
@@ -316,7 +316,7 @@ __global__ void __launch_bounds__(1024) k_validate_sets(const int32_t* set, int 
 }
 
 hipError_t launch_validate_sets(const int32_t* set, int B, int n, int range, int32_t* bad, hipStream_t st) {
-  hipLaunchKernelGGL(k_validate_sets, dim3(1), dim3(1024), 0, st, set, B, n, range, bad);
+  launch_k(k_validate_sets, dim3(1), dim3(1024), 0, st, set, B, n, range, bad);
   return hipGetLastError();
 }
 

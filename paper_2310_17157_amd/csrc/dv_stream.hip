@@ -57,7 +57,7 @@ static hipError_t launch_stream_read(const void* buf, size_t n16, float* sink, h
   constexpr int NW = 16;
   const size_t want = (size_t)device_cu_count() * 2, need = (n16 / 64 + NW - 1) / NW;
   const int blocks = (int)(want < need ? want : (need > 0 ? need : 1));
-  hipLaunchKernelGGL((k_stream_read<NW, 4>), dim3(blocks), dim3(NW * 64), 0, st, reinterpret_cast<const u32x4*>(buf),
+  launch_k((k_stream_read<NW, 4>), dim3(blocks), dim3(NW * 64), 0, st, reinterpret_cast<const u32x4*>(buf),
                      n16, sink);
   return hipGetLastError();
 }
