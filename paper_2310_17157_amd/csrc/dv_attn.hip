@@ -148,7 +148,7 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   constexpr int SUB = NSTEP * NW * PPW;
   __shared__ float sm_m[NW], sm_l[NW];
   __shared__ float sm_o[NW][256];
-  const int j = blockIdx.y, c = blockIdx.x, b = blockIdx.z;
+  const int j = blockIdx.y, c = blockIdx.x, b = a.reorder ? a.seq_of[blockIdx.z] : (int)blockIdx.z;
   const int jb = b * a.n_heads + j;               // (sequence, selected head)
   const int head = min(max(a.heads[jb], 0), a.H - 1);
   const int t0 = c * a.chunk;

@@ -398,6 +398,10 @@ constexpr int kMaxBatch = 32;
 struct AttnArgs {
   int H, dh, cap, n_heads, n_split, chunk;
   int posb[kMaxBatch];              // row of the current token, per sequence
+  // reorder != 0: grid slot z (blockIdx.z) attends sequence seq_of[z] (a permutation of
+  // the batch), so that the host can choose which workgroups share a CU.
+  int seq_of[kMaxBatch];
+  int reorder;
   const float* q;                   // [B][n_heads][dh]
   const int32_t* heads;             // [B][n_heads]
   const void* K; const void* V;     // [B][H][cap][dh]
