@@ -354,14 +354,14 @@ hipError_t launch_attn(int kvtype, const AttnArgs& a, int B, hipStream_t st) {
 // a head missing many positions is not one workgroup's serial work. Nothing is read when
 // nothing is missing. The prologue's copy of this token's input and the valid marks are
 // read kFillPre per thread before any is used. Over 32 decode steps with about 59
-// missing rows each: 70 -> 56-58 us per fill with the slices, 54.5 us with both.
+// missing rows each: 70-71 us per fill with one workgroup per row block, 55-57 us.
 constexpr int kFillRows = 16, kFillSlices = 4, kFillPre = 8;
 
 template <typename T, typename KT, int RPW, int MT>
 __global__ void __launch_bounds__(256) k_kv_fill(KvFillArgs a) {
   constexpr int E = Chunk<T>::E;
   extern __shared__ int flist[];
-  __shared__ int fcnt;
+  __shared__ int wtot[4];
   const int nrb = (2 * a.dh + kFillRows - 1) / kFillRows;
   const int j = blockIdx.x / nrb, rb = blockIdx.x - j * nrb;
   const int head = min(max(a.heads[j], 0), a.H - 1);
@@ -379,19 +379,39 @@ __global__ void __launch_bounds__(256) k_kv_fill(KvFillArgs a) {
         if (i0 + 256 * k < n4) dst[i0 + 256 * k] = v[k];
     }
   }
-  if (threadIdx.x == 0) fcnt = 0;
-  __syncthreads();
+  // The head's missing positions below pos, in ascending order: every workgroup of the
+  // head builds the same list, since the slices split it by index. Each thread takes
+  // kFillPre consecutive positions; a workgroup-wide prefix sum of their counts places them.
   const uint8_t* vh = a.valid + (size_t)head * a.cap;
-  for (int t0 = threadIdx.x; t0 < a.pos; t0 += 256 * kFillPre) {
+  int m = 0;
+  for (int c0 = 0; c0 < a.pos; c0 += 256 * kFillPre) {
+    const int tb = c0 + (int)threadIdx.x * kFillPre;
     uint8_t mk[kFillPre];
 #pragma unroll
-    for (int k = 0; k < kFillPre; ++k) mk[k] = vh[min(t0 + 256 * k, a.pos - 1)];
+    for (int k = 0; k < kFillPre; ++k) mk[k] = vh[min(tb + k, a.pos - 1)];
+    int cnt = 0;
+#pragma unroll
+    for (int k = 0; k < kFillPre; ++k) cnt += (tb + k < a.pos && mk[k] == 0) ? 1 : 0;
+    int incl = cnt;                                   // inclusive scan within the wavefront
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int v = __shfl_up(incl, o, kWave);
+      if (lane >= o) incl += v;
+    }
+    if (lane == kWave - 1) wtot[wave] = incl;
+    __syncthreads();
+    int off = m + incl - cnt, tot = 0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      off += w < wave ? wtot[w] : 0;
+      tot += wtot[w];
+    }
 #pragma unroll
     for (int k = 0; k < kFillPre; ++k)
-      if (t0 + 256 * k < a.pos && mk[k] == 0) flist[atomicAdd(&fcnt, 1)] = t0 + 256 * k;
+      if (tb + k < a.pos && mk[k] == 0) flist[off++] = tb + k;
+    m += tot;
+    __syncthreads();                                  // wtot is rewritten by the next round
   }
-  __syncthreads();
-  const int m = fcnt;
   if (m == 0) return;
   const int nch = a.d / E, nit = (nch + 63) / 64;
   // this wavefront's rows (clamped into the block; duplicates are not written)

@@ -90,3 +90,45 @@ def test_kvfill_equals_a_cache_with_every_head_written():
         ref = Bd.dv_sparse_attn(attn, x, kv2, S.view(1, -1), scale)
         torch.cuda.synchronize()
         assert rel_l2(host(out)[0], host(ref)[0]) < REL_TOL, s
+
+
+@pytest.mark.parametrize("name,M", [("small_f16", 70), ("opt175b_b1", 150)])
+def test_kvfill_heads_missing_many_positions(name, M):
+    """Selected heads missing far more positions than one workgroup slice takes per
+    group (4 positions x 4 slices), some contiguous and some scattered: every slice
+    runs several groups, and the filled rows and the output match the oracle."""
+    cfg = get_config(name)
+    t = make_layer(cfg, 140, device="cuda", biases=True)
+    attn = Bd.Attn(t["Wq"], t["Wk"], t["Wv"], t["WoT"], cfg.H, t["bq"], t["bk"], t["bv"], t["bo"])
+    cap, d, H = cfg.kv_cap, cfg.d, cfg.H
+    pos = cap - 1
+    kv = Bd.KVCache(t["K"], t["V"], [pos])
+    Y = torch.zeros((cap, d), dtype=torch.float32, device="cuda")
+    Y[:pos] = torch.randn((pos, d), device="cuda")
+    rng = np.random.default_rng(141)
+    vh = np.ones((H, cap), dtype=np.uint8)
+    vh[:, pos:] = 0
+    vh[0, pos - M:pos] = 0                                       # a long contiguous gap
+    vh[1, rng.choice(pos, M, replace=False)] = 0                 # scattered
+    vh[2, rng.choice(pos, 5, replace=False)] = 0                 # a few
+    valid = torch.tensor(vh, device="cuda")
+    S = np.array(sorted({0, 1, 2} | set(rng.choice(np.arange(3, H), cfg.k_heads - 3, replace=False).tolist())),
+                 dtype=np.int32)
+    a = oracle_attn(t)
+    Ko, Vo = host(t["K"])[0].astype(np.float64), host(t["V"])[0].astype(np.float64)
+    Yo, vo = host(Y).astype(np.float64), vh.astype(bool)
+    scale = 1.0 / np.sqrt(cfg.dh)
+    x = torch.randn((1, d), device="cuda")
+    out = Bd.dv_sparse_attn_kvfill(attn, x, kv, Y, valid, torch.tensor(S, device="cuda"), scale)
+    torch.cuda.synchronize()
+    ref, Ko, Vo, Yo, vo = O.mha_sparse_kvfill(host(x)[0], a, Ko, Vo, Yo, vo, pos, S, scale)
+    assert rel_l2(host(out)[0], ref) < REL_TOL
+    assert np.array_equal(host(valid).astype(bool), vo)
+    Kg, Vg = host(t["K"])[0], host(t["V"])[0]
+    for h in S:
+        assert rel_l2(Kg[h, :pos + 1].astype(np.float64), Ko[h, :pos + 1]) < REL_TOL, h
+        assert rel_l2(Vg[h, :pos + 1].astype(np.float64), Vo[h, :pos + 1]) < REL_TOL, h
+    for h in (0, 1, 2):   # the filled rows themselves, not only the whole head
+        miss = np.flatnonzero(vh[h, :pos] == 0)
+        assert rel_l2(Kg[h, miss].astype(np.float64), Ko[h, miss]) < REL_TOL, h
+        assert rel_l2(Vg[h, miss].astype(np.float64), Vo[h, miss]) < REL_TOL, h
