@@ -344,39 +344,51 @@ hipError_t launch_attn(int kvtype, const AttnArgs& a, int B, hipStream_t st) {
 }
 
 // ------------------------------------------------------------ missing keys and values
-// One workgroup per (selected head, block of kFillRows rows of [W^K_h; W^V_h], group
-// slice). It lists the head's missing positions (valid == 0 below pos); each wavefront
-// then takes RPW of the rows at once and, for groups of MT missing positions, walks the
-// rows in 16-byte chunks: the RPW weight chunks and the MT matching slices of the kept
-// inputs (L2 hits: every workgroup of the head reads the same few rows of Y) are loaded
+// One workgroup of 4 wavefronts per (selected head, block of kFillRows rows of
+// [W^K_h; W^V_h], group slice). It lists the head's missing positions (valid == 0 below
+// pos); wavefront w then takes RPW of the rows (w mod kFillRows / RPW) over one of
+// kFillCols parts of the columns and, for groups of MT missing positions, walks them in
+// 16-byte chunks: the RPW weight chunks and the MT matching slices of the kept inputs
+// (L2 hits: every workgroup of the head reads the same few rows of Y) are loaded
 // together, two steps in flight, with indices clamped so that no load is predicated.
-// The groups of a head are dealt round-robin to kFillSlices workgroups per row block, so
-// a head missing many positions is not one workgroup's serial work. Nothing is read when
-// nothing is missing. The prologue's copy of this token's input and the valid marks are
-// read kFillPre per thread before any is used. Over 32 decode steps with about 59
-// missing rows each: 70-71 us per fill with one workgroup per row block, 55-57 us.
-constexpr int kFillRows = 16, kFillSlices = 4, kFillPre = 8;
+// The other parts' sums are added to the first's through LDS, in part order. The
+// groups of a head are dealt round-robin to kFillSlices workgroups per row block.
+// Nothing is read when nothing is missing.
+// A fill has few heads with missing rows (about 21 at the benchmark's 59 rows per
+// token), so few wavefronts have work: the column parts multiply them and the bytes in
+// flight, the slices keep a head missing many positions from being serial work, and
+// the prologue's copy of this token's input and the valid marks are read kFillPre per
+// thread before any is used. Over 32 decode steps with about 59 missing rows each:
+// 70-71 us per fill with 16 rows over all columns per workgroup and no slices, 55-57 us
+// with the slices and that prologue, 51 us with two column parts (four: 64 us, the
+// listing repeated by four times the workgroups).
+constexpr int kFillRows = 8, kFillCols = 2, kFillSlices = 4, kFillPre = 8, kFillNT = 256;
 
 template <typename T, typename KT, int RPW, int MT>
-__global__ void __launch_bounds__(256) k_kv_fill(KvFillArgs a) {
+__global__ void __launch_bounds__(kFillNT, 3) k_kv_fill(KvFillArgs a) {
   constexpr int E = Chunk<T>::E;
+  constexpr int NW = kFillNT / kWave;
+  constexpr int NRW = kFillRows / RPW;               // wavefronts per column part
+  static_assert(NW == kFillCols * NRW, "the row block's wavefronts cover its column parts");
   extern __shared__ int flist[];
-  __shared__ int wtot[4];
+  __shared__ int wtot[NW];
+  __shared__ float part[kFillCols - 1][NRW][RPW][MT];
   const int nrb = (2 * a.dh + kFillRows - 1) / kFillRows;
   const int j = blockIdx.x / nrb, rb = blockIdx.x - j * nrb;
   const int head = min(max(a.heads[j], 0), a.H - 1);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int rw = wave % NRW, cp = wave / NRW;
   if (blockIdx.x == 0 && blockIdx.y == 0) {   // keep this token's input: Y[pos] = x
     const int n4 = a.d >> 2;                    // (x, Y 16-byte aligned, d % 4 == 0)
     const f32x4* src = reinterpret_cast<const f32x4*>(a.x);
     f32x4* dst = reinterpret_cast<f32x4*>(a.Y + (size_t)a.pos * a.d);
-    for (int i0 = threadIdx.x; i0 < n4; i0 += 256 * kFillPre) {
+    for (int i0 = threadIdx.x; i0 < n4; i0 += kFillNT * kFillPre) {
       f32x4 v[kFillPre];
 #pragma unroll
-      for (int k = 0; k < kFillPre; ++k) v[k] = src[min(i0 + 256 * k, n4 - 1)];
+      for (int k = 0; k < kFillPre; ++k) v[k] = src[min(i0 + kFillNT * k, n4 - 1)];
 #pragma unroll
       for (int k = 0; k < kFillPre; ++k)
-        if (i0 + 256 * k < n4) dst[i0 + 256 * k] = v[k];
+        if (i0 + kFillNT * k < n4) dst[i0 + kFillNT * k] = v[k];
     }
   }
   // The head's missing positions below pos, in ascending order: every workgroup of the
@@ -384,7 +396,7 @@ __global__ void __launch_bounds__(256) k_kv_fill(KvFillArgs a) {
   // kFillPre consecutive positions; a workgroup-wide prefix sum of their counts places them.
   const uint8_t* vh = a.valid + (size_t)head * a.cap;
   int m = 0;
-  for (int c0 = 0; c0 < a.pos; c0 += 256 * kFillPre) {
+  for (int c0 = 0; c0 < a.pos; c0 += kFillNT * kFillPre) {
     const int tb = c0 + (int)threadIdx.x * kFillPre;
     uint8_t mk[kFillPre];
 #pragma unroll
@@ -402,7 +414,7 @@ __global__ void __launch_bounds__(256) k_kv_fill(KvFillArgs a) {
     __syncthreads();
     int off = m + incl - cnt, tot = 0;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
+    for (int w = 0; w < NW; ++w) {
       off += w < wave ? wtot[w] : 0;
       tot += wtot[w];
     }
@@ -414,8 +426,9 @@ __global__ void __launch_bounds__(256) k_kv_fill(KvFillArgs a) {
   }
   if (m == 0) return;
   const int nch = a.d / E, nit = (nch + 63) / 64;
+  const int it_b = (int)((long)cp * nit / kFillCols), it_e = (int)((long)(cp + 1) * nit / kFillCols);
   // this wavefront's rows (clamped into the block; duplicates are not written)
-  const int r0 = rb * kFillRows + wave * RPW, rend = min(2 * a.dh, (rb + 1) * kFillRows);
+  const int r0 = rb * kFillRows + rw * RPW, rend = min(2 * a.dh, (rb + 1) * kFillRows);
   const T* W[RPW];
 #pragma unroll
   for (int r = 0; r < RPW; ++r) {
@@ -458,32 +471,49 @@ __global__ void __launch_bounds__(256) k_kv_fill(KvFillArgs a) {
       }
     };
     // two steps in flight: the next step's loads go out before this step is used
-    Step sa, sb;
-    load(sa, 0);
-    for (int it = 0; it < nit;) {
-      load(sb, min(it + 1, nit - 1));
-      use(sa, it);
-      if (++it >= nit) break;
-      load(sa, min(it + 1, nit - 1));
-      use(sb, it);
-      ++it;
+    if (it_b < it_e) {
+      Step sa, sb;
+      load(sa, it_b);
+      for (int it = it_b; it < it_e;) {
+        load(sb, min(it + 1, it_e - 1));
+        use(sa, it);
+        if (++it >= it_e) break;
+        load(sa, min(it + 1, it_e - 1));
+        use(sb, it);
+        ++it;
+      }
     }
+    // every part reduces its lanes before the barrier (after it, the first part's
+    // reductions would lengthen every group's tail: 53.6-55.1 against 50.9-51.4 us per fill)
 #pragma unroll
-    for (int r = 0; r < RPW; ++r) {
-      const int rr = r0 + r;
-      const bool isv = rr >= a.dh;
-      const int tr = isv ? rr - a.dh : rr;
-      const float* bias = isv ? a.bv : a.bk;
-      const float bb = (bias != nullptr && rr < rend) ? bias[(size_t)head * a.dh + tr] : 0.f;
+    for (int r = 0; r < RPW; ++r)
 #pragma unroll
       for (int u = 0; u < MT; ++u) {
-        const float v = wave_sum(acc[r][u]);
-        if (lane == 0 && rr < rend && t0 + u < m) {
-          KT* C = static_cast<KT*>(isv ? a.V : a.K);
-          C[((size_t)head * a.cap + flist[t0 + u]) * a.dh + tr] = (KT)(v + bb);
+        acc[r][u] = wave_sum(acc[r][u]);
+        if (cp > 0 && lane == 0) part[cp - 1][rw][r][u] = acc[r][u];
+      }
+    __syncthreads();
+    if (cp == 0) {
+#pragma unroll
+      for (int r = 0; r < RPW; ++r) {
+        const int rr = r0 + r;
+        const bool isv = rr >= a.dh;
+        const int tr = isv ? rr - a.dh : rr;
+        const float* bias = isv ? a.bv : a.bk;
+        const float bb = (bias != nullptr && rr < rend) ? bias[(size_t)head * a.dh + tr] : 0.f;
+#pragma unroll
+        for (int u = 0; u < MT; ++u) {
+          float v = acc[r][u];
+#pragma unroll
+          for (int q = 0; q < kFillCols - 1; ++q) v += part[q][rw][r][u];
+          if (lane == 0 && rr < rend && t0 + u < m) {
+            KT* C = static_cast<KT*>(isv ? a.V : a.K);
+            C[((size_t)head * a.cap + flist[t0 + u]) * a.dh + tr] = (KT)(v + bb);
+          }
         }
       }
     }
+    __syncthreads();                                  // part is rewritten by the next group
   }
 }
 
@@ -491,10 +521,10 @@ template <typename T, typename KT>
 static hipError_t launch_kv_fill_t(const KvFillArgs& a, hipStream_t st) {
   const int nrb = (2 * a.dh + kFillRows - 1) / kFillRows;
   const size_t lds = (size_t)max(a.pos, 1) * sizeof(int);
-  constexpr int RPW = kFillRows / 4, MT = 4;
+  constexpr int RPW = kFillRows / (kFillNT / kWave / kFillCols), MT = 4;
   const hipError_t e = ensure_dyn_lds(reinterpret_cast<const void*>(k_kv_fill<T, KT, RPW, MT>), lds);
   if (e != hipSuccess) return e;
-  launch_k((k_kv_fill<T, KT, RPW, MT>), dim3(max(1, a.n_heads) * nrb, kFillSlices), dim3(256), lds, st, a);
+  launch_k((k_kv_fill<T, KT, RPW, MT>), dim3(max(1, a.n_heads) * nrb, kFillSlices), dim3(kFillNT), lds, st, a);
   return hipGetLastError();
 }
 
