@@ -179,13 +179,15 @@ static dv_status battn_run(const dv_attn* a, const dv_kv* kv, const BAttn& o, in
   // into a matrix the QKV finisher clears; otherwise a launch combines the chunks.
   const bool direct = at.n_split == 1;
   if (direct && B > 1) {
-    // Balance the CUs. Here every (sequence, head) workgroup is resident from the start,
-    // workgroup w runs on XCD w mod 8 and the CUs of an XCD take its workgroups in turn,
-    // so a CU's share is the slots z0 + P j (P = CUs / heads per sequence): the
-    // workgroups of one round of one per CU. Its time is the sum of their sequences'
-    // lengths, which differ up to 4x here. Slots get the sequences by decreasing length,
-    // every other row of P slots reversed, so a CU's rows alternate long and short.
-    // Batch 32, lengths U[512, 2048]: 115 -> 107 us (104 us with equal lengths).
+    // Balance the CUs. At up to 4 (sequence, head) workgroups per CU (batch 32 with 32
+    // heads each: all resident from the start) workgroup w runs on XCD w mod 8 and the
+    // CUs of an XCD take its workgroups in turn, so a CU's share is the slots z0 + P j
+    // (P = CUs / heads per sequence: the workgroups of one round of one per CU) and its
+    // time the sum of their sequences' lengths, which differ up to 4x. Slots get the
+    // sequences by decreasing length, every other row of P slots reversed, so a CU's
+    // rows alternate long and short; with more workgroups than fit, dispatch then starts
+    // the long ones first. Batch 32, lengths U[512, 2048]: 115 -> 107 us (104 us with
+    // equal lengths).
     int idx[kMaxBatch];
     for (int b = 0; b < B; ++b) idx[b] = b;
     std::stable_sort(idx, idx + B, [&](int x, int y) { return kv->pos[x] > kv->pos[y]; });
