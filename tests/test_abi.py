@@ -210,3 +210,55 @@ def test_noalloc_block_rejects_what_its_scratch_cannot_hold(lib):
     assert st == B.DV_ERR_WORKSPACE
     hdr = open(HEADER).read()
     assert f"#define DV_STATIC_SCRATCH_BYTES (16u << 20)" in hdr and B.STATIC_SCRATCH_BYTES == 16 << 20
+
+
+C_PROGRAM = r"""
+#include <stdint.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "dv.h"
+
+/* A C caller of the library: the header compiles as C99 and the entry points link and
+ * reject bad arguments on the host (no device is touched). */
+int main(void) {
+  dv_mlp m;
+  float *x = (float *)(uintptr_t)0x10000000u;
+  int32_t *idx = (int32_t *)(uintptr_t)0x10000000u;
+  void *ws = (void *)(uintptr_t)0x10000000u;
+  size_t need;
+  if (dv_abi_version() != 1) return 1;
+  if (strcmp(dv_status_string(DV_OK), dv_status_string(DV_ERR_NULL)) == 0) return 2;
+  memset(&m, 0, sizeof m);
+  m.d = 64;
+  m.n = 128;
+  m.wtype = DV_F16;
+  m.act = DV_ACT_RELU;
+  m.W1T = x;
+  m.W2T = x;
+  if (dv_sparse_mlp(NULL, x, 1, idx, 8, 0, 0, x, ws, 1u << 30, 0, NULL) != DV_ERR_NULL) return 3;
+  if (dv_sparse_mlp(&m, x, 1, idx, 129, 0, 0, x, ws, 1u << 30, 0, NULL) != DV_ERR_SHAPE) return 4;
+  need = dv_sparse_mlp_workspace_bytes(&m, 1, 8, 0);
+  if (need == 0 || need % 256 != 0) return 5;
+  if (dv_sparse_mlp(&m, x, 1, idx, 8, 0, 0, x, ws, need - 1, 0, NULL) != DV_ERR_WORKSPACE) return 6;
+  printf("c caller ok\n");
+  return 0;
+}
+"""
+
+
+def test_header_compiles_as_c_and_links(tmp_path):
+    """include/dv.h is a C header: a C99 program (-Wall -Wextra -Werror -pedantic) compiles
+    against it, links the library and gets the documented host-side statuses."""
+    src = tmp_path / "caller.c"
+    exe = tmp_path / "caller"
+    src.write_text(C_PROGRAM)
+    libdir = os.path.dirname(B.lib_path())
+    libname = os.path.basename(B.lib_path())
+    cc = subprocess.run(["gcc", "-std=c99", "-Wall", "-Wextra", "-Werror", "-pedantic", "-I",
+                         os.path.join(ROOT, "include"), str(src), "-o", str(exe), os.path.join(libdir, libname),
+                         "-Wl,-rpath," + libdir], capture_output=True, text=True)
+    assert cc.returncode == 0, cc.stderr
+    run = subprocess.run([str(exe)], capture_output=True, text=True, timeout=60)
+    assert run.returncode == 0, (run.returncode, run.stdout, run.stderr)
+    assert "c caller ok" in run.stdout
