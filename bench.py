@@ -657,7 +657,7 @@ def kvfill_steps(cfg, t, stream, scale, T=32):
     attn = Bd.Attn(t["Wq"], t["Wk"], t["Wv"], t["WoT"], H)
     p0 = cap - T
     kv = Bd.KVCache(t["K"], t["V"], [p0])
-    Y = torch.randn((cap, d), dtype=torch.float32, device="cuda")
+    Y = torch.randn((cap, d), device="cuda").to(t["K"].dtype)   # kept inputs, in the cache's type
     valid = torch.zeros((H, cap), dtype=torch.uint8, device="cuda")
     valid[:, :p0] = 1
     rng = np.random.default_rng(17)

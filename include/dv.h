@@ -262,7 +262,9 @@ dv_status dv_sparse_attn(const dv_attn *a, const float *x, int32_t B, const dv_k
  * every token is kept, and the missing rows of the selected heads are computed from it
  * (K[h][t] = Y[t] W^K_h + bk_h, likewise V) before those heads attend.
  *   x      [d] fp32 device: this token's attention input (normalised, as for dv_sparse_attn).
- *   Y      [cap][d] fp32 device, in/out: the kept inputs; the call writes Y[pos] = x.
+ *   Y      [cap][d] device, in/out, in the cache's type (kv->ktype: fp16 or fp32, like
+ *          the keys and values computed from it): the kept inputs; the call writes
+ *          Y[pos] = x, rounded to nearest even for fp16. 16-byte aligned.
  *   valid  [H][cap] uint8 device, in/out: 1 where row t of head h holds token t's key
  *          and value. On return valid[h][0..pos] = 1 for every selected head and
  *          valid[h][pos] = 0 for the others; rows above pos are not touched. A sequence
@@ -272,7 +274,7 @@ dv_status dv_sparse_attn(const dv_attn *a, const float *x, int32_t B, const dv_k
  * Cost: one launch more than dv_sparse_attn; it reads no weights when no selected head
  * misses a row, otherwise each selected head's W^K and W^V rows once per 4 missing
  * positions. Limits: pos <= 32768 (else DV_ERR_UNSUPPORTED). */
-dv_status dv_sparse_attn_kvfill(const dv_attn *a, const float *x, const dv_kv *kv, float *Y, uint8_t *valid,
+dv_status dv_sparse_attn_kvfill(const dv_attn *a, const float *x, const dv_kv *kv, void *Y, uint8_t *valid,
                                 const int32_t *heads, int32_t n_heads, float scale, float *out, void *ws,
                                 size_t ws_bytes, uint32_t flags, void *stream);
 

@@ -55,7 +55,9 @@ Readings where the paper is silent or loose (each is also listed in the design n
       normalised input LN1^l(y_l); layer 0's sets from its predictors on LN1^0(y_0).
   R18 Missing keys and values (Section 4.2): the kept per-token input is the
       attention block's normalised input (what the keys and values are computed
-      from); a head selected now gets its missing rows from it before it attends.
+      from), stored in the cache's type (an fp16 cache keeps it rounded to the
+      nearest half, like the keys and values themselves); a head selected now gets
+      its missing rows from it before it attends.
 
 Parity pins: every function here is checked in tests/test_oracle_*.py against
 something other than itself (closed forms, brute force on tiny shapes, invariants,
@@ -288,7 +290,7 @@ def mha_sparse(y, attn: Dict, K, V, pos: int, S_A, scale: float
     return out, K_new, V_new, heads
 
 
-def mha_sparse_kvfill(y, attn: Dict, K, V, Y, valid, pos: int, S_A, scale: float):
+def mha_sparse_kvfill(y, attn: Dict, K, V, Y, valid, pos: int, S_A, scale: float, y_keep=None):
     """Sparsified MHA for one token with the missing-KV rule of Section 4.2 ("Approach").
 
     Keys and values are computed only for the selected heads, so a head that was not
@@ -298,6 +300,9 @@ def mha_sparse_kvfill(y, attn: Dict, K, V, Y, valid, pos: int, S_A, scale: float
     before the head attends, and marked present. valid[h, t] is True where row t of
     head h holds that token's key and value; after the call it is True for every row
     0..pos of the selected heads and False at pos for the others.
+    y_keep: the storage type of the kept inputs (reading R18: the cache's type); None
+    keeps y exactly, np.float16 keeps y rounded to the nearest half (ties to even), as
+    an fp16 store of it holds.
     Y: [cap, d]; valid: [H, cap] bool (neither is modified; copies are returned).
     Returns (out [d], K_new, V_new, Y_new, valid_new).
     """
@@ -307,7 +312,7 @@ def mha_sparse_kvfill(y, attn: Dict, K, V, Y, valid, pos: int, S_A, scale: float
     V_fill = _f64(V).copy()
     Y_new = _f64(Y).copy()
     valid_new = np.asarray(valid, dtype=bool).copy()
-    Y_new[pos] = y
+    Y_new[pos] = y if y_keep is None else y.astype(y_keep).astype(np.float64)
     for i in S_A:
         i = int(i)
         for t in range(pos):

@@ -471,12 +471,13 @@ def dv_sparse_mlp_q4(mlp: MLPQ4, x, idx, out=None, ws=None, flags=0, stream=None
 def dv_sparse_attn_kvfill(attn: Attn, x, kv: KVCache, Y, valid, heads, scale, out=None, ws=None, flags=0,
                           stream=None):
     """dv_sparse_attn for one sequence with the missing-KV rule of Section 4.2: Y [cap][d]
-    fp32 keeps every token's attention input, valid [H][cap] uint8 marks the cache rows
-    that hold their token's key and value (both updated in place)."""
+    keeps every token's attention input in the cache's dtype (fp16 or fp32, like K and
+    V), valid [H][cap] uint8 marks the cache rows that hold their token's key and value
+    (both updated in place)."""
     lib = load()
     ca, ck = attn.c(), kv.c()
     _tensor("x", x, _F32, 2, (1, ca.d), dev=False)
-    _tensor("Y", Y, _F32, 2, (ck.cap, ca.d), dev=False)
+    _tensor("Y", Y, (kv.K.dtype,), 2, (ck.cap, ca.d), dev=False)
     _tensor("valid", valid, (torch.uint8,), 2, (ca.H, ck.cap), dev=False)
     _tensor("heads", heads, _I32, dev=False)
     n_heads = heads.shape[-1]

@@ -413,7 +413,7 @@ extern "C" dv_status dv_sparse_mlp_q4(const dv_mlp_q4* m, const float* x, const 
 // ------------------------------------------- sparse attention, missing keys and values
 static constexpr int kMaxFillPos = 32768;   // the fill launch lists missing positions in LDS
 
-extern "C" dv_status dv_sparse_attn_kvfill(const dv_attn* a, const float* x, const dv_kv* kv, float* Y,
+extern "C" dv_status dv_sparse_attn_kvfill(const dv_attn* a, const float* x, const dv_kv* kv, void* Y,
                                            uint8_t* valid, const int32_t* heads, int32_t n_heads, float scale,
                                            float* out, void* ws, size_t ws_bytes, uint32_t flags, void* stream) {
   trace_reset();
@@ -444,9 +444,8 @@ extern "C" dv_status dv_sparse_attn_kvfill(const dv_attn* a, const float* x, con
   f.Wk = a->Wk; f.Wv = a->Wv; f.bk = a->bk; f.bv = a->bv; f.K = kv->K; f.V = kv->V;
   if (n_heads > 0) {
     DV_LAUNCH("kv_fill", hs, launch_kv_fill(a->wtype, kv->ktype, f, hs));
-  } else if (hipMemcpyAsync(Y + (size_t)pos * a->d, x, (size_t)a->d * sizeof(float), hipMemcpyDeviceToDevice,
-                            hs) != hipSuccess) {
-    return DV_ERR_HIP;   // (no head selected: nothing to compute, the input is still kept)
+  } else {   // no head selected: nothing to compute, the input is still kept
+    DV_LAUNCH("kv_keep", hs, launch_keep_input(kv->ktype, f, hs));
   }
   QkvArgs q{};
   q.d = a->d; q.H = a->H; q.dh = a->dh; q.cap = kv->cap; q.pos = pos; q.n_heads = n_heads;

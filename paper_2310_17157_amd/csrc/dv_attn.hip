@@ -364,6 +364,42 @@ hipError_t launch_attn(int kvtype, const AttnArgs& a, int B, hipStream_t st) {
 // listing repeated by four times the workgroups).
 constexpr int kFillRows = 8, kFillCols = 2, kFillSlices = 4, kFillPre = 8, kFillNT = 256;
 
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+
+// The kept inputs are stored in the cache's type (fp16 or fp32, like the keys and
+// values computed from them): four inputs converted with round-to-nearest-even.
+__device__ __forceinline__ void keep4(float* dst, f32x4 v) { *reinterpret_cast<f32x4*>(dst) = v; }
+__device__ __forceinline__ void keep4(_Float16* dst, f32x4 v) {
+  *reinterpret_cast<f16x4*>(dst) = f16x4{(_Float16)v[0], (_Float16)v[1], (_Float16)v[2], (_Float16)v[3]};
+}
+
+// The kept-input slice that meets one 16-byte weight chunk of E elements: 8, 16 or 32
+// bytes of one position's row, in the cache's type.
+template <typename KT, int E> struct Kept;
+template <> struct Kept<float, 8> {
+  f32x4 v[2];
+  __device__ __forceinline__ void load(const float* p) {
+    v[0] = *reinterpret_cast<const f32x4*>(p);
+    v[1] = *reinterpret_cast<const f32x4*>(p + 4);
+  }
+  __device__ __forceinline__ float at(int e) const { return v[e >> 2][e & 3]; }
+};
+template <> struct Kept<float, 4> {
+  f32x4 v;
+  __device__ __forceinline__ void load(const float* p) { v = *reinterpret_cast<const f32x4*>(p); }
+  __device__ __forceinline__ float at(int e) const { return v[e]; }
+};
+template <> struct Kept<_Float16, 8> {
+  f16x8 v;
+  __device__ __forceinline__ void load(const _Float16* p) { v = *reinterpret_cast<const f16x8*>(p); }
+  __device__ __forceinline__ float at(int e) const { return (float)v[e]; }
+};
+template <> struct Kept<_Float16, 4> {
+  f16x4 v;
+  __device__ __forceinline__ void load(const _Float16* p) { v = *reinterpret_cast<const f16x4*>(p); }
+  __device__ __forceinline__ float at(int e) const { return (float)v[e]; }
+};
+
 template <typename T, typename KT, int RPW, int MT>
 __global__ void __launch_bounds__(kFillNT, 3) k_kv_fill(KvFillArgs a) {
   constexpr int E = Chunk<T>::E;
@@ -381,14 +417,14 @@ __global__ void __launch_bounds__(kFillNT, 3) k_kv_fill(KvFillArgs a) {
   if (blockIdx.x == 0 && blockIdx.y == 0) {   // keep this token's input: Y[pos] = x
     const int n4 = a.d >> 2;                    // (x, Y 16-byte aligned, d % 4 == 0)
     const f32x4* src = reinterpret_cast<const f32x4*>(a.x);
-    f32x4* dst = reinterpret_cast<f32x4*>(a.Y + (size_t)a.pos * a.d);
+    KT* dst = static_cast<KT*>(a.Y) + (size_t)a.pos * a.d;
     for (int i0 = threadIdx.x; i0 < n4; i0 += kFillNT * kFillPre) {
       f32x4 v[kFillPre];
 #pragma unroll
       for (int k = 0; k < kFillPre; ++k) v[k] = src[min(i0 + kFillNT * k, n4 - 1)];
 #pragma unroll
       for (int k = 0; k < kFillPre; ++k)
-        if (i0 + kFillNT * k < n4) dst[i0 + kFillNT * k] = v[k];
+        if (i0 + kFillNT * k < n4) keep4(dst + 4 * (i0 + kFillNT * k), v[k]);
     }
   }
   // The head's missing positions below pos, in ascending order: every workgroup of the
@@ -437,9 +473,9 @@ __global__ void __launch_bounds__(kFillNT, 3) k_kv_fill(KvFillArgs a) {
     W[r] = static_cast<const T*>(isv ? a.Wv : a.Wk) + ((size_t)head * a.dh + (isv ? rr - a.dh : rr)) * a.d;
   }
   for (int t0 = (int)blockIdx.y * MT; t0 < m; t0 += MT * (int)gridDim.y) {
-    const float* Yp[MT];
+    const KT* Yp[MT];
 #pragma unroll
-    for (int u = 0; u < MT; ++u) Yp[u] = a.Y + (size_t)flist[min(t0 + u, m - 1)] * a.d;
+    for (int u = 0; u < MT; ++u) Yp[u] = static_cast<const KT*>(a.Y) + (size_t)flist[min(t0 + u, m - 1)] * a.d;
     float acc[RPW][MT];
 #pragma unroll
     for (int r = 0; r < RPW; ++r)
@@ -447,16 +483,14 @@ __global__ void __launch_bounds__(kFillNT, 3) k_kv_fill(KvFillArgs a) {
       for (int u = 0; u < MT; ++u) acc[r][u] = 0.f;
     struct Step {
       u32x4 w[RPW];
-      f32x4 y[MT][E / 4];
+      Kept<KT, E> y[MT];
     };
     auto load = [&](Step& st, int it) {
       const int c = min(it * 64 + lane, nch - 1);
 #pragma unroll
       for (int r = 0; r < RPW; ++r) st.w[r] = ld_stream(W[r] + (size_t)c * E);
 #pragma unroll
-      for (int u = 0; u < MT; ++u)
-#pragma unroll
-        for (int q = 0; q < E / 4; ++q) st.y[u][q] = *reinterpret_cast<const f32x4*>(Yp[u] + (size_t)c * E + 4 * q);
+      for (int u = 0; u < MT; ++u) st.y[u].load(Yp[u] + (size_t)c * E);
     };
     auto use = [&](const Step& st, int it) {
       if (it * 64 + lane >= nch) return;
@@ -467,7 +501,7 @@ __global__ void __launch_bounds__(kFillNT, 3) k_kv_fill(KvFillArgs a) {
 #pragma unroll
         for (int u = 0; u < MT; ++u)
 #pragma unroll
-          for (int e = 0; e < E; ++e) acc[r][u] = fmaf(wv[e], st.y[u][e >> 2][e & 3], acc[r][u]);
+          for (int e = 0; e < E; ++e) acc[r][u] = fmaf(wv[e], st.y[u].at(e), acc[r][u]);
       }
     };
     // two steps in flight: the next step's loads go out before this step is used
@@ -532,6 +566,21 @@ hipError_t launch_kv_fill(int wtype, int kvtype, const KvFillArgs& a, hipStream_
   if (wtype == DV_F16)
     return kvtype == DV_F16 ? launch_kv_fill_t<_Float16, _Float16>(a, st) : launch_kv_fill_t<_Float16, float>(a, st);
   return kvtype == DV_F16 ? launch_kv_fill_t<float, _Float16>(a, st) : launch_kv_fill_t<float, float>(a, st);
+}
+
+template <typename KT>
+__global__ void __launch_bounds__(256) k_keep_input(const float* __restrict__ x, KT* __restrict__ Y, int d) {
+  const int i = ((int)blockIdx.x * 256 + (int)threadIdx.x) * 4;
+  if (i < d) keep4(Y + i, *reinterpret_cast<const f32x4*>(x + i));
+}
+
+hipError_t launch_keep_input(int kvtype, const KvFillArgs& a, hipStream_t st) {
+  const dim3 grid((a.d / 4 + 255) / 256);
+  if (kvtype == DV_F16)
+    launch_k(k_keep_input<_Float16>, grid, dim3(256), 0, st, a.x, static_cast<_Float16*>(a.Y) + (size_t)a.pos * a.d, a.d);
+  else
+    launch_k(k_keep_input<float>, grid, dim3(256), 0, st, a.x, static_cast<float*>(a.Y) + (size_t)a.pos * a.d, a.d);
+  return hipGetLastError();
 }
 
 }  // namespace dv

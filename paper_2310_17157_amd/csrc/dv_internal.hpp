@@ -422,13 +422,15 @@ hipError_t launch_attn(int kvtype, const AttnArgs& a, int B, hipStream_t st);
 struct KvFillArgs {
   int d, H, dh, cap, pos, n_heads;
   const float* x;                   // [d] this token's attention input
-  float* Y;                         // [cap][d] kept attention inputs
+  void* Y;                          // [cap][d] kept attention inputs, in the cache's type
   const uint8_t* valid;             // [H][cap]
   const int32_t* heads;             // [n_heads]
   const void* Wk; const void* Wv; const float* bk; const float* bv;
   void* K; void* V;                 // [H][cap][dh]
 };
 hipError_t launch_kv_fill(int wtype, int kvtype, const KvFillArgs& a, hipStream_t st);
+// Y[pos] = x in the cache's type alone (no head selected, so no fill runs).
+hipError_t launch_keep_input(int kvtype, const KvFillArgs& a, hipStream_t st);
 
 // Gathered row-axpy: out = resid + bias + sum_rows coef[row] * M[rowidx(row)], tiled by
 // 128-byte column tiles; every workgroup sums all selected rows of its tile.

@@ -2,7 +2,9 @@
 decode steps with changing head sets: each step's output against the fp64 oracle
 (oracle.dejavu.mha_sparse_kvfill, run step by step on its own state), the validity
 marks bit for bit, the filled cache rows of the selected heads, and the outputs of a
-run whose cache holds every head's key and value at every token."""
+run whose cache holds every head's key and value at every token. The kept inputs Y are
+stored in the cache's type (reading R18): fp16 caches keep them rounded to nearest even,
+which the oracle models with its y_keep argument."""
 import numpy as np
 import pytest
 import torch
@@ -13,6 +15,11 @@ from synth import get_config, make_layer
 from tests.gpu_util import REL_TOL, host, oracle_attn, rel_l2
 
 pytestmark = pytest.mark.gpu
+
+
+def _keep(Y):
+    """The oracle's storage type for the kept inputs: that of the GPU's Y."""
+    return np.float16 if Y.dtype == torch.float16 else None
 
 
 def _head_schedule(rng, H, k, T, starve=None):
@@ -34,7 +41,7 @@ def test_kvfill_decode_steps_against_oracle(name, T, empty_step):
     cap, d, H = cfg.kv_cap, cfg.d, cfg.H
     p0 = cap - T                                  # the prompt filled rows 0..p0-1 of every head
     kv = Bd.KVCache(t["K"], t["V"], [p0])
-    Y = torch.zeros((cap, d), dtype=torch.float32, device="cuda")
+    Y = torch.zeros((cap, d), dtype=t["K"].dtype, device="cuda")
     Y[:p0] = torch.randn((p0, d), device="cuda")
     valid = torch.zeros((H, cap), dtype=torch.uint8, device="cuda")
     valid[:, :p0] = 1
@@ -52,10 +59,11 @@ def test_kvfill_decode_steps_against_oracle(name, T, empty_step):
         x = torch.randn((1, d), device="cuda")
         out = Bd.dv_sparse_attn_kvfill(attn, x, kv, Y, valid, torch.tensor(sets[s], device="cuda"), scale)
         torch.cuda.synchronize()
-        ref, Ko, Vo, Yo, vo = O.mha_sparse_kvfill(host(x)[0], a, Ko, Vo, Yo, vo, pos, sets[s], scale)
+        ref, Ko, Vo, Yo, vo = O.mha_sparse_kvfill(host(x)[0], a, Ko, Vo, Yo, vo, pos, sets[s], scale,
+                                                  y_keep=_keep(Y))
         assert rel_l2(host(out)[0], ref) < REL_TOL, (s, rel_l2(host(out)[0], ref))
         assert np.array_equal(host(valid).astype(bool), vo), s
-        assert np.array_equal(host(Y)[pos], host(x)[0])
+        assert np.array_equal(host(Y)[pos].astype(np.float64), Yo[pos])   # rounded to nearest even
         Kg, Vg = host(t["K"])[0], host(t["V"])[0]
         for h in sets[s]:
             assert rel_l2(Kg[h, :pos + 1].astype(np.float64), Ko[h, :pos + 1]) < REL_TOL, (s, h)
@@ -74,7 +82,7 @@ def test_kvfill_equals_a_cache_with_every_head_written():
     K2, V2 = t["K"].clone(), t["V"].clone()
     kv = Bd.KVCache(t["K"], t["V"], [p0])
     kv2 = Bd.KVCache(K2, V2, [p0])
-    Y = torch.zeros((cap, d), dtype=torch.float32, device="cuda")
+    Y = torch.zeros((cap, d), dtype=t["K"].dtype, device="cuda")
     valid = torch.zeros((H, cap), dtype=torch.uint8, device="cuda")
     valid[:, :p0] = 1
     rng = np.random.default_rng(131)
@@ -92,18 +100,22 @@ def test_kvfill_equals_a_cache_with_every_head_written():
         assert rel_l2(host(out)[0], host(ref)[0]) < REL_TOL, s
 
 
-@pytest.mark.parametrize("name,M", [("small_f16", 70), ("opt175b_b1", 150)])
-def test_kvfill_heads_missing_many_positions(name, M):
+@pytest.mark.parametrize("name,M,wd,kvd", [("small_f16", 70, None, None), ("opt175b_b1", 150, None, None),
+                                           ("small_f16", 40, "f16", "f32"), ("small_f16", 40, "f32", "f16")])
+def test_kvfill_heads_missing_many_positions(name, M, wd, kvd):
     """Selected heads missing far more positions than one workgroup slice takes per
     group (4 positions x 4 slices), some contiguous and some scattered: every slice
-    runs several groups, and the filled rows and the output match the oracle."""
+    runs several groups, and the filled rows and the output match the oracle. Also
+    with mixed weight and cache types (the kept inputs follow the cache's type)."""
     cfg = get_config(name)
+    if wd is not None:
+        cfg = cfg.with_(name=f"{name}_{wd}_{kvd}", wdtype=wd, kvdtype=kvd)
     t = make_layer(cfg, 140, device="cuda", biases=True)
     attn = Bd.Attn(t["Wq"], t["Wk"], t["Wv"], t["WoT"], cfg.H, t["bq"], t["bk"], t["bv"], t["bo"])
     cap, d, H = cfg.kv_cap, cfg.d, cfg.H
     pos = cap - 1
     kv = Bd.KVCache(t["K"], t["V"], [pos])
-    Y = torch.zeros((cap, d), dtype=torch.float32, device="cuda")
+    Y = torch.zeros((cap, d), dtype=t["K"].dtype, device="cuda")
     Y[:pos] = torch.randn((pos, d), device="cuda")
     rng = np.random.default_rng(141)
     vh = np.ones((H, cap), dtype=np.uint8)
@@ -121,7 +133,7 @@ def test_kvfill_heads_missing_many_positions(name, M):
     x = torch.randn((1, d), device="cuda")
     out = Bd.dv_sparse_attn_kvfill(attn, x, kv, Y, valid, torch.tensor(S, device="cuda"), scale)
     torch.cuda.synchronize()
-    ref, Ko, Vo, Yo, vo = O.mha_sparse_kvfill(host(x)[0], a, Ko, Vo, Yo, vo, pos, S, scale)
+    ref, Ko, Vo, Yo, vo = O.mha_sparse_kvfill(host(x)[0], a, Ko, Vo, Yo, vo, pos, S, scale, y_keep=_keep(Y))
     assert rel_l2(host(out)[0], ref) < REL_TOL
     assert np.array_equal(host(valid).astype(bool), vo)
     Kg, Vg = host(t["K"])[0], host(t["V"])[0]

@@ -197,3 +197,29 @@ def test_kvfill_only_touches_missing_rows_of_selected_heads():
     assert (Kn[4, 5] == 7.0).all() and not vn[4, 5]                  # head 4 not selected: still missing
     rows = [(h, t) for h in range(5) for t in range(6) if (h, t) != (2, 3)]
     assert all((Kn[h, t] == 7.0).all() and (Vn[h, t] == -7.0).all() for h, t in rows)
+
+
+def test_kvfill_keeps_the_input_in_the_storage_type():
+    """Reading R18: with a half-precision keep, Y[pos] is the input rounded to the
+    nearest half (ties to even, checked on values exactly between two halves), and a
+    row filled later is the projection of that rounded input, not of the exact one."""
+    rng = np.random.default_rng(43)
+    attn = _kv_layer(rng)
+    H, cap, dh, d = 5, 12, 4, 16
+    K = np.zeros((H, cap, dh))
+    V = np.zeros((H, cap, dh))
+    Y = np.zeros((cap, d))
+    valid = np.zeros((H, cap), dtype=bool)
+    y = rng.normal(size=d)
+    y[0] = 1.0 + 2.0 ** -11          # halfway between 1 and 1 + 2^-10: ties to even, 1.0
+    y[1] = 1.0 + 3.0 * 2.0 ** -11    # halfway between 1 + 2^-10 and 1 + 2^-9: ties to even, 1 + 2^-9
+    _, K, V, Y, valid = O.mha_sparse_kvfill(y, attn, K, V, Y, valid, 0, [0], 0.5, y_keep=np.float16)
+    assert Y[0, 0] == 1.0 and Y[0, 1] == 1.0 + 2.0 ** -9
+    assert np.array_equal(Y[0], y.astype(np.float16).astype(np.float64))
+    assert (np.abs(Y[0] - y) <= 2.0 ** -11 * np.maximum(np.abs(y), 2.0 ** -14)).all()   # half an ulp
+    # head 3 was not selected at token 0; at token 1 it is, and fills row 0 from Y[0]
+    y1 = rng.normal(size=d)
+    _, K, V, Y, valid = O.mha_sparse_kvfill(y1, attn, K, V, Y, valid, 1, [3], 0.5, y_keep=np.float16)
+    k0 = np.asarray(attn["Wk"])[12:16] @ Y[0] + attn["bk"][12:16]
+    k0_exact = np.asarray(attn["Wk"])[12:16] @ y + attn["bk"][12:16]
+    assert np.allclose(K[3, 0], k0, rtol=1e-14) and not np.allclose(K[3, 0], k0_exact, rtol=1e-9)
