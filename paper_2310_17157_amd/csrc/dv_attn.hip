@@ -346,7 +346,7 @@ hipError_t launch_attn(int kvtype, const AttnArgs& a, int B, hipStream_t st) {
 // ------------------------------------------------------------ missing keys and values
 // One workgroup of 4 wavefronts per (selected head, block of kFillRows rows of
 // [W^K_h; W^V_h], group slice). It lists the head's missing positions (valid == 0 below
-// pos); wavefront w then takes RPW of the rows (w mod kFillRows / RPW) over one of
+// pos); wavefront w then takes RPW of the rows (w mod (kFillRows / RPW)) over one of
 // kFillCols parts of the columns and, for groups of MT missing positions, walks them in
 // 16-byte chunks: the RPW weight chunks and the MT matching slices of the kept inputs
 // (L2 hits: every workgroup of the head reads the same few rows of Y) are loaded
