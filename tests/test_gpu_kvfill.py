@@ -144,3 +144,34 @@ def test_kvfill_heads_missing_many_positions(name, M, wd, kvd):
         miss = np.flatnonzero(vh[h, :pos] == 0)
         assert rel_l2(Kg[h, miss].astype(np.float64), Ko[h, miss]) < REL_TOL, h
         assert rel_l2(Vg[h, miss].astype(np.float64), Vo[h, miss]) < REL_TOL, h
+
+
+def test_kvfill_is_deterministic():
+    """The same decode steps from the same starting state, twice: outputs, filled cache
+    rows, kept inputs and marks are bitwise identical (the fill adds its column halves in
+    a fixed order, and every workgroup of a head lists its missing positions in order)."""
+    cfg = get_config("opt175b_b1")
+    t = make_layer(cfg, 150, device="cuda", biases=True)
+    attn = Bd.Attn(t["Wq"], t["Wk"], t["Wv"], t["WoT"], cfg.H, t["bq"], t["bk"], t["bv"], t["bo"])
+    cap, d, H, T = cfg.kv_cap, cfg.d, cfg.H, 6
+    p0 = cap - T
+    K0, V0 = t["K"].clone(), t["V"].clone()
+    Y0 = torch.randn((cap, d), device="cuda").to(t["K"].dtype)
+    v0 = torch.ones((H, cap), dtype=torch.uint8, device="cuda")
+    v0[:, p0:] = 0
+    v0[:, p0 - 40:p0:3] = 0                      # scattered gaps in every head
+    rng = np.random.default_rng(151)
+    sets = [torch.tensor(np.sort(rng.choice(H, cfg.k_heads, replace=False)).astype(np.int32), device="cuda")
+            for _ in range(T)]
+    xs = [torch.randn((1, d), device="cuda") for _ in range(T)]
+    runs = []
+    for _ in range(2):
+        K, V, Y, valid = K0.clone(), V0.clone(), Y0.clone(), v0.clone()
+        kv = Bd.KVCache(K, V, [p0])
+        outs = []
+        for s in range(T):
+            kv.set_pos([p0 + s])
+            outs.append(Bd.dv_sparse_attn_kvfill(attn, xs[s], kv, Y, valid, sets[s], 1.0 / np.sqrt(cfg.dh)))
+        torch.cuda.synchronize()
+        runs.append([host(o).tobytes() for o in outs] + [host(a).tobytes() for a in (K, V, Y, valid)])
+    assert runs[0] == runs[1]
