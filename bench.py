@@ -396,17 +396,24 @@ def bench_b1(args, cfg):
     b = accounting.layer_bytes(cfg)
     spread = step_spread(stream, step, args.steps)
 
-    # measured ceiling: a plain contiguous read of the block's bytes and of the step's bytes
+    # measured ceiling: a plain contiguous read of the block's bytes and of the step's bytes,
+    # and of each block kernel's own bytes (what one launch of that size can do at best)
     torch.cuda.set_stream(torch.cuda.default_stream())
-    ceil = stream_ceiling([b.block, b.total, kb[dom]], args.steps)
+    sizes = [b.block, b.total, kb[dom]] + [kb[k] for k in BLOCK_KERNELS if k in kb]
+    ceil = stream_ceiling(list(dict.fromkeys(sizes)), args.steps)
     torch.cuda.set_stream(stream)
     blk_us = sum(statistics.mean(per_one[k]) * 1e3 for k in BLOCK_KERNELS if k in per_one)
     blk_gbps = b.block / (blk_us * 1e-6) / 1e9
+    floors_us = sum(ceil[str(kb[k])]["avg_launch_us"] for k in BLOCK_KERNELS if k in kb)
     block = {"kernels": list(BLOCK_KERNELS), "bytes": b.block, "us": round(blk_us, 2),
              "achieved": round(blk_gbps, 1), "frac": round(blk_gbps / PEAK_HBM_GBPS, 4),
              "target_frac": TARGET_FRAC, "met": bool(blk_gbps / PEAK_HBM_GBPS >= TARGET_FRAC),
              "stream_same_bytes_GBps": ceil[str(b.block)]["GBps"],
-             "frac_vs_measured_stream": round(blk_gbps / ceil[str(b.block)]["GBps"], 4)}
+             "frac_vs_measured_stream": round(blk_gbps / ceil[str(b.block)]["GBps"], 4),
+             # five plain reads, each of one block kernel's bytes: the best five launches can do
+             "per_kernel_stream_floors_us": round(floors_us, 2),
+             "per_kernel_floors_frac": round(b.block / (floors_us * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4),
+             "us_over_per_kernel_floors": round(blk_us / floors_us, 4)}
     roofline = {"bound": "hbm", "kernel": dom, "scope": "dominant kernel", "achieved": round(achieved, 1),
                 "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
                 "traffic": counter_traffic(cfg.name, dom),
