@@ -43,23 +43,27 @@ constexpr int kAxMaxSplit = kAttnMaxSplit;   // split-KV chunks, combined with a
 
 // HEADS selects the attention form (rows are dh-row blocks of selected heads, the
 // coefficients are combined from split-KV partials); otherwise rows are single
-// neurons with coefficients given per row.
-template <typename T, int NW, int U, bool HEADS>
+// neurons with coefficients given per row. R rows share one load instruction, each
+// read by 64 / R lanes (R = 4 for 4-bit rows, whose 16-byte chunk holds 32 columns:
+// a span stays 512 columns wide, as for fp16 rows).
+template <typename T, int NW, int U, bool HEADS, int R = 1>
 __global__ void __launch_bounds__(NW * 64) k_axpy(AxpyArgs a) {
   constexpr int NT = NW * 64;
   constexpr int E = Chunk<T>::E;
-  constexpr int SW = 64 * E;                                     // columns per span
+  constexpr int LR = 64 / R;                                     // lanes per row of a load
+  constexpr int SW = LR * E;                                     // columns per span
   extern __shared__ float smem[];
   const int rpb = a.rows_per_batch;
   float* cf = smem;                                              // [rpb] coefficients
   int* ri = reinterpret_cast<int*>(cf + rpb);                    // [rpb] row indices
   float* red = reinterpret_cast<float*>(ri + rpb);               // [NW][SW] wavefront sums
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int q = R == 1 ? 0 : lane / LR, lcol = lane - q * LR;   // row of a load, lane within the row
   const int S = gridDim.y, sp = blockIdx.y;
   const int r0 = (int)((long)sp * a.nrows / S), r1 = (int)((long)(sp + 1) * a.nrows / S);
   constexpr bool Q4 = kIsQ4<T>;
   const int nch = a.d / E;
-  const int lc = min((int)blockIdx.x * 64 + lane, nch - 1);          // this lane's chunk of a row
+  const int lc = min((int)blockIdx.x * LR + lcol, nch - 1);          // this lane's chunk of a row
   const char* Mb = static_cast<const char*>(a.M) + (size_t)lc * 16;
   const size_t rowb = Q4 ? (size_t)a.d / 2 : (size_t)a.d * sizeof(T);
   const _Float16* Sb = Q4 ? a.scales + lc : nullptr;                  // 4-bit rows: chunk scales
@@ -84,9 +88,10 @@ __global__ void __launch_bounds__(NW * 64) k_axpy(AxpyArgs a) {
       }
     }
     __syncthreads();
-    // this wavefront's rows: wave + NW * i, i < nwr; loads past the end are clamped
-    // to the last row (and weighted by zero), so every batch issues U loads
-    const int nwr = nb > wave ? (nb - wave + NW - 1) / NW : 0;
+    // this wavefront's groups of R rows: wave + NW * i, i < nwr; loads past the end are
+    // clamped to the last row (and weighted by zero), so every batch issues U loads
+    const int ng = (nb + R - 1) / R;
+    const int nwr = ng > wave ? (ng - wave + NW - 1) / NW : 0;
     struct Batch {
       u32x4 w[U];
       _Float16 s[Q4 ? U : 1];
@@ -94,7 +99,7 @@ __global__ void __launch_bounds__(NW * 64) k_axpy(AxpyArgs a) {
     auto load = [&](Batch& b, int i0) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        const int i = min(wave + NW * (i0 + u), nb - 1);
+        const int i = min((wave + NW * (i0 + u)) * R + q, nb - 1);
         b.w[u] = ld_stream(Mb + (size_t)ri[i] * rowb);
         if constexpr (Q4) b.s[u] = Sb[(size_t)ri[i] * srow];
       }
@@ -102,8 +107,8 @@ __global__ void __launch_bounds__(NW * 64) k_axpy(AxpyArgs a) {
     auto consume = [&](const Batch& b, int i0) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        const int i = i0 + u;
-        float f = i < nwr ? cf[wave + NW * i] : 0.f;
+        const int i = i0 + u, row = (wave + NW * i) * R + q;
+        float f = i < nwr && (R == 1 || row < nb) ? cf[row] : 0.f;
         if constexpr (Q4) f *= (float)b.s[u];
         float v[E];
         unpack<T>(b.w[u], v);
@@ -160,9 +165,15 @@ __global__ void __launch_bounds__(NW * 64) k_axpy(AxpyArgs a) {
     }
     __syncthreads();   // ri / cf are rewritten by the next batch
   }
-  // ---- combine wavefronts in order, then write out (one split) or partial[sp]
+  // ---- combine the R rows of a load (lanes q and q ^ 1, then q and q ^ 2, ...),
+  // then wavefronts in order, then write out (one split) or partial[sp]
 #pragma unroll
-  for (int e = 0; e < E; ++e) red[wave * SW + lane * E + e] = acc[e];
+  for (int off = LR; off < 64; off <<= 1)
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] += __shfl_xor(acc[e], off);
+  if (q == 0)
+#pragma unroll
+    for (int e = 0; e < E; ++e) red[wave * SW + lcol * E + e] = acc[e];
   __syncthreads();
   for (int t = tid; t < SW; t += NT) {
     const int col = blockIdx.x * SW + t;
@@ -230,38 +241,37 @@ __global__ void __launch_bounds__(256) k_axpy_sum(AxpyArgs a, int S) {
   if (a.out2) *reinterpret_cast<f32x4*>(a.out2 + i) = v;
 }
 
-// Row splits: enough workgroups to give every CU one, each split at least two rows
-// per wavefront; one split when there is no partial buffer.
-static int axpy_row_splits(int d, int E, int nrows) {
-  const int spans = (d / E + 63) / 64;
+// Row splits: enough workgroups to give every CU one, each split at least two groups
+// of rows per wavefront; one split when there is no partial buffer.
+static int axpy_row_splits(int spans, int nrows, int rows_per_round) {
   int S = device_cu_count() / spans;
-  S = min(S, nrows / (2 * kAxNW));
+  S = min(S, nrows / (2 * rows_per_round));
   return max(1, min(S, kAxpyMaxRowSplit));
 }
 
-template <typename T, bool HEADS, int NW = kAxNW, int U = kAxU>
+template <typename T, bool HEADS, int NW = kAxNW, int U = kAxU, int R = 1>
 static hipError_t launch_axpy_t(AxpyArgs a, hipStream_t st) {
   constexpr int E = Chunk<T>::E;
-  const int spans = (a.d / E + 63) / 64;
-  const int S = a.partial != nullptr ? axpy_row_splits(a.d, E, a.nrows) : 1;
+  constexpr int LR = 64 / R;
+  const int spans = (a.d / E + LR - 1) / LR;
+  const int S = a.partial != nullptr ? axpy_row_splits(spans, a.nrows, NW * R) : 1;
   if (spans > kAxpyMaxSpans) a.cnt = nullptr;   // no counter per span: the split sum is a launch
-  // 4-bit rows: a span is 2048 columns, too wide for one workgroup to add all its splits
-  // in its tail (each thread would wait for 8 rounds of loads); the sum is a launch
-  if (kIsQ4<T>) a.cnt = nullptr;
   // LDS: (coefficient, row index) pairs of a batch of the split's rows and the
   // wavefront sums.
   const int rpb = min(kAxRowsLds, max(1, (a.nrows + S - 1) / S));
   a.rows_per_batch = rpb;
-  const size_t lds = (size_t)rpb * 8 + (size_t)NW * 64 * E * 4;
-  launch_k((k_axpy<T, NW, U, HEADS>), dim3(spans, S), dim3(NW * 64), lds, st, a);
+  const size_t lds = (size_t)rpb * 8 + (size_t)NW * LR * E * 4;
+  launch_k((k_axpy<T, NW, U, HEADS, R>), dim3(spans, S), dim3(NW * 64), lds, st, a);
   if (S > 1 && a.cnt == nullptr) launch_k(k_axpy_sum, dim3((a.d / 4 + 255) / 256), dim3(256), 0, st, a, S);
   return hipGetLastError();
 }
 
 hipError_t launch_axpy(int wtype, const AxpyArgs& a, hipStream_t st) {
-  // 4-bit rows: 32 columns per lane, so four wavefronts (their 2048-column sums fit in
-  // 32 KB of LDS) with batches of 4 rows
-  if (wtype == DV_Q4) return a.dh > 0 ? hipErrorInvalidValue : launch_axpy_t<q4_t, false, 4, 4>(a, st);
+  // 4-bit rows: 32 columns per lane, so a load covers 4 rows of a 512-column span;
+  // 8 wavefronts with batches of 2 loads (19.0 -> 13.9-14.4 us at the OPT-175B set
+  // against the 2048-column spans of one row per load with a separate split-sum
+  // launch; batches of 4 and 8, and 4 wavefronts, were slower)
+  if (wtype == DV_Q4) return a.dh > 0 ? hipErrorInvalidValue : launch_axpy_t<q4_t, false, 8, 2, 4>(a, st);
   if (a.dh > 0)
     return wtype == DV_F16 ? launch_axpy_t<_Float16, true>(a, st) : launch_axpy_t<float, true>(a, st);
   return wtype == DV_F16 ? launch_axpy_t<_Float16, false>(a, st) : launch_axpy_t<float, false>(a, st);

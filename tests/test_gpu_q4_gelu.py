@@ -56,6 +56,20 @@ def test_q4_empty_set_is_bias_and_determinism():
     assert torch.equal(a, b)
 
 
+def test_q4_full_size_is_deterministic():
+    """The OPT-175B set: ten row splits per 512-column span, added by the last split to
+    arrive; two calls agree bit for bit."""
+    P1, S1, P2, S2, b1, b2 = _q4_layer(12288, 49152, 151)
+    m = Bd.MLPQ4(P1, S1, P2, S2, b1, b2)
+    x = torch.randn((1, 12288), device="cuda")
+    rng = np.random.default_rng(152)
+    idx = torch.tensor(np.sort(rng.choice(49152, 2457, replace=False)).astype(np.int32), device="cuda")
+    a = Bd.dv_sparse_mlp_q4(m, x, idx).clone()
+    b = Bd.dv_sparse_mlp_q4(m, x, idx)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
 @pytest.mark.parametrize("name", ["small_f16", "small_f32", "opt175b_b1"])
 def test_gelu_sparse_mlp(name):
     cfg = get_config(name)
