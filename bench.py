@@ -20,6 +20,7 @@ events stamped by its launches' own dispatches on the library's stream, and the 
 oracle timed on this host's cores on a bounded sample.
 """
 import argparse
+import collections
 import json
 import os
 import statistics
@@ -680,33 +681,41 @@ def kvfill_steps(cfg, t, stream, scale, T=32):
     out = torch.empty((1, d), dtype=torch.float32, device="cuda")
     x = torch.randn((1, d), device="cuda")
     res = {}
-    for key in ("kvfill", "plain"):
+    # the per-token times come from passes without launch events (each timed launch
+    # leaves the GPU idle for a few microseconds); a third pass times the fill's launches
+    for key in ("kvfill", "plain", "launches"):
         valid[:, p0:] = 0
         valid[:, :p0] = 1
-        tm = [Bd.LaunchTimer(8, only="kv_fill") for _ in range(T)] if key == "kvfill" else None
+        tm = [Bd.LaunchTimer(8) for _ in range(T)] if key == "launches" else None
         torch.cuda.synchronize()
         ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         ev0.record(stream)
         for s_ in range(T):
             kv.set_pos([p0 + s_])
-            if key == "kvfill":
-                tm[s_].arm()
-                Bd.dv_sparse_attn_kvfill(attn, x, kv, Y, valid, sets[s_], scale, out=out, ws=ws, stream=stream)
-                tm[s_].disarm()
-            else:
+            if key == "plain":
                 Bd.dv_sparse_attn(attn, x, kv, sets[s_].view(1, -1), scale, out=out, ws=ws, stream=stream)
+                continue
+            if tm:
+                tm[s_].arm()
+            Bd.dv_sparse_attn_kvfill(attn, x, kv, Y, valid, sets[s_], scale, out=out, ws=ws, stream=stream)
+            if tm:
+                tm[s_].disarm()
         ev1.record(stream)
         torch.cuda.synchronize()
         res[key] = ev0.elapsed_time(ev1) * 1e3 / T
         if tm:
-            fill = [ms for tmr in tm for _, ms in tmr.times_ms()]
+            per = collections.defaultdict(list)
             for tmr in tm:
+                for lab, ms in tmr.times_ms():
+                    per[lab].append(ms * 1e3)
                 tmr.close()
-            res["fill_launch_us"] = round(statistics.mean(fill) * 1e3, 2)
+            res["fill_launch_us"] = round(statistics.mean(per["kv_fill"]), 2)
+            res["qkv_launch_us"] = round(statistics.mean(per["qkv"]), 2)
     kv.set_pos([cap - 1])
     return {"tokens": T, "k_heads": cfg.k_heads, "heads": H, "missing_rows_filled_per_token": round(statistics.mean(
             filled[1:]), 2), "us_per_token_kvfill": round(res["kvfill"], 2),
-            "us_per_token_without_fill": round(res["plain"], 2), "fill_launch_us": res["fill_launch_us"]}
+            "us_per_token_without_fill": round(res["plain"], 2), "fill_launch_us": res["fill_launch_us"],
+            "qkv_launch_us": res["qkv_launch_us"]}
 
 
 def cpu_baseline_b32(cfg, th, heads, sets, pos):

@@ -442,9 +442,17 @@ extern "C" dv_status dv_sparse_attn_kvfill(const dv_attn* a, const float* x, con
   f.d = a->d; f.H = a->H; f.dh = a->dh; f.cap = kv->cap; f.pos = pos; f.n_heads = n_heads;
   f.x = x; f.Y = Y; f.valid = valid; f.heads = heads;
   f.Wk = a->Wk; f.Wv = a->Wv; f.bk = a->bk; f.bv = a->bv; f.K = kv->K; f.V = kv->V;
-  if (n_heads > 0) {
+  // The missing positions are listed by a workgroup hosted in the QKV launch, into the
+  // row-axpy partial buffer of the workspace (unused until the out-projection), when they
+  // fit; the fill then runs after QKV. Otherwise every fill workgroup lists its head's
+  // positions itself, in a fill before QKV.
+  const int stride = max(pos, 1);
+  const bool listed =
+      n_heads > 0 && (size_t)n_heads * (stride + 1) <= axpy_partial_bytes(a->d) / sizeof(int32_t);
+  int32_t* list = listed ? reinterpret_cast<int32_t*>(o.axp) : nullptr;
+  if (n_heads > 0 && !listed) {
     DV_LAUNCH("kv_fill", hs, launch_kv_fill(a->wtype, kv->ktype, f, hs));
-  } else {   // no head selected: nothing to compute, the input is still kept
+  } else if (n_heads == 0) {   // no head selected: nothing to compute, the input is still kept
     DV_LAUNCH("kv_keep", hs, launch_keep_input(kv->ktype, f, hs));
   }
   QkvArgs q{};
@@ -453,7 +461,11 @@ extern "C" dv_status dv_sparse_attn_kvfill(const dv_attn* a, const float* x, con
   q.Wq = a->Wq; q.Wk = a->Wk; q.Wv = a->Wv; q.bq = a->bq; q.bk = a->bk; q.bv = a->bv;
   q.K = kv->K; q.V = kv->V; q.q = o.q; q.heads_in = heads; q.heads_ws = o.heads;
   q.clear = o.axc; q.clear_n = kAxpyMaxSpans; q.valid = valid;
+  if (listed) {
+    q.list = list; q.list_stride = stride; q.list_count = list + (size_t)n_heads * stride;
+  }
   DV_LAUNCH("qkv", hs, launch_qkv(a->wtype, kv->ktype, q, hs));   // also marks row pos of every head
+  if (listed) DV_LAUNCH("kv_fill", hs, launch_kv_fill_listed(a->wtype, kv->ktype, f, list, stride, hs));
   if (n_heads == 0) {
     AxpyArgs ax{};
     ax.d = a->d; ax.nrows = 0; ax.M = a->WoT; ax.m_rows = a->H * a->dh; ax.set = o.heads; ax.dh = 0;

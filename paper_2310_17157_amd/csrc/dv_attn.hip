@@ -17,14 +17,80 @@
 
 namespace dv {
 
+// ------------------------------------------------ missing positions of a head (Section 4.2)
+// Threads per listing and positions each thread takes per round.
+constexpr int kFillNT = 256, kFillPre = 8;
+
+// The positions below pos whose mark in vh is 0, in ascending order, into out[0..m)
+// (when write); returns m. kFillNT threads of the workgroup (lt: their index among
+// them) take kFillPre consecutive positions each per round, and a prefix sum over them
+// places the positions (wtot: kFillNT / kWave ints of LDS). It holds workgroup barriers:
+// every thread of the workgroup calls it, the same number of times.
+__device__ __forceinline__ int list_missing(const uint8_t* vh, int pos, int* out, int* wtot, int lt, bool write) {
+  constexpr int NW = kFillNT / kWave;
+  const int wave = lt >> 6, lane = lt & 63;
+  int m = 0;
+  for (int c0 = 0; c0 < pos; c0 += kFillNT * kFillPre) {
+    const int tb = c0 + lt * kFillPre;
+    uint8_t mk[kFillPre];
+#pragma unroll
+    for (int k = 0; k < kFillPre; ++k) mk[k] = vh[min(tb + k, pos - 1)];
+    int cnt = 0;
+#pragma unroll
+    for (int k = 0; k < kFillPre; ++k) cnt += (tb + k < pos && mk[k] == 0) ? 1 : 0;
+    int incl = cnt;                                   // inclusive scan within the wavefront
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int v = __shfl_up(incl, o, kWave);
+      if (lane >= o) incl += v;
+    }
+    if (lane == kWave - 1) wtot[wave] = incl;
+    __syncthreads();
+    int off = m + incl - cnt, tot = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      off += w < wave ? wtot[w] : 0;
+      tot += wtot[w];
+    }
+    if (write) {
+#pragma unroll
+      for (int k = 0; k < kFillPre; ++k)
+        if (tb + k < pos && mk[k] == 0) out[off++] = tb + k;
+    }
+    m += tot;
+    __syncthreads();                                  // wtot is rewritten by the next round
+  }
+  return m;
+}
+
+// The listing for the missing-KV fill hosted beside the QKV stream by one workgroup of
+// NT threads: its NT / kFillNT parts list one selected head each per round.
+template <int NT>
+__device__ __forceinline__ void hosted_list(const QkvArgs& a) {
+  constexpr int NQ = NT / kFillNT;
+  __shared__ int wtot[NT / kWave];
+  const int qp = (int)threadIdx.x / kFillNT, lt = (int)threadIdx.x - qp * kFillNT;
+  for (int j0 = 0; j0 < a.n_heads; j0 += NQ) {
+    const int j = j0 + qp, jj = min(j, a.n_heads - 1);
+    const int head = min(max(a.heads_in[jj], 0), a.H - 1);
+    const int m = list_missing(a.valid + (size_t)head * a.cap, a.pos, a.list + (size_t)jj * a.list_stride,
+                               wtot + qp * (kFillNT / kWave), lt, j < a.n_heads);
+    if (j < a.n_heads && lt == 0) a.list_count[j] = m;
+  }
+}
+
 template <typename T, typename KT, int NW, int U, int KX, bool LN>
 __global__ void __launch_bounds__(NW * 64) k_qkv(QkvArgs a) {
   extern __shared__ float smem[];
   constexpr int NT = NW * 64;
-  const int wg = blockIdx.x, nwg = gridDim.x - (a.sel_n > 0 ? 1 : 0);
+  const bool host = a.sel_n > 0 || a.list != nullptr;
+  const int wg = blockIdx.x, nwg = gridDim.x - (host ? 1 : 0);
   clear_counters(a.clear, a.clear_n);
-  if (a.sel_n > 0 && wg == nwg) {
-    hosted_select<NT>(a.sel_scores, a.sel_n, a.sel_k, a.sel_idx, a.sel_idx_out, smem);
+  if (host && wg == nwg) {
+    if (a.sel_n > 0)
+      hosted_select<NT>(a.sel_scores, a.sel_n, a.sel_k, a.sel_idx, a.sel_idx_out, smem);
+    else
+      hosted_list<NT>(a);
     return;
   }
   float* xs = smem;
@@ -95,11 +161,12 @@ static hipError_t launch_qkv_t(const QkvArgs& a, hipStream_t st) {
   // One workgroup per CU, each a contiguous range of rows (rowdot_flat). A hosted
   // selection gets one more workgroup, and a few CUs are left free for it to start at once.
   const int cus = device_cu_count();
-  const int blocks = max(1, min(nrows, a.sel_n > 0 ? max(1, cus - kQkvSelFreeCUs) : cus));
+  const bool host = a.sel_n > 0 || a.list != nullptr;
+  const int blocks = max(1, min(nrows, host ? max(1, cus - kQkvSelFreeCUs) : cus));
   size_t lds = (size_t)(a.d + NW) * sizeof(float) + (size_t)a.n_heads * sizeof(int32_t) +
                (size_t)rowdot_flat_part(nrows, blocks, NW) * sizeof(float) + 16;
   if (a.sel_n > 0) lds = max(lds, (size_t)kSelBins * 4 + kSelSm(NT) * sizeof(int));
-  const dim3 grid(blocks + (a.sel_n > 0 ? 1 : 0));
+  const dim3 grid(blocks + (host ? 1 : 0));
   if (a.g != nullptr) {
     const hipError_t e = ensure_dyn_lds(reinterpret_cast<const void*>(k_qkv<T, KT, NW, U, KX, true>), lds);
     if (e != hipSuccess) return e;
@@ -362,7 +429,10 @@ hipError_t launch_attn(int kvtype, const AttnArgs& a, int B, hipStream_t st) {
 // 70-71 us per fill with 16 rows over all columns per workgroup and no slices, 55-57 us
 // with the slices and that prologue, 51 us with two column parts (four: 64 us, the
 // listing repeated by four times the workgroups), 44 us with the kept inputs in fp16.
-constexpr int kFillRows = 8, kFillCols = 2, kFillSlices = 4, kFillPre = 8, kFillNT = 256;
+constexpr int kFillRows = 8, kFillCols = 2, kFillSlices = 4;
+// The listed fill: rows per wavefront of a work item (items of 2 * kFillListedRPW rows)
+// and workgroups per CU of its resident grid (its launch bound).
+constexpr int kFillListedRPW = 2, kFillResident = 5;
 
 typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
 
@@ -400,71 +470,43 @@ template <> struct Kept<_Float16, 4> {
   __device__ __forceinline__ float at(int e) const { return (float)v[e]; }
 };
 
-template <typename T, typename KT, int RPW, int MT>
-__global__ void __launch_bounds__(kFillNT, 3) k_kv_fill(KvFillArgs a) {
-  constexpr int E = Chunk<T>::E;
-  constexpr int NW = kFillNT / kWave;
-  constexpr int NRW = kFillRows / RPW;               // wavefronts per column part
-  static_assert(NW == kFillCols * NRW, "the row block's wavefronts cover its column parts");
-  extern __shared__ int flist[];
-  __shared__ int wtot[NW];
-  __shared__ float part[kFillCols - 1][NRW][RPW][MT];
-  const int nrb = (2 * a.dh + kFillRows - 1) / kFillRows;
-  const int j = blockIdx.x / nrb, rb = blockIdx.x - j * nrb;
-  const int head = min(max(a.heads[j], 0), a.H - 1);
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int rw = wave % NRW, cp = wave / NRW;
-  if (blockIdx.x == 0 && blockIdx.y == 0) {   // keep this token's input: Y[pos] = x
-    const int n4 = a.d >> 2;                    // (x, Y 16-byte aligned, d % 4 == 0)
-    const f32x4* src = reinterpret_cast<const f32x4*>(a.x);
-    KT* dst = static_cast<KT*>(a.Y) + (size_t)a.pos * a.d;
-    for (int i0 = threadIdx.x; i0 < n4; i0 += kFillNT * kFillPre) {
-      f32x4 v[kFillPre];
+// This token's input kept in the cache's type (Y[pos] = x), by one workgroup of kFillNT.
+template <typename KT>
+__device__ __forceinline__ void keep_input_wg(const KvFillArgs& a) {
+  const int n4 = a.d >> 2;                    // (x, Y 16-byte aligned, d % 4 == 0)
+  const f32x4* src = reinterpret_cast<const f32x4*>(a.x);
+  KT* dst = static_cast<KT*>(a.Y) + (size_t)a.pos * a.d;
+  for (int i0 = threadIdx.x; i0 < n4; i0 += kFillNT * kFillPre) {
+    f32x4 v[kFillPre];
 #pragma unroll
-      for (int k = 0; k < kFillPre; ++k) v[k] = src[min(i0 + kFillNT * k, n4 - 1)];
-#pragma unroll
-      for (int k = 0; k < kFillPre; ++k)
-        if (i0 + kFillNT * k < n4) keep4(dst + 4 * (i0 + kFillNT * k), v[k]);
-    }
-  }
-  // The head's missing positions below pos, in ascending order: every workgroup of the
-  // head builds the same list, since the slices split it by index. Each thread takes
-  // kFillPre consecutive positions; a workgroup-wide prefix sum of their counts places them.
-  const uint8_t* vh = a.valid + (size_t)head * a.cap;
-  int m = 0;
-  for (int c0 = 0; c0 < a.pos; c0 += kFillNT * kFillPre) {
-    const int tb = c0 + (int)threadIdx.x * kFillPre;
-    uint8_t mk[kFillPre];
-#pragma unroll
-    for (int k = 0; k < kFillPre; ++k) mk[k] = vh[min(tb + k, a.pos - 1)];
-    int cnt = 0;
-#pragma unroll
-    for (int k = 0; k < kFillPre; ++k) cnt += (tb + k < a.pos && mk[k] == 0) ? 1 : 0;
-    int incl = cnt;                                   // inclusive scan within the wavefront
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-      const int v = __shfl_up(incl, o, kWave);
-      if (lane >= o) incl += v;
-    }
-    if (lane == kWave - 1) wtot[wave] = incl;
-    __syncthreads();
-    int off = m + incl - cnt, tot = 0;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) {
-      off += w < wave ? wtot[w] : 0;
-      tot += wtot[w];
-    }
+    for (int k = 0; k < kFillPre; ++k) v[k] = src[min(i0 + kFillNT * k, n4 - 1)];
 #pragma unroll
     for (int k = 0; k < kFillPre; ++k)
-      if (tb + k < a.pos && mk[k] == 0) flist[off++] = tb + k;
-    m += tot;
-    __syncthreads();                                  // wtot is rewritten by the next round
+      if (i0 + kFillNT * k < n4) keep4(dst + 4 * (i0 + kFillNT * k), v[k]);
   }
-  if (m == 0) return;
+}
+
+// One group of the fill: the keys and values of head `head` at the missing positions
+// plist[t0 .. t0 + MT) (clamped to m) for the block rb of NRW * RPW rows of
+// [W^K_h; W^V_h]. Wavefront w takes RPW rows (w mod NRW) over one of kFillCols parts of
+// the columns, walking them in 16-byte chunks with the RPW weight chunks and the MT
+// matching slices of the kept inputs loaded together, two steps in flight (indices
+// clamped, so no load is predicated); the other parts' sums are added to the first's
+// through LDS (part: [kFillCols - 1][NRW][RPW][MT] floats), in part order.
+template <typename T, typename KT, int RPW, int MT>
+__device__ __forceinline__ void fill_group(const KvFillArgs& a, int head, int rb, const int* plist, int t0, int m,
+                                           float* part) {
+  constexpr int E = Chunk<T>::E;
+  constexpr int NW = kFillNT / kWave;
+  constexpr int NRW = NW / kFillCols;                // wavefronts per column part
+  constexpr int RB = NRW * RPW;                      // rows of the block
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int rw = wave % NRW, cp = wave / NRW;
+  auto pidx = [&](int q, int r, int u) { return ((q * NRW + rw) * RPW + r) * MT + u; };
   const int nch = a.d / E, nit = (nch + 63) / 64;
   const int it_b = (int)((long)cp * nit / kFillCols), it_e = (int)((long)(cp + 1) * nit / kFillCols);
   // this wavefront's rows (clamped into the block; duplicates are not written)
-  const int r0 = rb * kFillRows + rw * RPW, rend = min(2 * a.dh, (rb + 1) * kFillRows);
+  const int r0 = rb * RB + rw * RPW, rend = min(2 * a.dh, (rb + 1) * RB);
   const T* W[RPW];
 #pragma unroll
   for (int r = 0; r < RPW; ++r) {
@@ -472,90 +514,157 @@ __global__ void __launch_bounds__(kFillNT, 3) k_kv_fill(KvFillArgs a) {
     const bool isv = rr >= a.dh;
     W[r] = static_cast<const T*>(isv ? a.Wv : a.Wk) + ((size_t)head * a.dh + (isv ? rr - a.dh : rr)) * a.d;
   }
-  for (int t0 = (int)blockIdx.y * MT; t0 < m; t0 += MT * (int)gridDim.y) {
-    const KT* Yp[MT];
+  int pp[MT];
 #pragma unroll
-    for (int u = 0; u < MT; ++u) Yp[u] = static_cast<const KT*>(a.Y) + (size_t)flist[min(t0 + u, m - 1)] * a.d;
-    float acc[RPW][MT];
+  for (int u = 0; u < MT; ++u) pp[u] = plist[min(t0 + u, m - 1)];
+  const KT* Yp[MT];
 #pragma unroll
-    for (int r = 0; r < RPW; ++r)
+  for (int u = 0; u < MT; ++u) Yp[u] = static_cast<const KT*>(a.Y) + (size_t)pp[u] * a.d;
+  float acc[RPW][MT];
 #pragma unroll
-      for (int u = 0; u < MT; ++u) acc[r][u] = 0.f;
-    struct Step {
-      u32x4 w[RPW];
-      Kept<KT, E> y[MT];
-    };
-    auto load = [&](Step& st, int it) {
-      const int c = min(it * 64 + lane, nch - 1);
+  for (int r = 0; r < RPW; ++r)
 #pragma unroll
-      for (int r = 0; r < RPW; ++r) st.w[r] = ld_stream(W[r] + (size_t)c * E);
+    for (int u = 0; u < MT; ++u) acc[r][u] = 0.f;
+  struct Step {
+    u32x4 w[RPW];
+    Kept<KT, E> y[MT];
+  };
+  auto load = [&](Step& st, int it) {
+    const int c = min(it * 64 + lane, nch - 1);
 #pragma unroll
-      for (int u = 0; u < MT; ++u) st.y[u].load(Yp[u] + (size_t)c * E);
-    };
-    auto use = [&](const Step& st, int it) {
-      if (it * 64 + lane >= nch) return;
+    for (int r = 0; r < RPW; ++r) st.w[r] = ld_stream(W[r] + (size_t)c * E);
 #pragma unroll
-      for (int r = 0; r < RPW; ++r) {
-        float wv[E];
-        unpack<T>(st.w[r], wv);
+    for (int u = 0; u < MT; ++u) st.y[u].load(Yp[u] + (size_t)c * E);
+  };
+  auto use = [&](const Step& st, int it) {
+    if (it * 64 + lane >= nch) return;
 #pragma unroll
-        for (int u = 0; u < MT; ++u)
+    for (int r = 0; r < RPW; ++r) {
+      float wv[E];
+      unpack<T>(st.w[r], wv);
 #pragma unroll
-          for (int e = 0; e < E; ++e) acc[r][u] = fmaf(wv[e], st.y[u].at(e), acc[r][u]);
-      }
-    };
-    // two steps in flight: the next step's loads go out before this step is used
-    if (it_b < it_e) {
-      Step sa, sb;
-      load(sa, it_b);
-      for (int it = it_b; it < it_e;) {
-        load(sb, min(it + 1, it_e - 1));
-        use(sa, it);
-        if (++it >= it_e) break;
-        load(sa, min(it + 1, it_e - 1));
-        use(sb, it);
-        ++it;
-      }
+      for (int u = 0; u < MT; ++u)
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[r][u] = fmaf(wv[e], st.y[u].at(e), acc[r][u]);
     }
-    // every part reduces its lanes before the barrier (after it, the first part's
-    // reductions would lengthen every group's tail: 53.6-55.1 against 50.9-51.4 us per fill)
+  };
+  // two steps in flight: the next step's loads go out before this step is used
+  if (it_b < it_e) {
+    Step sa, sb;
+    load(sa, it_b);
+    for (int it = it_b; it < it_e;) {
+      load(sb, min(it + 1, it_e - 1));
+      use(sa, it);
+      if (++it >= it_e) break;
+      load(sa, min(it + 1, it_e - 1));
+      use(sb, it);
+      ++it;
+    }
+  }
+  // every part reduces its lanes before the barrier (after it, the first part's
+  // reductions would lengthen every group's tail: 53.6-55.1 against 50.9-51.4 us per fill)
 #pragma unroll
-    for (int r = 0; r < RPW; ++r)
+  for (int r = 0; r < RPW; ++r)
+#pragma unroll
+    for (int u = 0; u < MT; ++u) {
+      acc[r][u] = wave_sum(acc[r][u]);
+      if (cp > 0 && lane == 0) part[pidx(cp - 1, r, u)] = acc[r][u];
+    }
+  __syncthreads();
+  if (cp == 0) {
+#pragma unroll
+    for (int r = 0; r < RPW; ++r) {
+      const int rr = r0 + r;
+      const bool isv = rr >= a.dh;
+      const int tr = isv ? rr - a.dh : rr;
+      const float* bias = isv ? a.bv : a.bk;
+      const float bb = (bias != nullptr && rr < rend) ? bias[(size_t)head * a.dh + tr] : 0.f;
 #pragma unroll
       for (int u = 0; u < MT; ++u) {
-        acc[r][u] = wave_sum(acc[r][u]);
-        if (cp > 0 && lane == 0) part[cp - 1][rw][r][u] = acc[r][u];
-      }
-    __syncthreads();
-    if (cp == 0) {
+        float v = acc[r][u];
 #pragma unroll
-      for (int r = 0; r < RPW; ++r) {
-        const int rr = r0 + r;
-        const bool isv = rr >= a.dh;
-        const int tr = isv ? rr - a.dh : rr;
-        const float* bias = isv ? a.bv : a.bk;
-        const float bb = (bias != nullptr && rr < rend) ? bias[(size_t)head * a.dh + tr] : 0.f;
-#pragma unroll
-        for (int u = 0; u < MT; ++u) {
-          float v = acc[r][u];
-#pragma unroll
-          for (int q = 0; q < kFillCols - 1; ++q) v += part[q][rw][r][u];
-          if (lane == 0 && rr < rend && t0 + u < m) {
-            KT* C = static_cast<KT*>(isv ? a.V : a.K);
-            C[((size_t)head * a.cap + flist[t0 + u]) * a.dh + tr] = (KT)(v + bb);
-          }
+        for (int q = 0; q < kFillCols - 1; ++q) v += part[pidx(q, r, u)];
+        if (lane == 0 && rr < rend && t0 + u < m) {
+          KT* C = static_cast<KT*>(isv ? a.V : a.K);
+          C[((size_t)head * a.cap + pp[u]) * a.dh + tr] = (KT)(v + bb);
         }
       }
     }
-    __syncthreads();                                  // part is rewritten by the next group
+  }
+  __syncthreads();                                    // part is rewritten by the next group
+}
+
+// Without a list buffer: one workgroup per (selected head, block of rows, group slice)
+// lists its head's missing positions in LDS itself, the slices dealing the head's
+// groups of MT positions round-robin.
+template <typename T, typename KT, int RPW, int MT>
+__global__ void __launch_bounds__(kFillNT, 3) k_kv_fill(KvFillArgs a) {
+  constexpr int NW = kFillNT / kWave;
+  constexpr int NRW = NW / kFillCols;
+  extern __shared__ int flist[];
+  __shared__ int wtot[NW];
+  __shared__ float part[(kFillCols - 1) * NRW * RPW * MT];
+  const int RB = NRW * RPW;
+  const int nrb = (2 * a.dh + RB - 1) / RB;
+  const int j = blockIdx.x / nrb, rb = blockIdx.x - j * nrb;
+  const int head = min(max(a.heads[j], 0), a.H - 1);
+  if (blockIdx.x == 0 && blockIdx.y == 0) keep_input_wg<KT>(a);
+  const int m = list_missing(a.valid + (size_t)head * a.cap, a.pos, flist, wtot, (int)threadIdx.x, true);
+  for (int t0 = (int)blockIdx.y * MT; t0 < m; t0 += MT * (int)gridDim.y)
+    fill_group<T, KT, RPW, MT>(a, head, rb, flist, t0, m, part);
+}
+
+// The listed fill (the QKV launch listed each selected head's missing positions in
+// list[j * stride ..] and their count in count[j]; workgroup 0 keeps this token's
+// input): the work items (head with missing positions, block of NRW * RPW
+// rows, group of MT positions) are numbered head by head, and a resident grid deals
+// them round-robin, so every CU streams a near-equal share of the weight rows however
+// the missing positions fall on the heads (a grid per head and block leaves heads
+// without missing positions idle and the rest unevenly placed on the CUs).
+template <typename T, typename KT, int RPW, int MT>
+__global__ void __launch_bounds__(kFillNT, kFillResident) k_kv_fill_listed(KvFillArgs a, const int32_t* list, int stride,
+                                                               const int32_t* count) {
+  constexpr int NW = kFillNT / kWave;
+  constexpr int NRW = NW / kFillCols;
+  extern __shared__ int first[];                       // [n_heads + 1] first item of each head
+  __shared__ float part[(kFillCols - 1) * NRW * RPW * MT];
+  const int RB = NRW * RPW;
+  const int nrb = (2 * a.dh + RB - 1) / RB;
+  if (blockIdx.x == 0) keep_input_wg<KT>(a);
+  if (threadIdx.x == 0) {
+    int n = 0;
+    for (int j = 0; j < a.n_heads; ++j) {
+      first[j] = n;
+      n += (min(max(count[j], 0), a.pos) + MT - 1) / MT * nrb;
+    }
+    first[a.n_heads] = n;
+  }
+  __syncthreads();
+  const int total = first[a.n_heads];
+  int j = 0;
+  for (int it = blockIdx.x; it < total; it += gridDim.x) {
+    while (first[j + 1] <= it) ++j;                    // items ascend, so j only moves forward
+    const int k = it - first[j], g = k / nrb, rb = k - g * nrb;
+    const int head = min(max(a.heads[j], 0), a.H - 1);
+    const int m = min(max(count[j], 0), a.pos);
+    const int* hl = list + (size_t)j * stride;
+    // a head's last group may hold fewer than MT positions (most heads miss one or two):
+    // it loads only the kept inputs it uses
+    const int left = m - g * MT;
+    if (left >= 3)
+      fill_group<T, KT, RPW, MT>(a, head, rb, hl, g * MT, m, part);
+    else if (left == 2)
+      fill_group<T, KT, RPW, 2>(a, head, rb, hl, g * MT, m, part);
+    else
+      fill_group<T, KT, RPW, 1>(a, head, rb, hl, g * MT, m, part);
   }
 }
 
 template <typename T, typename KT>
 static hipError_t launch_kv_fill_t(const KvFillArgs& a, hipStream_t st) {
+  constexpr int RPW = kFillRows / (kFillNT / kWave / kFillCols), MT = 4;
   const int nrb = (2 * a.dh + kFillRows - 1) / kFillRows;
   const size_t lds = (size_t)max(a.pos, 1) * sizeof(int);
-  constexpr int RPW = kFillRows / (kFillNT / kWave / kFillCols), MT = 4;
   const hipError_t e = ensure_dyn_lds(reinterpret_cast<const void*>(k_kv_fill<T, KT, RPW, MT>), lds);
   if (e != hipSuccess) return e;
   launch_k((k_kv_fill<T, KT, RPW, MT>), dim3(max(1, a.n_heads) * nrb, kFillSlices), dim3(kFillNT), lds, st, a);
@@ -566,6 +675,28 @@ hipError_t launch_kv_fill(int wtype, int kvtype, const KvFillArgs& a, hipStream_
   if (wtype == DV_F16)
     return kvtype == DV_F16 ? launch_kv_fill_t<_Float16, _Float16>(a, st) : launch_kv_fill_t<_Float16, float>(a, st);
   return kvtype == DV_F16 ? launch_kv_fill_t<float, _Float16>(a, st) : launch_kv_fill_t<float, float>(a, st);
+}
+
+template <typename T, typename KT>
+static hipError_t launch_kv_fill_listed_t(const KvFillArgs& a, const int32_t* list, int stride, hipStream_t st) {
+  constexpr int RPW = kFillListedRPW, MT = 4;
+  const int32_t* count = list + (size_t)a.n_heads * stride;
+  const size_t lds = (size_t)(a.n_heads + 1) * sizeof(int);
+  const hipError_t e = ensure_dyn_lds(reinterpret_cast<const void*>(k_kv_fill_listed<T, KT, RPW, MT>), lds);
+  if (e != hipSuccess) return e;
+  // resident: kFillResident workgroups per CU (the launch bound) deal the items round-robin
+  launch_k((k_kv_fill_listed<T, KT, RPW, MT>), dim3(kFillResident * device_cu_count()), dim3(kFillNT), lds, st, a,
+           list, stride, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_fill_listed(int wtype, int kvtype, const KvFillArgs& a, const int32_t* list, int stride,
+                                 hipStream_t st) {
+  if (wtype == DV_F16)
+    return kvtype == DV_F16 ? launch_kv_fill_listed_t<_Float16, _Float16>(a, list, stride, st)
+                            : launch_kv_fill_listed_t<_Float16, float>(a, list, stride, st);
+  return kvtype == DV_F16 ? launch_kv_fill_listed_t<float, _Float16>(a, list, stride, st)
+                          : launch_kv_fill_listed_t<float, float>(a, list, stride, st);
 }
 
 template <typename KT>

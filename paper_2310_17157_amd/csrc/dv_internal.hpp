@@ -388,6 +388,10 @@ struct QkvArgs {
   // layer's normalised input): hid0[j] = x-hat . AT0[j] (j < r0), likewise AT1 (r0, r1 = 0: none).
   const void* AT0; int r0; float* hid0;
   const void* AT1; int r1; float* hid1;
+  // The missing-KV fill's listing run by one extra workgroup instead (list NULL: none;
+  // not with a hosted selection): for each selected head j, the positions below pos
+  // marked 0 in valid, ascending, in list[j * list_stride ..], their count in list_count[j].
+  int32_t* list; int list_stride; int32_t* list_count;
 };
 hipError_t launch_qkv(int wtype, int kvtype, const QkvArgs& a, hipStream_t st);
 
@@ -429,6 +433,12 @@ struct KvFillArgs {
   void* K; void* V;                 // [H][cap][dh]
 };
 hipError_t launch_kv_fill(int wtype, int kvtype, const KvFillArgs& a, hipStream_t st);
+// The fill after a QKV launch that listed each selected head's missing positions
+// (ascending) in list[j * stride ..] (stride >= pos) and their count in
+// list[n_heads * stride + j]: a resident grid streams the listed heads' rows, and
+// keeps this token's input.
+hipError_t launch_kv_fill_listed(int wtype, int kvtype, const KvFillArgs& a, const int32_t* list, int stride,
+                                 hipStream_t st);
 // Y[pos] = x in the cache's type alone (no head selected, so no fill runs).
 hipError_t launch_keep_input(int kvtype, const KvFillArgs& a, hipStream_t st);
 

@@ -33,9 +33,17 @@ def _head_schedule(rng, H, k, T, starve=None):
     return sets
 
 
-@pytest.mark.parametrize("name,T,empty_step", [("small_f16", 12, 5), ("small_f32", 10, None), ("opt175b_b1", 8, None)])
+# The fill lists the missing positions into the workspace when k_heads * (pos + 1)
+# ints fit in 32 * d; at this shape (8 heads x 1600 positions > 32 x 384) every fill
+# workgroup lists its head's positions itself instead.
+UNLISTED = get_config("small_f16").with_(name="kvfill_unlisted", d=384, N=1536, H=12, dh=32, L=1600, r=32,
+                                         k_mlp=150, k_heads=8)
+
+
+@pytest.mark.parametrize("name,T,empty_step", [("small_f16", 12, 5), ("small_f32", 10, None), ("opt175b_b1", 8, None),
+                                               ("unlisted", 8, 3)])
 def test_kvfill_decode_steps_against_oracle(name, T, empty_step):
-    cfg = get_config(name)
+    cfg = UNLISTED if name == "unlisted" else get_config(name)
     t = make_layer(cfg, 120, device="cuda", biases=True)
     attn = Bd.Attn(t["Wq"], t["Wk"], t["Wv"], t["WoT"], cfg.H, t["bq"], t["bk"], t["bv"], t["bo"])
     cap, d, H = cfg.kv_cap, cfg.d, cfg.H
