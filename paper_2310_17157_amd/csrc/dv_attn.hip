@@ -5,10 +5,13 @@
 //   k_qkv   gathered row-dots: for every selected head i, the dh rows of W^Q_i, W^K_i
 //           and W^V_i (contiguous row blocks) against the staged x-hat; q goes to the
 //           workspace, k and v to cache row pos. An extra workgroup may host the
-//           neuron top-k of the look-ahead layer.
+//           neuron top-k of the look-ahead layer, or the listing of the selected
+//           heads' missing positions for the fill.
 //   k_attn  split-KV decode attention: one workgroup per (sequence, selected head,
 //           position chunk) computes the chunk's max logit, sum of exponentials and
 //           unnormalised value sum; the out-projection kernel combines the chunks.
+//   k_kv_fill_listed / k_kv_fill  the missing keys and values of the selected heads
+//           (Section 4.2), computed from the kept attention inputs.
 #include <math.h>
 
 #include "dv_internal.hpp"
@@ -411,7 +414,10 @@ hipError_t launch_attn(int kvtype, const AttnArgs& a, int B, hipStream_t st) {
 }
 
 // ------------------------------------------------------------ missing keys and values
-// One workgroup of 4 wavefronts per (selected head, block of kFillRows rows of
+// Two forms share the group body (fill_group). The listed form (the default) runs after
+// a QKV launch that listed the positions, on a resident grid of work items; the form
+// below lists in every workgroup and runs when the lists do not fit the workspace:
+// one workgroup of 4 wavefronts per (selected head, block of kFillRows rows of
 // [W^K_h; W^V_h], group slice). It lists the head's missing positions (valid == 0 below
 // pos); wavefront w then takes RPW of the rows (w mod (kFillRows / RPW)) over one of
 // kFillCols parts of the columns and, for groups of MT missing positions, walks them in
@@ -428,7 +434,8 @@ hipError_t launch_attn(int kvtype, const AttnArgs& a, int B, hipStream_t st) {
 // thread before any is used. Over 32 decode steps with about 59 missing rows each:
 // 70-71 us per fill with 16 rows over all columns per workgroup and no slices, 55-57 us
 // with the slices and that prologue, 51 us with two column parts (four: 64 us, the
-// listing repeated by four times the workgroups), 44 us with the kept inputs in fp16.
+// listing repeated by four times the workgroups), 44 us with the kept inputs in fp16;
+// the listed form, 37.5-38.3 us.
 constexpr int kFillRows = 8, kFillCols = 2, kFillSlices = 4;
 // The listed fill: rows per wavefront of a work item (items of 2 * kFillListedRPW rows)
 // and workgroups per CU of its resident grid (its launch bound).
