@@ -183,3 +183,36 @@ def test_kvfill_is_deterministic():
         torch.cuda.synchronize()
         runs.append([host(o).tobytes() for o in outs] + [host(a).tobytes() for a in (K, V, Y, valid)])
     assert runs[0] == runs[1]
+
+
+@pytest.mark.parametrize("name", ["small_f16", "opt175b_b1"])
+def test_kvfill_from_the_first_token(name):
+    """Decode from an empty cache (pos = 0, nothing valid yet) for a few tokens with
+    changing head sets: at pos 0 nothing is missing and the listing is empty; at later
+    tokens a newly selected head is missing every earlier row."""
+    cfg = get_config(name)
+    t = make_layer(cfg, 160, device="cuda", biases=True)
+    attn = Bd.Attn(t["Wq"], t["Wk"], t["Wv"], t["WoT"], cfg.H, t["bq"], t["bk"], t["bv"], t["bo"])
+    cap, d, H, T = cfg.kv_cap, cfg.d, cfg.H, 4
+    kv = Bd.KVCache(t["K"], t["V"], [0])
+    Y = torch.zeros((cap, d), dtype=t["K"].dtype, device="cuda")
+    valid = torch.zeros((H, cap), dtype=torch.uint8, device="cuda")
+    rng = np.random.default_rng(161)
+    sets = _head_schedule(rng, H, cfg.k_heads, T)
+    a = oracle_attn(t)
+    Ko, Vo = host(t["K"])[0].astype(np.float64), host(t["V"])[0].astype(np.float64)
+    Yo, vo = host(Y).astype(np.float64), host(valid).astype(bool)
+    scale = 1.0 / np.sqrt(cfg.dh)
+    for pos in range(T):
+        kv.set_pos([pos])
+        x = torch.randn((1, d), device="cuda")
+        out = Bd.dv_sparse_attn_kvfill(attn, x, kv, Y, valid, torch.tensor(sets[pos], device="cuda"), scale)
+        torch.cuda.synchronize()
+        ref, Ko, Vo, Yo, vo = O.mha_sparse_kvfill(host(x)[0], a, Ko, Vo, Yo, vo, pos, sets[pos], scale,
+                                                  y_keep=_keep(Y))
+        assert rel_l2(host(out)[0], ref) < REL_TOL, pos
+        assert np.array_equal(host(valid).astype(bool), vo), pos
+        Kg, Vg = host(t["K"])[0], host(t["V"])[0]
+        for h in sets[pos]:
+            assert rel_l2(Kg[h, :pos + 1].astype(np.float64), Ko[h, :pos + 1]) < REL_TOL, (pos, h)
+            assert rel_l2(Vg[h, :pos + 1].astype(np.float64), Vo[h, :pos + 1]) < REL_TOL, (pos, h)
